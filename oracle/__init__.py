@@ -1,0 +1,398 @@
+"""CPU oracle for the CoSpec verify-and-arbitrate step.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the package smoke check and the
+benchmark's CPU-baseline leg may import this package.  It is never a fallback
+for the GPU path and shares no code with it: the two vocabulary/weight loops are
+plain C in double precision (cospec_oracle.c, built with gcc), the rest is plain
+Python/numpy written from the paper's definitions ("Beyond the Target: From
+Imitation to Collaboration in Speculative Decoding", Section 3).
+
+Arrays are numpy: logits and hidden states are float32 arrays or uint16 arrays
+holding raw bf16 bit patterns (the dtype says which).
+
+Readings of the paper used here (each also listed with the design notes):
+  * ties in an argmax go to the lowest index;
+  * entropy is the Shannon entropy in nats of softmax(logits) over the whole
+    vocabulary; log-probabilities are reported (logp = x[token] - lse);
+  * the head g_phi is a two-layer MLP  z = w2 . relu(W1 h + b1) + b2;
+  * the threshold is strict (a = 1[pi > lambda]) and is decided in fp32, the
+    precision the GPU path takes it in; decisions with |sigma(z) - lambda| <= 1e-3
+    (in fp64) are flagged ambiguous;
+  * every mismatch decision is scored, not only those before the stop;
+  * trees: node 0 is the root; child c of p is verified by target row p and
+    scored on hidden row c; the accepted node is the deepest node whose whole
+    root path passes (match or accepted), ties to the lowest node id.
+Parity for the tree tie-break and for the head form is pinned only by these
+stated rules (no printed value in the paper covers them).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+__all__ = [
+    "F32", "BF16", "AMBIGUITY_BAND", "build", "row_stats", "element", "head_logits",
+    "policy_accept", "chain_length", "chain_tokens", "tree_select", "verify_block",
+    "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats",
+]
+
+F32, BF16 = 0, 1
+AMBIGUITY_BAND = 1e-3
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cospec_oracle.c")
+_SO = os.path.join(_HERE, "libcospec_oracle.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile the C half of the oracle with gcc (IEEE semantics, no fast-math)."""
+    tmp = _SO + ".tmp"
+    subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math", "-o", tmp,
+                    _SRC, "-lm"], check=True)
+    os.replace(tmp, _SO)
+    return _SO
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO) or os.path.getmtime(_SO) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_SO)
+        P = ctypes.c_void_p
+        I64 = ctypes.c_int64
+        lib.oracle_row_stats.restype = I64
+        lib.oracle_row_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P]
+        lib.oracle_head.restype = None
+        lib.oracle_head.argtypes = [P, ctypes.c_int, I64, P, I64, P, P, P, ctypes.c_double, I64,
+                                    I64, P]
+        _lib = lib
+    return _lib
+
+
+def _code(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return F32
+    if a.dtype == np.uint16:
+        return BF16
+    raise TypeError(f"oracle arrays are float32 or uint16 (bf16 bits), got {a.dtype}")
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def element(a: np.ndarray) -> np.ndarray:
+    """Exact float64 values of an fp32 or bf16-bit array."""
+    if a.dtype == np.float32:
+        return a.astype(np.float64)
+    return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+@dataclass
+class RowStats:
+    max: np.ndarray      # float64
+    arg: np.ndarray      # int64
+    lse: np.ndarray      # float64
+    ent: np.ndarray      # float64
+
+
+def row_stats(rows: np.ndarray) -> RowStats:
+    """max, first argmax, log-sum-exp and entropy (nats) of every row of a [..., V]
+    array (Section 3.1 greedy verification token; see cospec_oracle.c)."""
+    rows = np.ascontiguousarray(rows)
+    shape = rows.shape[:-1]
+    V = rows.shape[-1]
+    n = int(np.prod(shape)) if shape else 1
+    mx = np.empty(n, np.float64)
+    arg = np.empty(n, np.int64)
+    lse = np.empty(n, np.float64)
+    ent = np.empty(n, np.float64)
+    if n:
+        rc = _load().oracle_row_stats(_ptr(rows), _code(rows), V, n, V, _ptr(mx), _ptr(arg),
+                                      _ptr(lse), _ptr(ent))
+        if rc != 0:
+            raise ValueError(f"non-finite logit in row {-rc - 1}")
+    return RowStats(mx.reshape(shape), arg.reshape(shape), lse.reshape(shape), ent.reshape(shape))
+
+
+def head_logits(hidden: np.ndarray, rows, w1: np.ndarray, b1: Optional[np.ndarray],
+                w2: np.ndarray, b2: float) -> np.ndarray:
+    """z = w2 . relu(W1 h + b1) + b2 (Section 3.3, z_i = g_phi(h)) for hidden rows `rows`
+    of a [n, d] array, in float64."""
+    hidden = np.ascontiguousarray(hidden)
+    w1 = np.ascontiguousarray(w1)
+    w2 = np.ascontiguousarray(w2)
+    code = _code(hidden)
+    if _code(w1) != code or _code(w2) != code or (b1 is not None and _code(b1) != code):
+        raise TypeError("hidden states and head weights must share one dtype")
+    hdim, d = w1.shape
+    assert hidden.shape[-1] == d and w2.shape == (hdim,)
+    rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    n_hidden = int(np.prod(hidden.shape[:-1]))
+    if rows.size and (rows.min() < 0 or rows.max() >= n_hidden):
+        raise IndexError("hidden row index out of range")
+    b1c = None if b1 is None else np.ascontiguousarray(b1)
+    out = np.empty(rows.size, np.float64)
+    if rows.size:
+        _load().oracle_head(_ptr(hidden), code, d, _ptr(rows), rows.size, _ptr(w1),
+                            None if b1c is None else _ptr(b1c), _ptr(w2), float(b2), d, hdim,
+                            _ptr(out))
+    return out
+
+
+def policy_accept(z: np.ndarray, lam: float):
+    """pi = sigma(z) (Eq. policy-prob) and a = 1[pi > lambda] (Eq. infer_thre).
+
+    The decision is taken in fp32 (z rounded to fp32, sigma in fp32, compared with
+    lambda as fp32), the precision the GPU takes it in; pi is also returned in
+    fp64 with the flag |pi - lambda| <= 1e-3 marking decisions too close to call.
+    """
+    z = np.asarray(z, dtype=np.float64)
+    lam32 = np.float32(lam)
+    with np.errstate(over="ignore"):
+        z32 = z.astype(np.float32)
+        pi32 = np.float32(1.0) / (np.float32(1.0) + np.exp(-z32))
+        pi = 1.0 / (1.0 + np.exp(-z))
+    accept = pi32 > lam32
+    ambiguous = np.abs(pi - np.float64(lam32)) <= AMBIGUITY_BAND
+    return accept, pi, ambiguous
+
+
+def chain_length(delta, accept) -> int:
+    """Eq. cospec_length: s = min{i : Delta_i = 0 and a_i = 0} (1-based), else K+1."""
+    K = len(delta)
+    rejected = [i for i in range(1, K + 1) if not delta[i - 1] and not accept[i - 1]]
+    return min(rejected) if rejected else K + 1
+
+
+def chain_tokens(s: int, draft_tokens, target_argmax) -> list:
+    """Tokens a round of length s emits (Section 3.3): draft tokens 1..s-1, then the
+    target's token at position s (the bonus token when s = K+1).  target_argmax[j]
+    is the argmax of target row j, i.e. ytilde_{j+1}.  Padded with -1 to K+1."""
+    K = len(draft_tokens)
+    out = [int(t) for t in draft_tokens[: s - 1]] + [int(target_argmax[s - 1])]
+    return out + [-1] * (K + 1 - len(out))
+
+
+def tree_select(parent, passed):
+    """Accepted node of a token tree (tree reading of Eq. cospec_length): a node is
+    reachable when every node on its root path (root excluded) passes; the
+    accepted node is the deepest reachable node, ties to the lowest id.
+    Returns (node, depth of every node, path from the root to the node)."""
+    N = len(parent)
+    ok = [False] * N
+    depth = [0] * N
+    ok[0] = True
+    for n in range(1, N):
+        p = int(parent[n])
+        ok[n] = ok[p] and bool(passed[n])
+        depth[n] = depth[p] + 1
+    best = 0
+    for n in range(1, N):
+        if ok[n] and depth[n] > depth[best]:
+            best = n
+    path = [best]
+    while path[-1] != 0:
+        path.append(int(parent[path[-1]]))
+    return best, depth, path[::-1]
+
+
+def _tree_emit(best, path, node_tokens, target_argmax, N):
+    toks = [int(node_tokens[n]) for n in path[1:]] + [int(target_argmax[best])]
+    return toks + [-1] * (N - len(toks)), list(path) + [-1] * (N - len(path))
+
+
+def _gather(rows: np.ndarray, tokens: np.ndarray) -> np.ndarray:
+    """rows[..., tokens[...]] as exact float64 (one logit per decision)."""
+    g = np.take_along_axis(rows, tokens[..., None].astype(np.int64), axis=-1)[..., 0]
+    return element(g)
+
+
+def _head_arrays(head):
+    w1, b1, w2, b2 = head
+    return w1, b1, w2, float(b2)
+
+
+def verify_block(target, draft, draft_tokens, hidden, head, lam: float) -> dict:
+    """Oracle of one chain verify step.
+
+    target [B, K+1, V], draft [B, K, V] (float32 or bf16 bits), draft_tokens int
+    [B, K], hidden [B, K, d], head = (W1 [h, d], b1 [h] or None, w2 [h], b2).
+    Decision i (1..K) compares draft token i with the argmax of target row i-1
+    (Section 3.1, Delta_i), scores mismatches with the head (Section 3.3), and the
+    round stops at the first rejected mismatch (Eq. cospec_length).
+    """
+    B, K1, V = target.shape
+    K = K1 - 1
+    assert draft.shape == (B, K, V) and draft_tokens.shape == (B, K)
+    toks = np.asarray(draft_tokens, dtype=np.int64)
+    if toks.size and (toks.min() < 0 or toks.max() >= V):
+        raise ValueError("draft token out of range")
+    ts = row_stats(target)
+    ds = row_stats(draft)
+    ytil = ts.arg[:, :K]                                   # ytilde_i = argmax of row i-1
+    delta = (toks == ytil)
+    logp_tgt = _gather(target[:, :K, :], toks) - ts.lse[:, :K]
+    logp_drf = _gather(draft, toks) - ds.lse
+    w1, b1, w2, b2 = _head_arrays(head)
+    mism = np.argwhere(~delta)                             # (b, i-1) pairs
+    z = np.full((B, K), np.nan)
+    if len(mism):
+        rows = mism[:, 0] * K + mism[:, 1]
+        z[mism[:, 0], mism[:, 1]] = head_logits(hidden.reshape(B * K, -1), rows, w1, b1, w2, b2)
+    acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    accept = np.where(delta, True, acc_m)
+    pi = np.where(delta, 1.0, pi_m)
+    ambiguous = np.where(delta, False, amb_m)
+    z_tilde = np.where(delta, np.inf, z)
+    accept_len = np.empty(B, np.int64)
+    tokens = np.empty((B, K + 1), np.int64)
+    outcomes = []
+    for b in range(B):
+        s = chain_length(delta[b], accept[b])
+        accept_len[b] = s
+        tokens[b] = chain_tokens(s, toks[b], ts.arg[b])
+        outcomes.append(chain_outcomes(delta[b], accept[b], ambiguous[b], toks[b], ts.arg[b]))
+    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent,
+                drf_max=ds.max, drf_arg=ds.arg, drf_lse=ds.lse, drf_ent=ds.ent,
+                delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z, z_tilde=z_tilde,
+                pi=pi, accept=accept, ambiguous=ambiguous, accept_len=accept_len,
+                tokens=tokens, outcomes=outcomes)
+
+
+def chain_outcomes(delta, accept, ambiguous, draft_tokens, target_argmax, cap: int = 16):
+    """Every (s, tokens) the round can produce when each ambiguous mismatch decision
+    may go either way; None when more than `cap` such decisions could matter."""
+    K = len(delta)
+    certain_stop = [i for i in range(K) if not delta[i] and not ambiguous[i] and not accept[i]]
+    limit = certain_stop[0] if certain_stop else K
+    free = [i for i in range(limit) if not delta[i] and ambiguous[i]]
+    if len(free) > cap:
+        return None
+    outs = set()
+    for mask in range(1 << len(free)):
+        a = [bool(x) for x in accept]
+        for j, i in enumerate(free):
+            a[i] = bool((mask >> j) & 1)
+        s = chain_length(delta, a)
+        outs.add((s, tuple(chain_tokens(s, draft_tokens, target_argmax))))
+    return outs
+
+
+def _internal(parent) -> np.ndarray:
+    N = len(parent)
+    has_child = np.zeros(N, bool)
+    for n in range(1, N):
+        has_child[int(parent[n])] = True
+    return has_child
+
+
+def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float) -> dict:
+    """Oracle of one tree verify step (tree reading of Section 3.1/3.3).
+
+    target, draft [B, N, V]; parent int [B, N] (parent[0] = -1, parent[n] < n);
+    node_tokens int [B, N]; hidden [B, N, d].  Only draft rows of nodes with a
+    child are reduced (leaf draft rows verify nothing); their statistics are NaN /
+    -1 for leaves.  Node 0 carries no decision.
+    """
+    B, N, V = target.shape
+    par = np.asarray(parent, dtype=np.int64)
+    toks = np.asarray(node_tokens, dtype=np.int64)
+    for b in range(B):
+        if par[b, 0] != -1 or any(not (0 <= par[b, n] < n) for n in range(1, N)):
+            raise ValueError("parent array must satisfy parent[0] = -1, 0 <= parent[n] < n")
+    if N > 1 and (toks[:, 1:].min() < 0 or toks[:, 1:].max() >= V):
+        raise ValueError("node token out of range")
+    ts = row_stats(target)
+    internal = np.stack([_internal(par[b]) for b in range(B)])
+    drf_max = np.full((B, N), np.nan)
+    drf_arg = np.full((B, N), -1, np.int64)
+    drf_lse = np.full((B, N), np.nan)
+    drf_ent = np.full((B, N), np.nan)
+    ib, inn = np.nonzero(internal)
+    if len(ib):
+        ds = row_stats(draft[ib, inn])
+        drf_max[ib, inn], drf_arg[ib, inn], drf_lse[ib, inn], drf_ent[ib, inn] = (
+            ds.max, ds.arg, ds.lse, ds.ent)
+    delta = np.ones((B, N), bool)
+    logp_tgt = np.full((B, N), np.nan)
+    logp_drf = np.full((B, N), np.nan)
+    for b in range(B):
+        for n in range(1, N):
+            p = par[b, n]
+            t = toks[b, n]
+            delta[b, n] = t == ts.arg[b, p]
+            logp_tgt[b, n] = element(target[b, p, t:t + 1])[0] - ts.lse[b, p]
+            logp_drf[b, n] = element(draft[b, p, t:t + 1])[0] - drf_lse[b, p]
+    w1, b1, w2, b2 = _head_arrays(head)
+    z = np.full((B, N), np.nan)
+    mb, mn = np.nonzero(~delta)
+    if len(mb):
+        z[mb, mn] = head_logits(hidden.reshape(B * N, -1), mb * N + mn, w1, b1, w2, b2)
+    acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    accept = np.where(delta, True, acc_m)
+    pi = np.where(delta, 1.0, pi_m)
+    ambiguous = np.where(delta, False, amb_m)
+    z_tilde = np.where(delta, np.inf, z)
+    accept_len = np.empty(B, np.int64)
+    tokens = np.empty((B, N), np.int64)
+    path = np.empty((B, N), np.int64)
+    outcomes = []
+    for b in range(B):
+        passed = delta[b] | accept[b]
+        best, depth, pth = tree_select(par[b], passed)
+        accept_len[b] = depth[best] + 1
+        tokens[b], path[b] = _tree_emit(best, pth, toks[b], ts.arg[b], N)
+        outcomes.append(tree_outcomes(par[b], delta[b], accept[b], ambiguous[b], toks[b],
+                                      ts.arg[b]))
+    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent,
+                drf_max=drf_max, drf_arg=drf_arg, drf_lse=drf_lse, drf_ent=drf_ent,
+                internal=internal, delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z,
+                z_tilde=z_tilde, pi=pi, accept=accept, ambiguous=ambiguous,
+                accept_len=accept_len, tokens=tokens, path=path, outcomes=outcomes)
+
+
+def tree_outcomes(parent, delta, accept, ambiguous, node_tokens, target_argmax, cap: int = 16):
+    """Every (accept_len, tokens, path) a tree round can produce when each ambiguous
+    mismatch decision may go either way; None when more than `cap` could matter."""
+    N = len(parent)
+    # a node's decision can matter only if no certain failure lies on its root path
+    blocked = [False] * N
+    for n in range(1, N):
+        p = int(parent[n])
+        certain_fail = (not delta[n]) and (not ambiguous[n]) and (not accept[n])
+        blocked[n] = blocked[p] or certain_fail
+    free = [n for n in range(1, N) if not delta[n] and ambiguous[n] and not blocked[int(parent[n])]]
+    if len(free) > cap:
+        return None
+    outs = set()
+    for mask in range(1 << len(free)):
+        a = [bool(x) for x in accept]
+        for j, n in enumerate(free):
+            a[n] = bool((mask >> j) & 1)
+        passed = [bool(delta[n]) or a[n] for n in range(N)]
+        best, depth, pth = tree_select(parent, passed)
+        toks, pth_pad = _tree_emit(best, pth, node_tokens, target_argmax, N)
+        outs.add((depth[best] + 1, tuple(toks), tuple(pth_pad)))
+    return outs
+
+
+def arbitrate(hidden, rows, head, lam: float) -> dict:
+    """Head alone over selected hidden rows (rows=None: all rows): z, pi, a and the
+    ambiguity flag (Section 3.3, Eq. policy-prob and Eq. infer_thre without the
+    match override, which needs Delta)."""
+    hidden2 = hidden.reshape(-1, hidden.shape[-1])
+    if rows is None:
+        rows = np.arange(hidden2.shape[0])
+    w1, b1, w2, b2 = _head_arrays(head)
+    z = head_logits(hidden2, rows, w1, b1, w2, b2)
+    a, pi, amb = policy_accept(z, lam)
+    return dict(z=z, pi=pi, accept=a, ambiguous=amb)

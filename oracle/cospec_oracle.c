@@ -1,0 +1,110 @@
+/*
+ * CPU oracle for the CoSpec verify-and-arbitrate step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  The test suite, the package smoke check and the
+ * benchmark's CPU-baseline leg are the only code allowed to load this library.
+ * It shares no code, header, table or helper with the GPU path, and it is never
+ * a fallback for it.
+ *
+ * Everything is computed in double precision with plain sequential loops that
+ * follow the definitions they cite ("Beyond the Target: From Imitation to
+ * Collaboration in Speculative Decoding", Section 3).  bf16 inputs are widened
+ * exactly (bf16 -> fp32 by placing the 16 stored bits in the high half, fp32 ->
+ * fp64 exactly).  Nothing here is blocked, fused or reordered.
+ *
+ * The scans (Eq. cospec_length, the tree reading) and the policy threshold live
+ * in the Python half of the oracle (oracle/__init__.py); this file holds the two
+ * loops that touch every logit or every weight.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
+
+/* Element i of an array of fp32 values or of raw bf16 bit patterns, as a double. */
+static double oracle_elem(const void *base, int dtype, int64_t i)
+{
+    if (dtype == ORACLE_F32)
+        return (double)((const float *)base)[i];
+    uint32_t bits = (uint32_t)((const uint16_t *)base)[i] << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+/*
+ * Statistics of `nrows` logit rows (row r starts at element r*ld) over the
+ * whole vocabulary [0, V):
+ *   max      m = max_v x[v]
+ *   argmax   the first v with x[v] = m.  With greedy decoding (Appendix C.3)
+ *            the target's verification token is the argmax of its row
+ *            (Section 3.1); ties go to the lowest index.
+ *   lse      log sum_v exp(x[v])  (the log-softmax normaliser), computed as
+ *            m + log sum_v exp(x[v] - m)
+ *   entropy  H = -sum_v p[v] log p[v] in nats, with p = softmax(x) and
+ *            log p[v] = x[v] - lse.
+ * Returns 0, or -(r+1) when row r holds a non-finite entry (finite logits
+ * are a precondition).
+ */
+int64_t oracle_row_stats(const void *rows, int dtype, int64_t ld, int64_t nrows, int64_t V,
+                         double *out_max, int64_t *out_arg, double *out_lse, double *out_ent)
+{
+    size_t esz = dtype == ORACLE_F32 ? 4 : 2;
+    for (int64_t r = 0; r < nrows; ++r) {
+        const void *row = (const char *)rows + (size_t)r * (size_t)ld * esz;
+        double m = -INFINITY;
+        int64_t arg = -1;
+        for (int64_t v = 0; v < V; ++v) {
+            double x = oracle_elem(row, dtype, v);
+            if (!isfinite(x))
+                return -(r + 1);
+            if (x > m) {            /* strict: the first occurrence of the max wins */
+                m = x;
+                arg = v;
+            }
+        }
+        double s = 0.0;
+        for (int64_t v = 0; v < V; ++v)
+            s += exp(oracle_elem(row, dtype, v) - m);
+        double lse = m + log(s);
+        double h = 0.0;
+        for (int64_t v = 0; v < V; ++v) {
+            double logp = oracle_elem(row, dtype, v) - lse;
+            h -= exp(logp) * logp;
+        }
+        out_max[r] = m;
+        out_arg[r] = arg;
+        out_lse[r] = lse;
+        out_ent[r] = h;
+    }
+    return 0;
+}
+
+/*
+ * Arbitration head g_phi applied to selected hidden rows (Section 3.3:
+ * z_i = g_phi(h_{l_c+1+i})).  The paper calls g_phi a lightweight binary head
+ * without giving its form; it is read here as a two-layer MLP with a ReLU:
+ *     u = W1 h + b1   (W1: [hdim][d] row-major, b1: [hdim] or absent = 0)
+ *     z = w2 . max(u, 0) + b2
+ * Row k of the output uses hidden row rows[k] (which starts at element
+ * rows[k]*ld_h).  hidden, W1, b1 and w2 share `dtype`.
+ */
+void oracle_head(const void *hidden, int dtype, int64_t ld_h, const int64_t *rows, int64_t nsel,
+                 const void *w1, const void *b1, const void *w2, double b2, int64_t d,
+                 int64_t hdim, double *out_z)
+{
+    size_t esz = dtype == ORACLE_F32 ? 4 : 2;
+    for (int64_t k = 0; k < nsel; ++k) {
+        const void *hrow = (const char *)hidden + (size_t)rows[k] * (size_t)ld_h * esz;
+        double z = b2;
+        for (int64_t j = 0; j < hdim; ++j) {
+            double u = b1 ? oracle_elem(b1, dtype, j) : 0.0;
+            for (int64_t c = 0; c < d; ++c)
+                u += oracle_elem(w1, dtype, j * d + c) * oracle_elem(hrow, dtype, c);
+            double r = u > 0.0 ? u : 0.0;
+            z += oracle_elem(w2, dtype, j) * r;
+        }
+        out_z[k] = z;
+    }
+}

@@ -1,0 +1,52 @@
+"""Planted mistakes in a copy of the oracle must fail its pins.
+
+Each case copies oracle/ to a temporary directory, applies one textual mutation
+(a dropped term, a wrong sign, a wrong index, a transposed operand, a flipped
+comparison), builds it, and runs tests/test_oracle_pins.py against the copy in a
+subprocess.  The pins must fail.  This runs on the CPU only.
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ORACLE = os.path.join(ROOT, "oracle")
+
+MUTATIONS = [
+    # (file, original text, planted mistake)
+    ("cospec_oracle.c", "if (x > m) {", "if (x >= m) {"),                       # ties to the last index
+    ("cospec_oracle.c", "h -= exp(logp) * logp;", "h += exp(logp) * logp;"),    # entropy sign
+    ("cospec_oracle.c", "double lse = m + log(s);", "double lse = log(s);"),   # dropped max shift
+    ("cospec_oracle.c", "s += exp(oracle_elem(row, dtype, v) - m);",
+     "s += exp(oracle_elem(row, dtype, v) - m) * (v > 0);"),                    # dropped first term
+    ("cospec_oracle.c", "double r = u > 0.0 ? u : 0.0;", "double r = u;"),     # dropped ReLU
+    ("cospec_oracle.c", "double u = b1 ? oracle_elem(b1, dtype, j) : 0.0;", "double u = 0.0;"),
+    ("cospec_oracle.c", "oracle_elem(w1, dtype, j * d + c)", "oracle_elem(w1, dtype, c * hdim + j)"),
+    ("cospec_oracle.c", "double z = b2;", "double z = 0.0;"),                  # dropped b2
+    ("__init__.py", "if not delta[i - 1] and not accept[i - 1]]", "if not delta[i - 1] and accept[i - 1]]"),
+    ("__init__.py", "[int(target_argmax[s - 1])]", "[int(target_argmax[s])]"),   # wrong emitted row
+    ("__init__.py", "ytil = ts.arg[:, :K]", "ytil = ts.arg[:, 1:]"),            # verify against wrong row
+    ("__init__.py", "logp_tgt = _gather(target[:, :K, :], toks)", "logp_tgt = _gather(target[:, 1:, :], toks)"),
+    ("__init__.py", "if ok[n] and depth[n] > depth[best]:", "if ok[n] and depth[n] >= depth[best]:"),
+    ("__init__.py", "accept = pi32 > lam32", "accept = pi32 >= lam32"),        # non-strict threshold
+    ("__init__.py", "ok[n] = ok[p] and bool(passed[n])", "ok[n] = bool(passed[n])"),  # ignores ancestors
+]
+
+
+@pytest.mark.parametrize("fname,old,new", MUTATIONS, ids=[f"{m[0]}:{m[2][:40]}" for m in MUTATIONS])
+def test_planted_mistake_fails_pins(tmp_path, fname, old, new):
+    dst = tmp_path / "oracle_mut"
+    dst.mkdir()
+    for f in ("__init__.py", "cospec_oracle.c"):
+        shutil.copy(os.path.join(ORACLE, f), dst / f)
+    text = (dst / fname).read_text()
+    assert text.count(old) == 1, f"mutation anchor not found once: {old!r}"
+    (dst / fname).write_text(text.replace(old, new))
+    env = dict(os.environ, COSPEC_ORACLE_UNDER_TEST=str(dst))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode == 1, f"pins did not catch {new!r}:\n{r.stdout[-2000:]}"

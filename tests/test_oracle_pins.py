@@ -1,0 +1,429 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Nothing here compares the oracle with itself: every expected value is a closed
+form, a hand-worked fixture (tests/golden/), a brute-force enumeration, an
+independent formulation of the same definition, or a numpy/scipy routine that
+the oracle does not call.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+from paper_2605_24793_amd import workloads
+
+# The mutation tests re-run these pins against a copy of the oracle with a planted
+# mistake; they name that copy's directory here.  Normal runs use oracle/.
+_UNDER_TEST = os.environ.get("COSPEC_ORACLE_UNDER_TEST")
+if _UNDER_TEST:
+    import importlib.util
+    _spec = importlib.util.spec_from_file_location(
+        "oracle_under_test", os.path.join(_UNDER_TEST, "__init__.py"),
+        submodule_search_locations=[_UNDER_TEST])
+    oracle = importlib.util.module_from_spec(_spec)
+    _spec.loader.exec_module(oracle)
+else:
+    import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _rows_from_fixture(r):
+    if "two_level" in r:
+        t = r["two_level"]
+        x = np.full(t["V"], t["c"], np.float32)
+        x[t["k"]] = t["c"] + t["L"]
+        return x
+    if r["dtype"] == "bf16":
+        return np.array(r["bits"], np.uint16)
+    return np.array(r["values"], np.float32)
+
+
+# ---------------------------------------------------------------- row statistics
+
+@pytest.mark.parametrize("r", _load("row_stats.json")["rows"], ids=lambda r: r["name"])
+def test_row_stats_golden(r):
+    env = {k: getattr(math, k) for k in ("log", "exp")}
+    if "two_level" in r:
+        env.update(r["two_level"])
+    assert eval(r["lse_expr"], env) == pytest.approx(r["lse"], rel=1e-15)
+    st = oracle.row_stats(_rows_from_fixture(r)[None])
+    assert st.arg[0] == r["argmax"]
+    assert st.max[0] == r["max"]
+    assert st.lse[0] == pytest.approx(r["lse"], rel=1e-12, abs=1e-12)
+    assert st.ent[0] == pytest.approx(r["entropy"], rel=1e-12, abs=1e-12)
+
+
+@pytest.mark.parametrize("V,c", [(1, 0.0), (7, -3.25), (32000, 1.5), (151936, -20.0)])
+def test_constant_row_closed_form(V, c):
+    st = oracle.row_stats(np.full((1, V), c, np.float32))
+    assert st.arg[0] == 0
+    assert st.lse[0] == pytest.approx(c + math.log(V), rel=1e-12, abs=1e-12)
+    assert st.ent[0] == pytest.approx(math.log(V), rel=1e-12, abs=1e-12)
+
+
+@pytest.mark.parametrize("V,c,L,k", [(2, 0.0, 1.0, 1), (1000, 3.0, -2.0, 5), (128256, -1.0, 12.0, 128255),
+                                     (151936, 4.0, 30.0, 0)])
+def test_two_level_row_closed_form(V, c, L, k):
+    x = np.full(V, c, np.float32)
+    x[k] = c + L
+    st = oracle.row_stats(x[None])
+    if L > 0:
+        assert st.arg[0] == k
+    else:
+        assert st.arg[0] == (0 if k != 0 else 1)
+    # p = e^L / (e^L + V - 1) at index k, q = 1 - p spread over the other V - 1,
+    # written without cancellation so the closed form itself stays exact to ~1e-15
+    lse = c + math.log(math.exp(L) + V - 1)
+    log_p = -math.log1p((V - 1) * math.exp(-L))
+    log_q1 = -math.log1p(math.exp(L) / (V - 1)) - math.log(V - 1)   # log(q / (V - 1))
+    p, q = math.exp(log_p), (V - 1) * math.exp(log_q1)
+    ent = -p * log_p - q * log_q1
+    assert st.lse[0] == pytest.approx(lse, rel=1e-12, abs=1e-12)
+    # a plain sequential fp64 sum of V terms onto the dominant one carries an absolute
+    # error of about sqrt(V) * 2^-53; with a +30 peak the entropy itself is ~4e-7
+    assert st.ent[0] == pytest.approx(ent, rel=1e-9, abs=1e-10)
+
+
+def test_argmax_ties_lowest_index():
+    rng = np.random.default_rng(5)
+    for V in (2, 9, 4096, 151936):
+        x = rng.normal(size=V).astype(np.float32)
+        pos = np.sort(rng.choice(V, size=min(V, 5), replace=False))
+        x[pos] = 100.0
+        st = oracle.row_stats(x[None])
+        assert st.arg[0] == pos[0]
+        assert int(np.argmax(x)) == pos[0]          # numpy documents first occurrence
+
+
+def test_row_stats_against_scipy_float64():
+    rng = np.random.default_rng(11)
+    for V, scale in ((17, 1.0), (4099, 4.0), (32000, 3.0)):
+        x = (rng.normal(size=(6, V)) * scale).astype(np.float32)
+        st = oracle.row_stats(x)
+        x64 = x.astype(np.float64)
+        lse = scipy.special.logsumexp(x64, axis=-1)
+        p = scipy.special.softmax(x64, axis=-1)
+        ent = scipy.special.entr(p).sum(axis=-1)
+        np.testing.assert_allclose(st.lse, lse, rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(st.ent, ent, rtol=1e-10, atol=1e-12)
+        np.testing.assert_array_equal(st.arg, np.argmax(x, axis=-1))
+        np.testing.assert_array_equal(st.max, x.max(axis=-1))
+
+
+def test_bf16_widening_matches_torch():
+    g = torch.Generator().manual_seed(3)
+    t = (torch.randn(3, 1000, generator=g) * 8).to(torch.bfloat16)
+    bits = workloads.bf16_bits(t)
+    np.testing.assert_array_equal(oracle.element(bits), t.double().numpy())
+    st = oracle.row_stats(bits)
+    np.testing.assert_allclose(st.lse, torch.logsumexp(t.double(), -1).numpy(), rtol=1e-13)
+    np.testing.assert_array_equal(st.arg, torch.argmax(t.float(), -1).numpy())
+
+
+def test_shift_invariance():
+    rng = np.random.default_rng(2)
+    # multiples of 2^-10 below 64 in magnitude: adding 8 is exact in fp32
+    x = (np.round(rng.normal(size=(3, 5000)) * 4 * 1024) / 1024).astype(np.float32)
+    a = oracle.row_stats(x)
+    b = oracle.row_stats((x + np.float32(8.0)).astype(np.float32))
+    np.testing.assert_allclose(b.lse, a.lse + 8.0, rtol=1e-13)
+    np.testing.assert_allclose(b.ent, a.ent, rtol=1e-10, atol=1e-12)
+    np.testing.assert_array_equal(b.arg, a.arg)
+
+
+def test_nonfinite_rejected():
+    x = np.zeros((2, 8), np.float32)
+    x[1, 3] = np.inf
+    with pytest.raises(ValueError, match="row 1"):
+        oracle.row_stats(x)
+
+
+# ---------------------------------------------------------------- head
+
+def test_head_identity_block_closed_form():
+    rng = np.random.default_rng(7)
+    d, h = 48, 16
+    w1 = np.zeros((h, d), np.float32)
+    w1[np.arange(h), np.arange(h)] = 1.0          # W1 = [I, 0]
+    w2 = np.ones(h, np.float32)
+    hid = rng.normal(size=(5, d)).astype(np.float32)
+    z = oracle.head_logits(hid, np.arange(5), w1, None, w2, 0.25)
+    expect = np.maximum(hid[:, :h].astype(np.float64), 0).sum(axis=1) + 0.25
+    np.testing.assert_allclose(z, expect, rtol=1e-15)
+
+
+def test_head_bias_paths():
+    rng = np.random.default_rng(8)
+    d, h = 32, 8
+    w1 = rng.normal(size=(h, d)).astype(np.float32)
+    w2 = rng.normal(size=h).astype(np.float32)
+    hid = rng.normal(size=(3, d)).astype(np.float32)
+    # b1 so negative that every unit is off: z = b2 exactly
+    b1 = np.full(h, -1e6, np.float32)
+    np.testing.assert_array_equal(oracle.head_logits(hid, [0, 1, 2], w1, b1, w2, -0.5), -0.5)
+    # b1 so positive that every unit is on: z = w2.(W1 h + b1) + b2 (linear)
+    b1 = np.full(h, 1e4, np.float32)
+    lin = (hid.astype(np.float64) @ w1.astype(np.float64).T + 1e4) @ w2.astype(np.float64) + 0.5
+    np.testing.assert_allclose(oracle.head_logits(hid, [0, 1, 2], w1, b1, w2, 0.5), lin, rtol=1e-12)
+
+
+def test_head_against_numpy_matmul_bf16():
+    g = torch.Generator().manual_seed(9)
+    d, h = 256, 64
+    hid = torch.randn(10, d, generator=g).to(torch.bfloat16)
+    w1 = (torch.randn(h, d, generator=g) / 16).to(torch.bfloat16)
+    b1 = (torch.randn(h, generator=g) * 0.3).to(torch.bfloat16)
+    w2 = (torch.randn(h, generator=g) / 8).to(torch.bfloat16)
+    rows = np.array([9, 0, 3, 3])
+    z = oracle.head_logits(workloads.bf16_bits(hid), rows, workloads.bf16_bits(w1),
+                           workloads.bf16_bits(b1), workloads.bf16_bits(w2), 0.125)
+    H, W1, B1, W2 = (t.double().numpy() for t in (hid, w1, b1, w2))
+    expect = np.maximum(H[rows] @ W1.T + B1, 0.0) @ W2 + 0.125
+    np.testing.assert_allclose(z, expect, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- policy threshold
+
+def test_policy_sigmoid_and_strict_threshold():
+    z = np.array([0.0, -3.0, 2.0, 40.0, -120.0])
+    a, pi, amb = oracle.policy_accept(z, 0.5)
+    np.testing.assert_allclose(pi, scipy.special.expit(z), rtol=1e-15)
+    assert pi[0] == 0.5 and not a[0] and amb[0]       # sigma(0) = 0.5 is not > 0.5
+    assert list(a[1:]) == [False, True, True, False]
+    a, _, _ = oracle.policy_accept(np.array([0.0]), 0.4999)
+    assert a[0]
+
+
+@pytest.mark.parametrize("lam", [1.0, 1.5, 1e9])
+def test_policy_lambda_ge_one_never_accepts(lam):
+    a, _, _ = oracle.policy_accept(np.array([-50.0, 0.0, 17.0, 100.0, 1e30]), lam)
+    assert not a.any()
+
+
+@pytest.mark.parametrize("lam", [-1e-7, -0.5, -1e9])
+def test_policy_lambda_negative_always_accepts(lam):
+    a, _, _ = oracle.policy_accept(np.array([-200.0, -17.0, 0.0, 50.0]), lam)
+    assert a.all()
+
+
+# ---------------------------------------------------------------- chain scan
+
+def _sequential(delta, accept):
+    for i in range(len(delta)):
+        if not delta[i] and not accept[i]:
+            return i + 1
+    return len(delta) + 1
+
+
+def _longest_passing_prefix(delta, accept):
+    L = 0
+    while L < len(delta) and (delta[L] or accept[L]):
+        L += 1
+    return L + 1
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 7])
+def test_chain_length_brute_force(K):
+    for delta in itertools.product([0, 1], repeat=K):
+        strict = oracle.chain_length(delta, [0] * K)
+        for acc in itertools.product([0, 1], repeat=K):
+            s = oracle.chain_length(delta, acc)
+            assert s == _sequential(delta, acc) == _longest_passing_prefix(delta, acc)
+            assert 1 <= s <= K + 1
+            assert s >= strict
+            for j in range(K):                  # accepting one more never shortens the round
+                if not acc[j]:
+                    up = list(acc)
+                    up[j] = 1
+                    assert oracle.chain_length(delta, up) >= s
+
+
+@pytest.mark.parametrize("c", _load("chain_rounds.json")["cases"], ids=lambda c: c["name"])
+def test_chain_golden(c):
+    delta = [int(a == b) for a, b in zip(c["draft"], c["target_tokens"])]
+    assert delta == c["delta"]
+    s = oracle.chain_length(delta, c["accept"])
+    assert s == c["s"]
+    assert oracle.chain_tokens(s, c["draft"], c["target_tokens"]) == c["tokens"]
+    assert oracle.chain_length(delta, [0] * c["K"]) == c["strict_s"]
+
+
+# ---------------------------------------------------------------- tree scan
+
+def _tree_brute(parent, passed):
+    N = len(parent)
+    best, best_depth = 0, 0
+    for n in range(N):
+        path = [n]
+        while path[-1] != 0:
+            path.append(parent[path[-1]])
+        if all(passed[m] for m in path[:-1]):
+            if len(path) - 1 > best_depth:
+                best, best_depth = n, len(path) - 1
+    return best, best_depth
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tree_select_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    N = int(rng.integers(1, 10))
+    parent = [-1] + [int(rng.integers(0, n)) for n in range(1, N)]
+    for bits in itertools.product([0, 1], repeat=N - 1):
+        passed = [1] + list(bits)
+        node, depth, path = oracle.tree_select(parent, passed)
+        bnode, bdepth = _tree_brute(parent, passed)
+        assert node == bnode and depth[node] == bdepth
+        assert path[0] == 0 and path[-1] == node and len(path) == bdepth + 1
+        assert all(parent[path[k + 1]] == path[k] for k in range(len(path) - 1))
+
+
+def test_tree_golden():
+    g = _load("tree_rounds.json")
+    for c in g["cases"]:
+        node, depth, path = oracle.tree_select(g["parent"], c["passed"])
+        assert node == c["node"] and depth[node] + 1 == c["accept_len"] and path == c["path"]
+        toks = [g["node_tokens"][n] for n in path[1:]] + [g["target_argmax"][node]]
+        assert toks == c["tokens"]
+
+
+def test_path_tree_equals_chain_scan():
+    for K in range(1, 7):
+        parent = [-1] + list(range(K))
+        for delta in itertools.product([0, 1], repeat=K):
+            for acc in itertools.product([0, 1], repeat=K):
+                passed = [1] + [d or a for d, a in zip(delta, acc)]
+                node, depth, _ = oracle.tree_select(parent, passed)
+                assert depth[node] + 1 == oracle.chain_length(delta, acc)
+
+
+# ---------------------------------------------------------------- whole verify step
+
+def _np_chain(wl):
+    conv = (lambda t: workloads.bf16_bits(t)) if wl.target.dtype == torch.bfloat16 else (
+        lambda t: t.contiguous().numpy())
+    head = (conv(wl.head.w1), None if wl.head.b1 is None else conv(wl.head.b1), conv(wl.head.w2),
+            wl.head.b2)
+    return conv(wl.target), conv(wl.draft), wl.draft_tokens.numpy(), conv(wl.hidden), head
+
+
+def _small_chain(dtype="bf16", B=6, K=5, V=3001, noise=1.0, seed=21, bias=True, **kw):
+    return workloads.make_chain(B=B, K=K, V=V, d=64, h=32, dtype=dtype, noise=noise, seed=seed,
+                                bias=bias, **kw)
+
+
+def _greedy_spd(target64, draft_tokens):
+    """Textbook greedy speculative decoding, one position at a time."""
+    K = len(draft_tokens)
+    out = []
+    for i in range(K):
+        t = int(np.argmax(target64[i]))
+        if t != int(draft_tokens[i]):
+            out.append(t)
+            return len(out), out
+        out.append(int(draft_tokens[i]))
+    out.append(int(np.argmax(target64[K])))
+    return K + 1, out
+
+
+@pytest.mark.parametrize("lam", [1.0, 2.5])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_always_defer_is_greedy_spd(lam, dtype):
+    wl = _small_chain(dtype=dtype, B=10, noise=0.7, peaked=0.3)
+    t, d, toks, hid, head = _np_chain(wl)
+    r = oracle.verify_block(t, d, toks, hid, head, lam)
+    t64 = oracle.element(t)
+    for b in range(wl.B):
+        s, out = _greedy_spd(t64[b], toks[b])
+        assert r["accept_len"][b] == s
+        assert list(r["tokens"][b][:s]) == out and all(x == -1 for x in r["tokens"][b][s:])
+        strict = [i + 1 for i in range(wl.K) if not r["delta"][b, i]]
+        assert s == (strict[0] if strict else wl.K + 1)     # Eq. strict-spd-len
+
+
+@pytest.mark.parametrize("lam", [-1e-6, -3.0])
+def test_always_accept_emits_block_plus_bonus(lam):
+    wl = _small_chain(B=5)
+    t, d, toks, hid, head = _np_chain(wl)
+    r = oracle.verify_block(t, d, toks, hid, head, lam)
+    t64 = oracle.element(t)
+    for b in range(wl.B):
+        assert r["accept_len"][b] == wl.K + 1
+        assert list(r["tokens"][b]) == list(toks[b]) + [int(np.argmax(t64[b, wl.K]))]
+
+
+def test_block_features_against_scipy():
+    wl = _small_chain(B=4, K=6, V=2049, peaked=0.25)
+    t, d, toks, hid, head = _np_chain(wl)
+    r = oracle.verify_block(t, d, toks, hid, head, 0.5)
+    t64, d64 = oracle.element(t), oracle.element(d)
+    K = wl.K
+    lt = scipy.special.log_softmax(t64, axis=-1)
+    ld = scipy.special.log_softmax(d64, axis=-1)
+    for b in range(wl.B):
+        for i in range(1, K + 1):
+            y = toks[b, i - 1]
+            # l_i = log p_T(yhat_i | prefix, yhat_<i): target row i-1 (Section 3.4)
+            assert r["logp_tgt"][b, i - 1] == pytest.approx(lt[b, i - 1, y], abs=1e-12)
+            assert r["logp_drf"][b, i - 1] == pytest.approx(ld[b, i - 1, y], abs=1e-12)
+            assert r["delta"][b, i - 1] == (y == np.argmax(t64[b, i - 1]))
+    np.testing.assert_allclose(r["tgt_ent"], scipy.special.entr(np.exp(lt)).sum(-1), rtol=1e-9)
+    np.testing.assert_allclose(r["drf_ent"], scipy.special.entr(np.exp(ld)).sum(-1), rtol=1e-9)
+    # z only on mismatches, +inf (forced accept) on matches (Eq. policy-prob)
+    assert np.isinf(r["z_tilde"][r["delta"]]).all() and r["accept"][r["delta"]].all()
+    mism = ~r["delta"]
+    W1, W2 = (oracle.element(x).astype(np.float64) for x in (head[0], head[2]))
+    B1 = oracle.element(head[1])
+    Hh = oracle.element(hid)
+    zz = np.maximum(Hh @ W1.T + B1, 0) @ W2 + head[3]
+    np.testing.assert_allclose(r["z"][mism], zz[mism], rtol=1e-12, atol=1e-14)
+
+
+def test_chain_outcome_set_enumerates_ambiguous_decisions():
+    delta = [1, 0, 0, 1]
+    accept = [1, 1, 0, 1]
+    amb = [False, True, False, False]
+    outs = oracle.chain_outcomes(delta, accept, amb, [7, 8, 9, 10], [7, 1, 2, 10, 5])
+    assert outs == {(3, (7, 8, 2, -1, -1)), (2, (7, 1, -1, -1, -1))}
+    # an ambiguous decision after a certain rejection cannot matter
+    outs = oracle.chain_outcomes([0, 0], [0, 1], [False, True], [3, 4], [5, 6, 7])
+    assert outs == {(1, (5, -1, -1))}
+
+
+def test_path_tree_verify_equals_chain_verify():
+    wl = _small_chain(B=4, K=5, V=1500, noise=0.6)
+    t, d, toks, hid, head = _np_chain(wl)
+    rc = oracle.verify_block(t, d, toks, hid, head, 0.5)
+    B, K = wl.B, wl.K
+    N = K + 1
+    dpad = np.concatenate([d, d[:, :1]], axis=1)          # leaf draft row: never read
+    parent = np.tile(np.array([-1] + list(range(K))), (B, 1))
+    node_tokens = np.concatenate([np.full((B, 1), -1), toks], axis=1)
+    hpad = np.concatenate([hid[:, :1], hid], axis=1)       # hidden row n <-> decision n
+    rt = oracle.verify_tree(t, dpad, parent, node_tokens, hpad, head, 0.5)
+    np.testing.assert_array_equal(rt["accept_len"], rc["accept_len"])
+    np.testing.assert_array_equal(rt["tokens"][:, :K + 1], rc["tokens"])
+    np.testing.assert_array_equal(rt["delta"][:, 1:], rc["delta"])
+    np.testing.assert_allclose(rt["z"][:, 1:], rc["z"], rtol=0, atol=0, equal_nan=True)
+    np.testing.assert_array_equal(rt["drf_arg"][:, :K], rc["drf_arg"])
+    assert (rt["drf_arg"][:, K] == -1).all()
+
+
+def test_tree_config_structure():
+    tr = workloads.make_config(5, B=2)
+    assert tr.N == 60
+    par = tr.parent.numpy()
+    for b in range(tr.B):
+        assert par[b, 0] == -1 and all(0 <= par[b, n] < n for n in range(1, 60))
+        _, depth, _ = oracle.tree_select(par[b], [1] * 60)
+        assert max(depth) == 6
