@@ -1,0 +1,173 @@
+"""Throughput of the CoSpec verify-and-arbitrate step on one MI355X.
+
+One step = one cospec_verify_block call (all of: vocabulary reductions of the
+target and draft rows, merge/Delta/compaction, MFMA head on the mismatch rows,
+first-stop scan and emission, features written) over one batch that is already
+resident in HBM.  Default workload: the large chain batch B=256, K=7,
+V=151936 bf16 logits, head 5120->512->1, lambda 0.5.
+
+Prints one JSON line: rows/s (B*(K+1) verified rows per second), the roofline
+of the dominant kernel (the vocabulary reduction, timed with HIP events on the
+stream it runs on), and the CPU oracle timed on a bounded sample of the same
+workload on this host, with a parity re-check of the timed outputs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified rows/sec (B×(k+1)) and achieved HBM GB/s vs peak, V=151936 bf16"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (default 4)")
+    ap.add_argument("--splits", type=int, default=0, help="workgroups per row (0 = automatic)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU budget of the oracle baseline sample (0 disables it)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2605_24793_amd as cs
+    from paper_2605_24793_amd import workloads
+    from paper_2605_24793_amd.workloads import bf16_bits
+
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating workload {args.config}", file=sys.stderr, flush=True)
+    wl = workloads.make_config(args.config)
+    tree = isinstance(wl, workloads.TreeBatch)
+    lam = wl.lambdas[len(wl.lambdas) // 2]
+    head = workloads.Head(wl.head.w1.to(dev), None if wl.head.b1 is None else wl.head.b1.to(dev),
+                          wl.head.w2.to(dev), wl.head.b2)
+    tgt, drf, hid = wl.target.to(dev), wl.draft.to(dev), wl.hidden.to(dev)
+    if tree:
+        par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
+        p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits)
+        rows = wl.B * wl.N
+        internal = np.zeros((wl.B, wl.N), bool)
+        pn = wl.parent.numpy()
+        for b in range(wl.B):
+            for n in range(1, wl.N):
+                internal[b, pn[b, n]] = True
+        reduced_rows = rows + int(internal.sum())
+    else:
+        tok = wl.draft_tokens.to(dev)
+        p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits)
+        rows = wl.B * (wl.K + 1)
+        reduced_rows = wl.B * (2 * wl.K + 1)
+    elem = tgt.element_size()
+    logit_bytes = reduced_rows * wl.V * elem       # algorithmic bytes of the reduction launch
+    torch.cuda.synchronize()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        p.launch()
+    torch.cuda.synchronize()
+    k_begin = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    k_end = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for e in k_begin + k_end:
+        e.record()                                 # materialise the HIP events
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    wall0 = time.perf_counter()
+    t0.record()
+    for i in range(args.steps):
+        p.launch(begin_event=k_begin[i], end_event=k_end[i])
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    k_ms = [b.elapsed_time(e) for b, e in zip(k_begin, k_end)]
+    k_avg = float(np.mean(k_ms))
+    ms_per_step = total_ms / args.steps
+    value = rows / (ms_per_step * 1e-3)
+    achieved = logit_bytes / (k_avg * 1e-3) / 1e9
+    res = p.result()
+    out = {k: v.cpu() for k, v in res.items()}
+
+    # CPU oracle on a bounded sample (first sequences of the same workload), also a
+    # parity re-check of the timed outputs on those sequences
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        from oracle import parity
+
+        def conv(t):
+            return bf16_bits(t) if t.dtype == torch.bfloat16 else t.contiguous().numpy()
+        head_np = (conv(wl.head.w1), None if wl.head.b1 is None else conv(wl.head.b1),
+                   conv(wl.head.w2), wl.head.b2)
+        done, spent, chunk = 0, 0.0, 8
+        checked = 0
+        while done < wl.B and spent < args.cpu_seconds:
+            seqs = list(range(done, min(wl.B, done + chunk)))
+            sub = wl.take(seqs)
+            c0 = time.perf_counter()
+            if tree:
+                ref = oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
+                                         sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam)
+            else:
+                ref = oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                          conv(sub.hidden), head_np, lam)
+            spent += time.perf_counter() - c0
+            gsub = {k: v[seqs] for k, v in out.items()}
+            (parity.check_tree if tree else parity.check_block)(gsub, ref)
+            checked += len(seqs)
+            done += len(seqs)
+        cpu_rows = done * (wl.N if tree else wl.K + 1)
+        cpu = {"value": cpu_rows / spent, "unit": "rows/s", "cores": 1, "kind": "oracle",
+               "sample": f"first {done} of {wl.B} sequences ({cpu_rows} verified rows) of the same "
+                         f"workload, fp64 oracle, single thread, {spent:.1f} s",
+               "parity_checked_sequences": checked}
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if elem == 2 else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
+                   "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
+                   "splits": args.splits or "auto", "rows_per_step": rows,
+                   "reduced_rows_per_step": reduced_rows},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
+                     "algorithmic_bytes_per_launch": logit_bytes},
+        "step_hbm_gbps": logit_bytes / (ms_per_step * 1e-3) / 1e9,
+        "wall_s": wall,
+        "mean_accept_len": float(out["accept_len"].float().mean()),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

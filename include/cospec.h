@@ -1,0 +1,214 @@
+/*
+ * cospec.h -- C ABI of the CoSpec verify-and-arbitrate step for MI355X (gfx950).
+ *
+ * Method: "Beyond the Target: From Imitation to Collaboration in Speculative
+ * Decoding".  In one speculative-decoding round (Section 3.1) the draft model
+ * proposes K tokens and the target model scores them in one teacher-forced
+ * pass, which gives K+1 next-token rows; with greedy decoding the target's
+ * verification token for position i is the argmax of target row i-1 and the
+ * mismatch indicator is Delta_i = 1[draft token i == that argmax].  CoSpec
+ * (Section 3.3) scores every mismatch with a learned head z_i = g_phi(h_i),
+ * accepts the draft token when sigma(z_i) > lambda (Eq. infer_thre; matches are
+ * always accepted, Eq. policy-prob), and ends the round at the first rejected
+ * mismatch (Eq. cospec_length): it emits the draft tokens before that position
+ * and the target token there, or all K draft tokens plus the bonus token.
+ *
+ * This library computes that step on the GPU from logits, draft tokens,
+ * arbitrator hidden states and head weights, and returns accept lengths and the
+ * emitted tokens, plus optional per-row and per-decision features.
+ *
+ * Conventions shared by every entry point
+ *  - Array arguments are DEVICE pointers on the current HIP device, owned by the
+ *    caller.  The library never allocates, frees or synchronises; all work is
+ *    enqueued on `stream` and the call returns before it runs.
+ *  - Scratch memory comes from the caller's `workspace` (size from the matching
+ *    *_workspace_size function).  Its contents need no initialisation and are
+ *    garbage afterwards.  Calls that may overlap in time need distinct workspaces.
+ *  - Host structs are read during the call and not retained.  There is no global
+ *    mutable state, so the library is reentrant.
+ *  - Every argument that lives on the host is checked before anything is
+ *    enqueued; an invalid call returns a negative status and enqueues nothing.
+ *    Launch failures return COSPEC_ERR_HIP.  No C++ exception crosses the ABI.
+ *  - Values that live in device memory (token ids, parent indices, row indices)
+ *    cannot be checked on the host.  Out-of-range values never cause an
+ *    out-of-bounds access; what they produce is stated per entry point.
+ *  - Logits must be finite (a precondition, not checked).
+ *  - Row layout: a logit row holds V entries followed by padding up to `ld`
+ *    entries; the pointer and ld * element size must be multiples of 16 bytes.
+ *  - Head dtype: hidden states, W1, b1 and w2 share head->dtype.
+ */
+#ifndef COSPEC_H
+#define COSPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define COSPEC_ABI_VERSION 1
+#define COSPEC_MAX_K 64      /* chain: draft tokens per block              */
+#define COSPEC_MAX_N 256     /* tree: nodes per tree, root included        */
+#define COSPEC_MAX_SPLITS 64 /* workgroups per logit row (tuning override) */
+
+typedef enum {
+    COSPEC_OK = 0,
+    COSPEC_ERR_INVALID_ARG = -1,  /* null/misaligned pointer, bad size, NaN lambda ... */
+    COSPEC_ERR_UNSUPPORTED = -2,  /* K, N or split count above the documented maximum   */
+    COSPEC_ERR_WORKSPACE = -3,    /* workspace missing, misaligned or too small         */
+    COSPEC_ERR_HIP = -4           /* a HIP call or kernel launch failed                 */
+} cospec_status;
+
+typedef enum { COSPEC_F32 = 0, COSPEC_BF16 = 1 } cospec_dtype;
+
+/*
+ * Arbitration head g_phi (Section 3.3).  The paper calls it a lightweight
+ * binary head on the arbitrator's hidden state without giving its form; this
+ * library reads it as a two-layer MLP with a ReLU:
+ *     z = w2 . max(W1 h + b1, 0) + b2
+ * d must be a multiple of 8 (bf16) or 4 (f32); w1 must be 16-byte aligned.
+ */
+typedef struct {
+    int32_t d;            /* hidden size (fan-in)                 */
+    int32_t h;            /* inner width                          */
+    cospec_dtype dtype;   /* of hidden states, w1, b1 and w2      */
+    const void *w1;       /* [h][d] row-major (nn.Linear layout)  */
+    const void *b1;       /* [h], or NULL for zeros               */
+    const void *w2;       /* [h]                                  */
+    float b2;             /* host scalar                          */
+} cospec_head;
+
+/*
+ * Optional outputs; any member may be NULL.  "Per target row" arrays are
+ * [B][K+1] (chain) or [B][N] (tree).  "Per draft row" arrays are [B][K]
+ * (chain) or [B][N] (tree; entries of leaf nodes, whose draft rows verify
+ * nothing and are not read, are -1 / NaN).  "Per decision" arrays are [B][K]
+ * (chain; entry i-1 is decision i) or [B][N] (tree; entry n is the decision on
+ * node n; entry 0, the root, reads delta 1, z_tilde +inf, policy 1, accept 1,
+ * log-probs NaN).
+ */
+typedef struct {
+    int32_t *tgt_argmax;   /* per target row: first index of the max           */
+    float *tgt_max;        /* per target row: max logit                        */
+    float *tgt_lse;        /* per target row: log sum exp (log-softmax norm.)  */
+    float *tgt_entropy;    /* per target row: Shannon entropy of softmax, nats */
+    int32_t *drf_argmax;   /* per draft row, as above                          */
+    float *drf_max;
+    float *drf_lse;
+    float *drf_entropy;
+    float *logp_tgt;       /* per decision: log p_T(draft token) (Section 3.4) */
+    float *logp_drf;       /* per decision: log p_D(draft token)               */
+    uint8_t *delta;        /* per decision: 1 if the draft token matches       */
+    float *z_tilde;        /* per decision: head logit, +inf on matches        */
+    float *policy;         /* per decision: sigma(z_tilde)                     */
+    uint8_t *accept;       /* per decision: a_i (1 on matches)                 */
+} cospec_features;
+
+/* Optional tuning and timing hooks; NULL means all defaults. */
+typedef struct {
+    hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ... */
+    hipEvent_t reduce_end;    /* ... and just after the vocabulary-reduction launch */
+    int32_t splits;           /* workgroups per logit row, 1..COSPEC_MAX_SPLITS; 0 = auto */
+} cospec_options;
+
+/* COSPEC_ABI_VERSION of the built library. */
+int32_t cospec_abi_version(void);
+
+/* Static string naming a status code (never NULL). */
+const char *cospec_status_string(int32_t status);
+
+/*
+ * Workspace bytes cospec_verify_block needs for these sizes (0 for invalid
+ * sizes).  The workspace must be 256-byte aligned.
+ */
+size_t cospec_verify_block_workspace_size(int32_t B, int32_t K, int32_t V, const cospec_head *head);
+
+/*
+ * One chain verify step over B blocks of K draft tokens (Sections 3.1 and 3.3).
+ *
+ *  target_logits  [B][K+1] rows: row j = target logits after the prefix and
+ *                 draft tokens 1..j; row K yields the bonus token.
+ *  draft_logits   [B][K] rows: row j = the draft logits token j+1 was drawn from.
+ *  logit_dtype, ld  element type of both logit arrays and their row stride in
+ *                 elements (ld >= V).
+ *  draft_tokens   [B][K] int32, the draft tokens 1..K.
+ *  hidden         [B][K][d] arbitrator hidden states; row i-1 feeds decision i.
+ *  head, lambda   the head and the acceptance threshold (any non-NaN value;
+ *                 lambda >= 1 never accepts a mismatch, lambda < 0 always does).
+ *  B >= 0, 0 <= K <= COSPEC_MAX_K, V >= 1.  With K = 0, draft_logits,
+ *                 draft_tokens and hidden may be NULL.
+ *  accept_len     [B] out: s in [1, K+1] (Eq. cospec_length).
+ *  out_tokens     [B][K+1] out: the emitted tokens, then -1.
+ *  feats, opts    optional (NULL).
+ *
+ * A draft token outside [0, V) never matches and is always rejected (its
+ * log-probabilities and z are NaN), so it is never emitted.
+ */
+cospec_status cospec_verify_block(const void *target_logits, const void *draft_logits,
+                                  cospec_dtype logit_dtype, int64_t ld,
+                                  const int32_t *draft_tokens, const void *hidden,
+                                  const cospec_head *head, float lambda, int32_t B, int32_t K,
+                                  int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                  const cospec_features *feats, const cospec_options *opts,
+                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes cospec_verify_tree needs (0 for invalid sizes). */
+size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const cospec_head *head);
+
+/*
+ * One tree verify step over B token trees of N nodes.  Trees are not in the
+ * paper; this applies its chain rule along every root path:
+ *  - node 0 is the root (the last verified token) and carries no decision;
+ *  - child c of node p is verified against argmax(target row p), its
+ *    log-probabilities come from rows p, and its head input is hidden row c;
+ *  - a node is reachable when every decision on its root path passes (a match,
+ *    or a mismatch whose draft token is accepted); the round accepts the
+ *    deepest reachable node n* (ties to the lowest node id) and emits the node
+ *    tokens along the path, then argmax(target row n*).
+ * On a path-shaped tree this is exactly the chain rule.
+ *
+ *  target_logits, draft_logits  [B][N] rows each (row n = distributions after
+ *                 node n).  Only draft rows of nodes that have a child are read.
+ *  parent         [B][N] int32: parent[0] = -1 and 0 <= parent[n] < n.
+ *  node_tokens    [B][N] int32 (entry 0 ignored).
+ *  hidden         [B][N][d] (row 0 ignored).
+ *  B >= 0, 1 <= N <= COSPEC_MAX_N, V >= 1.
+ *  accept_len     [B] out: depth(n*) + 1.
+ *  out_tokens     [B][N] out: path tokens then argmax(target row n*), then -1.
+ *  out_path       [B][N] out, nullable: node ids 0..n* along the path, then -1.
+ *
+ * A node whose parent index breaks 0 <= parent[n] < n, or whose token is
+ * outside [0, V), fails its decision (it and its subtree are unreachable).
+ */
+cospec_status cospec_verify_tree(const void *target_logits, const void *draft_logits,
+                                 cospec_dtype logit_dtype, int64_t ld, const int32_t *parent,
+                                 const int32_t *node_tokens, const void *hidden,
+                                 const cospec_head *head, float lambda, int32_t B, int32_t N,
+                                 int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                 int32_t *out_path, const cospec_features *feats,
+                                 const cospec_options *opts, void *workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes cospec_arbitrate needs (0 for invalid sizes). */
+size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head);
+
+/*
+ * The head alone (Section 3.3): for k < n_sel, with r = row_index[k] (or k when
+ * row_index is NULL), out_z[k] = g_phi(hidden row r) and out_accept[k] =
+ * 1[sigma(out_z[k]) > lambda] (Eq. infer_thre; no match override here).
+ *  hidden     [n_rows][d];  row_index [n_sel] int32 or NULL (then n_sel <= n_rows).
+ *  out_z      [n_sel] float; out_accept [n_sel] uint8 (either may be NULL).
+ * An index outside [0, n_rows) gives z = NaN and accept 0.
+ */
+cospec_status cospec_arbitrate(const void *hidden, int64_t n_rows, const int32_t *row_index,
+                               int64_t n_sel, const cospec_head *head, float lambda, float *out_z,
+                               uint8_t *out_accept, void *workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COSPEC_H */

@@ -1,0 +1,146 @@
+"""Comparison of a verify step's GPU outputs with the oracle's.
+
+TEST INFRASTRUCTURE ONLY (used by tests/, the package smoke check and the
+benchmark's parity re-check).  The rules:
+  * integers (argmax, Delta, accept flags outside the ambiguity band, accept
+    lengths, tokens, paths) must be bit-exact;
+  * where a decision lies within 1e-3 of the threshold, the GPU's
+    (accept_len, tokens[, path]) must be one member of the oracle's outcome set;
+  * floating-point features must agree within `contract` = 2e-3 * max(1, |ref|)
+    (the stated fp32-accumulation tolerance) and, as a tighter engineering
+    check that fp32 arithmetic easily meets, within the per-feature bounds in
+    TIGHT.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+CONTRACT_RTOL = 2e-3
+# (rtol, atol) per feature for the tighter check
+TIGHT = dict(max=(0.0, 0.0), lse=(1e-5, 1e-5), ent=(1e-5, 1e-4), logp=(1e-5, 1e-4),
+             z=(1e-4, 1e-4), pi=(0.0, 2e-5))
+
+
+class ParityError(AssertionError):
+    pass
+
+
+def _np(x):
+    if hasattr(x, "detach"):
+        x = x.detach().cpu().numpy()
+    return np.asarray(x)
+
+
+def _close(name, got, ref, kind, stats, mask=None):
+    got = _np(got).astype(np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if mask is not None:
+        got, ref = got[mask], ref[mask]
+    if got.size == 0:
+        return
+    err = np.abs(got - ref)
+    scale = np.maximum(1.0, np.abs(ref))
+    bad_contract = ~(err <= CONTRACT_RTOL * scale)
+    rtol, atol = TIGHT[kind]
+    bad_tight = ~(err <= atol + rtol * np.abs(ref))
+    stats[name] = float(np.max(err / scale))
+    if bad_contract.any() or bad_tight.any():
+        i = int(np.flatnonzero(bad_contract | bad_tight)[0])
+        raise ParityError(f"{name}: {int((bad_contract | bad_tight).sum())} of {got.size} outside "
+                          f"tolerance; first at flat index {i}: gpu {got.flat[i]!r} oracle {ref.flat[i]!r}")
+
+
+def _exact(name, got, ref, mask=None):
+    got = _np(got).astype(np.int64)
+    ref = np.asarray(ref).astype(np.int64)
+    if mask is not None:
+        got, ref = got[mask], ref[mask]
+    if not np.array_equal(got, ref):
+        i = int(np.flatnonzero(got != ref)[0])
+        raise ParityError(f"{name}: {int((got != ref).sum())} of {got.size} differ; first at flat "
+                          f"index {i}: gpu {got.flat[i]} oracle {ref.flat[i]}")
+
+
+def _decisions(gpu, ref, dmask, stats):
+    """Per-decision features; dmask selects real decision slots."""
+    delta = ref["delta"]
+    _exact("delta", gpu["delta"], delta, dmask)
+    _close("logp_tgt", gpu["logp_tgt"], ref["logp_tgt"], "logp", stats, dmask)
+    _close("logp_drf", gpu["logp_drf"], ref["logp_drf"], "logp", stats, dmask)
+    zt = _np(gpu["z_tilde"])
+    match = dmask & delta
+    mism = dmask & ~delta
+    if not np.all(np.isposinf(zt[match])):
+        raise ParityError("z_tilde must be +inf on matched decisions")
+    _close("z", zt, ref["z"], "z", stats, mism)
+    _close("policy", gpu["policy"], ref["pi"], "pi", stats, dmask)
+    acc = _np(gpu["accept"]).astype(bool)
+    firm = dmask & ~ref["ambiguous"]
+    _exact("accept", acc, ref["accept"], firm)
+    stats["ambiguous_decisions"] = int((dmask & ref["ambiguous"]).sum())
+
+
+def _outcomes(got_len, got_tok, got_path, ref, stats):
+    n_amb_seq = 0
+    for b, outs in enumerate(ref["outcomes"]):
+        key_len = int(got_len[b])
+        key_tok = tuple(int(x) for x in got_tok[b])
+        nominal = (int(ref["accept_len"][b]), tuple(int(x) for x in ref["tokens"][b]))
+        if got_path is not None:
+            key = (key_len, key_tok, tuple(int(x) for x in got_path[b]))
+            nominal = nominal + (tuple(int(x) for x in ref["path"][b]),)
+        else:
+            key = (key_len, key_tok)
+        if outs is None:
+            raise ParityError(f"sequence {b}: too many ambiguous decisions to enumerate")
+        if len(outs) > 1:
+            n_amb_seq += 1
+        if key not in outs:
+            raise ParityError(f"sequence {b}: gpu outcome {key} not among the oracle's {sorted(outs)[:4]} "
+                              f"(nominal {nominal})")
+    stats["sequences_with_ambiguity"] = n_amb_seq
+
+
+def check_block(gpu: dict, ref: dict) -> dict:
+    """GPU result of cospec_verify_block (features included) against oracle.verify_block."""
+    stats = {}
+    _exact("tgt_argmax", gpu["tgt_argmax"], ref["tgt_arg"])
+    _exact("drf_argmax", gpu["drf_argmax"], ref["drf_arg"])
+    _close("tgt_max", gpu["tgt_max"], ref["tgt_max"], "max", stats)
+    _close("drf_max", gpu["drf_max"], ref["drf_max"], "max", stats)
+    _close("tgt_lse", gpu["tgt_lse"], ref["tgt_lse"], "lse", stats)
+    _close("drf_lse", gpu["drf_lse"], ref["drf_lse"], "lse", stats)
+    _close("tgt_entropy", gpu["tgt_entropy"], ref["tgt_ent"], "ent", stats)
+    _close("drf_entropy", gpu["drf_entropy"], ref["drf_ent"], "ent", stats)
+    dmask = np.ones(ref["delta"].shape, bool)
+    _decisions(gpu, ref, dmask, stats)
+    _outcomes(_np(gpu["accept_len"]), _np(gpu["tokens"]), None, ref, stats)
+    return stats
+
+
+def check_tree(gpu: dict, ref: dict) -> dict:
+    """GPU result of cospec_verify_tree (features included) against oracle.verify_tree."""
+    stats = {}
+    _exact("tgt_argmax", gpu["tgt_argmax"], ref["tgt_arg"])
+    _close("tgt_max", gpu["tgt_max"], ref["tgt_max"], "max", stats)
+    _close("tgt_lse", gpu["tgt_lse"], ref["tgt_lse"], "lse", stats)
+    _close("tgt_entropy", gpu["tgt_entropy"], ref["tgt_ent"], "ent", stats)
+    internal = ref["internal"]
+    _exact("drf_argmax", gpu["drf_argmax"], ref["drf_arg"])          # -1 on leaves on both sides
+    _close("drf_lse", gpu["drf_lse"], ref["drf_lse"], "lse", stats, internal)
+    _close("drf_entropy", gpu["drf_entropy"], ref["drf_ent"], "ent", stats, internal)
+    if not np.all(np.isnan(_np(gpu["drf_lse"])[~internal])):
+        raise ParityError("draft statistics of leaf nodes must be NaN")
+    dmask = np.ones(ref["delta"].shape, bool)
+    dmask[:, 0] = False
+    _decisions(gpu, ref, dmask, stats)
+    _outcomes(_np(gpu["accept_len"]), _np(gpu["tokens"]), _np(gpu["path"]), ref, stats)
+    return stats
+
+
+def check_outputs_only(gpu: dict, ref: dict, tree: bool = False) -> dict:
+    """Accept lengths and tokens alone (for calls made without features)."""
+    stats = {}
+    _outcomes(_np(gpu["accept_len"]), _np(gpu["tokens"]), _np(gpu["path"]) if tree else None,
+              ref, stats)
+    return stats

@@ -1,0 +1,11 @@
+"""CoSpec verify-and-arbitrate step on MI355X (gfx950).
+
+The computation runs in libcospec.so (HIP kernels behind the C ABI of
+include/cospec.h); `binding` marshals torch tensors into it, `workloads` draws
+seeded synthetic inputs.
+"""
+from .binding import (CospecError, arbitrate, lib, prepare_block, prepare_tree, verify_block,
+                      verify_tree)
+
+__all__ = ["CospecError", "arbitrate", "lib", "prepare_block", "prepare_tree", "verify_block",
+           "verify_tree"]

@@ -1,0 +1,267 @@
+"""Thin ctypes binding of libcospec.so (include/cospec.h).
+
+Marshalling only: torch tensors supply device memory and the current stream,
+this module turns them into pointers and sizes and calls the C ABI.  Every step
+of the computation runs in the library's HIP kernels.  There is no fallback: if
+the library cannot be loaded or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+from . import _build
+
+__all__ = ["lib", "verify_block", "verify_tree", "arbitrate", "CospecError", "Prepared",
+           "prepare_block", "prepare_tree", "status_string", "MAX_K", "MAX_N", "MAX_SPLITS"]
+
+MAX_K, MAX_N, MAX_SPLITS = 64, 256, 64
+_F32, _BF16 = 0, 1
+_lib = None
+
+
+class CospecError(RuntimeError):
+    pass
+
+
+class _Head(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("h", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+                ("b2", ctypes.c_float)]
+
+
+_FEATURE_FIELDS = ["tgt_argmax", "tgt_max", "tgt_lse", "tgt_entropy", "drf_argmax", "drf_max",
+                   "drf_lse", "drf_entropy", "logp_tgt", "logp_drf", "delta", "z_tilde", "policy",
+                   "accept"]
+
+
+class _Features(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_void_p) for f in _FEATURE_FIELDS]
+
+
+class _Options(ctypes.Structure):
+    _fields_ = [("reduce_begin", ctypes.c_void_p), ("reduce_end", ctypes.c_void_p),
+                ("splits", ctypes.c_int32)]
+
+
+def lib():
+    """The loaded library (built first if no build exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB)
+        P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        HP = ctypes.POINTER(_Head)
+        L.cospec_abi_version.restype = I32
+        L.cospec_abi_version.argtypes = []
+        L.cospec_status_string.restype = ctypes.c_char_p
+        L.cospec_status_string.argtypes = [I32]
+        L.cospec_verify_block_workspace_size.restype = SZ
+        L.cospec_verify_block_workspace_size.argtypes = [I32, I32, I32, HP]
+        L.cospec_verify_tree_workspace_size.restype = SZ
+        L.cospec_verify_tree_workspace_size.argtypes = [I32, I32, I32, HP]
+        L.cospec_arbitrate_workspace_size.restype = SZ
+        L.cospec_arbitrate_workspace_size.argtypes = [I64, HP]
+        L.cospec_verify_block.restype = I32
+        L.cospec_verify_block.argtypes = [P, P, I32, I64, P, P, HP, ctypes.c_float, I32, I32, I32,
+                                          P, P, ctypes.POINTER(_Features),
+                                          ctypes.POINTER(_Options), P, SZ, P]
+        L.cospec_verify_tree.restype = I32
+        L.cospec_verify_tree.argtypes = [P, P, I32, I64, P, P, P, HP, ctypes.c_float, I32, I32,
+                                         I32, P, P, P, ctypes.POINTER(_Features),
+                                         ctypes.POINTER(_Options), P, SZ, P]
+        L.cospec_arbitrate.restype = I32
+        L.cospec_arbitrate.argtypes = [P, I64, P, I64, HP, ctypes.c_float, P, P, P, SZ, P]
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().cospec_status_string(code).decode()
+
+
+def _check(code: int, what: str):
+    if code != 0:
+        raise CospecError(f"{what}: {status_string(code)} ({code})")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return _BF16
+    if t.dtype == torch.float32:
+        return _F32
+    raise TypeError(f"logits, hidden states and head weights are bf16 or f32, got {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _head_struct(head) -> _Head:
+    w1, b1, w2, b2 = head.w1, head.b1, head.w2, head.b2
+    for t in (w1, w2) + ((b1,) if b1 is not None else ()):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("head weights must be contiguous device tensors")
+    return _Head(int(w1.shape[1]), int(w1.shape[0]), _dtype_code(w1), _ptr(w1), _ptr(b1),
+                 _ptr(w2), float(b2))
+
+
+def _row_stride(t: torch.Tensor) -> int:
+    """Row stride in elements of a [B, R, V] logit tensor whose rows may be padded."""
+    if t.dim() != 3 or (t.shape[2] > 1 and t.stride(2) != 1):
+        raise ValueError("logits must be [B, R, V] with unit element stride")
+    if t.shape[0] > 1 and t.shape[1] > 0 and t.stride(0) != t.shape[1] * t.stride(1):
+        raise ValueError("logit rows must be uniformly spaced: stride(0) == R * stride(1)")
+    return int(t.stride(1))
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+class Prepared:
+    """Pre-marshalled arguments of one verify call: outputs, features and workspace
+    are allocated once, so `launch()` enqueues the step with no allocation."""
+
+    def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, opts):
+        self._fn = fn
+        self._args = args_before_feats
+        self.outputs = outputs
+        self.features = feats
+        self._feats = feats_struct
+        self.workspace = workspace
+        self._opts = opts
+        self._keep = []
+
+    def launch(self, begin_event=None, end_event=None, splits: Optional[int] = None):
+        opts = self._opts
+        if begin_event is not None or end_event is not None or splits is not None:
+            opts = _Options(None if begin_event is None else begin_event.cuda_event,
+                            None if end_event is None else end_event.cuda_event,
+                            int(splits or (self._opts.splits if self._opts else 0)))
+        code = self._fn(*self._args, ctypes.byref(self._feats) if self._feats is not None else None,
+                        ctypes.byref(opts) if opts is not None else None,
+                        _ptr(self.workspace), self.workspace.numel(), _stream())
+        _check(code, self._fn.__name__)
+
+    def result(self) -> dict:
+        out = dict(self.outputs)
+        out.update(self.features or {})
+        return out
+
+
+def _features(alloc: bool, dev, B, RT, RD, D):
+    if not alloc:
+        return None, None
+    i32, f32, u8 = torch.int32, torch.float32, torch.uint8
+    shapes = dict(tgt_argmax=((B, RT), i32), tgt_max=((B, RT), f32), tgt_lse=((B, RT), f32),
+                  tgt_entropy=((B, RT), f32), drf_argmax=((B, RD), i32), drf_max=((B, RD), f32),
+                  drf_lse=((B, RD), f32), drf_entropy=((B, RD), f32), logp_tgt=((B, D), f32),
+                  logp_drf=((B, D), f32), delta=((B, D), u8), z_tilde=((B, D), f32),
+                  policy=((B, D), f32), accept=((B, D), u8))
+    feats = {k: torch.empty(s, dtype=t, device=dev) for k, (s, t) in shapes.items()}
+    st = _Features(*[_ptr(feats[f]) for f in _FEATURE_FIELDS])
+    return feats, st
+
+
+def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
+                  splits: int = 0) -> Prepared:
+    B, R, V = target.shape
+    K = R - 1
+    ld = _row_stride(target)
+    if K > 0 and _row_stride(draft) != ld:
+        raise ValueError("target and draft rows must share one stride")
+    if K > 0 and (tuple(draft.shape) != (B, K, V) or tuple(draft_tokens.shape) != (B, K)
+                  or draft_tokens.dtype != torch.int32 or not draft_tokens.is_contiguous()
+                  or hidden.shape[:2] != (B, K) or not hidden.is_contiguous()):
+        raise ValueError("shape/dtype mismatch between target, draft, draft_tokens and hidden")
+    dev = target.device
+    hs = _head_struct(head)
+    L = lib()
+    ws_bytes = L.cospec_verify_block_workspace_size(B, K, V, ctypes.byref(hs))
+    if ws_bytes == 0 and B > 0:
+        raise CospecError("invalid sizes for cospec_verify_block")
+    workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    outputs = dict(accept_len=torch.empty(B, dtype=torch.int32, device=dev),
+                   tokens=torch.empty((B, K + 1), dtype=torch.int32, device=dev))
+    feats, fst = _features(features, dev, B, K + 1, K, K)
+    args = (_ptr(target), _ptr(draft) if K > 0 else None, _dtype_code(target), ld,
+            _ptr(draft_tokens) if K > 0 else None, _ptr(hidden) if K > 0 else None,
+            ctypes.byref(hs), float(lam), B, K, V, _ptr(outputs["accept_len"]),
+            _ptr(outputs["tokens"]))
+    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace,
+                 _Options(None, None, int(splits)) if splits else None)
+    p._keep = [hs, target, draft, draft_tokens, hidden, head]
+    return p
+
+
+def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
+                 features: bool = True, splits: int = 0) -> Prepared:
+    B, N, V = target.shape
+    ld = _row_stride(target)
+    if _row_stride(draft) != ld or tuple(draft.shape) != (B, N, V):
+        raise ValueError("target and draft must both be [B, N, V] with one row stride")
+    for t in (parent, node_tokens):
+        if tuple(t.shape) != (B, N) or t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError("parent and node_tokens must be contiguous int32 [B, N]")
+    if hidden.shape[:2] != (B, N) or not hidden.is_contiguous():
+        raise ValueError("hidden must be contiguous [B, N, d]")
+    dev = target.device
+    hs = _head_struct(head)
+    L = lib()
+    ws_bytes = L.cospec_verify_tree_workspace_size(B, N, V, ctypes.byref(hs))
+    if ws_bytes == 0 and B > 0:
+        raise CospecError("invalid sizes for cospec_verify_tree")
+    workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    outputs = dict(accept_len=torch.empty(B, dtype=torch.int32, device=dev),
+                   tokens=torch.empty((B, N), dtype=torch.int32, device=dev),
+                   path=torch.empty((B, N), dtype=torch.int32, device=dev))
+    feats, fst = _features(features, dev, B, N, N, N)
+    args = (_ptr(target), _ptr(draft), _dtype_code(target), ld, _ptr(parent), _ptr(node_tokens),
+            _ptr(hidden), ctypes.byref(hs), float(lam), B, N, V, _ptr(outputs["accept_len"]),
+            _ptr(outputs["tokens"]), _ptr(outputs["path"]))
+    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace,
+                 _Options(None, None, int(splits)) if splits else None)
+    p._keep = [hs, target, draft, parent, node_tokens, hidden, head]
+    return p
+
+
+def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
+                 splits: int = 0) -> dict:
+    """cospec_verify_block on device tensors; returns accept_len, tokens (+ features)."""
+    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits)
+    p.launch()
+    return p.result()
+
+
+def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
+                features: bool = True, splits: int = 0) -> dict:
+    """cospec_verify_tree on device tensors; returns accept_len, tokens, path (+ features)."""
+    p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits)
+    p.launch()
+    return p.result()
+
+
+def arbitrate(hidden, head, lam: float, row_index: Optional[torch.Tensor] = None) -> dict:
+    """cospec_arbitrate: head logits and threshold decisions for selected hidden rows."""
+    h2 = hidden.reshape(-1, hidden.shape[-1])
+    if not h2.is_contiguous():
+        raise ValueError("hidden must be contiguous")
+    n_rows = h2.shape[0]
+    if row_index is not None and (row_index.dtype != torch.int32 or not row_index.is_contiguous()):
+        raise ValueError("row_index must be contiguous int32")
+    n_sel = n_rows if row_index is None else row_index.numel()
+    hs = _head_struct(head)
+    L = lib()
+    ws = torch.empty(max(L.cospec_arbitrate_workspace_size(n_sel, ctypes.byref(hs)), 256),
+                     dtype=torch.uint8, device=hidden.device)
+    z = torch.empty(n_sel, dtype=torch.float32, device=hidden.device)
+    acc = torch.empty(n_sel, dtype=torch.uint8, device=hidden.device)
+    code = L.cospec_arbitrate(_ptr(h2), n_rows, _ptr(row_index), n_sel, ctypes.byref(hs),
+                              float(lam), _ptr(z), _ptr(acc), _ptr(ws), ws.numel(), _stream())
+    _check(code, "cospec_arbitrate")
+    return dict(z=z, accept=acc)

@@ -1,0 +1,344 @@
+// C ABI of the verify-and-arbitrate step: host-side validation, workspace
+// carving and the launch sequence.  Declared in include/cospec.h.
+//
+// verify_block / verify_tree enqueue, on the caller's stream:
+//   1. k_vocab_reduce   every needed logit row once, split over `splits`
+//                       workgroups per row -> partial (max, argmax, S, T)
+//   2. k_decide         one workgroup per sequence: merge, features, Delta,
+//                       mismatch compaction (device-side count M)
+//   3. k_head           MFMA head over the M compacted rows (skipped when the
+//                       threshold decides every mismatch by itself and no
+//                       score is requested)
+//   4. k_chain_scan / k_tree_scan   verdicts, first stop, emission
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/cospec.h"
+#include "launch.h"
+
+using namespace cospec;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
+constexpr int64_t kAutoBlocks = 2048;         // aim: 8 workgroups per CU on 256 CUs
+
+inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+inline int elem_bytes(cospec_dtype t) { return t == COSPEC_BF16 ? 2 : 4; }
+
+inline bool dtype_ok(cospec_dtype t) { return t == COSPEC_F32 || t == COSPEC_BF16; }
+
+cospec_status check_head(const cospec_head *hd) {
+    if (!hd || !dtype_ok(hd->dtype) || hd->d <= 0 || hd->h <= 0 || !hd->w1 || !hd->w2)
+        return COSPEC_ERR_INVALID_ARG;
+    const int eb = elem_bytes(hd->dtype);
+    if ((static_cast<int64_t>(hd->d) * eb) % 16 != 0 || !aligned(hd->w1, 16) || !aligned(hd->w2, eb) ||
+        (hd->b1 && !aligned(hd->b1, eb)))
+        return COSPEC_ERR_INVALID_ARG;
+    return COSPEC_OK;
+}
+
+inline int n_htiles(const cospec_head *hd) { return (hd->h + kHeadTileN - 1) / kHeadTileN; }
+
+// Workspace carving shared by the size query and the call.
+struct Layout {
+    size_t partials, tgt_arg, state, listpos, list, count, zpart, total;
+    int64_t partial_slots;
+};
+
+Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head *hd) {
+    Layout L{};
+    L.partial_slots = rows > kMinPartialSlots ? rows : kMinPartialSlots;
+    size_t off = 0;
+    L.partials = off; off += round_up(static_cast<size_t>(L.partial_slots) * 16);
+    L.tgt_arg = off;  off += round_up(static_cast<size_t>(B * RT) * 4);
+    L.state = off;    off += round_up(static_cast<size_t>(B * D));
+    L.listpos = off;  off += round_up(static_cast<size_t>(B * D) * 4);
+    L.list = off;     off += round_up(static_cast<size_t>(B * D) * 4);
+    L.count = off;    off += kAlign;
+    L.zpart = off;    off += round_up(static_cast<size_t>(n_htiles(hd)) * static_cast<size_t>(B * D) * 4);
+    L.total = off;
+    return L;
+}
+
+int32_t auto_splits(int64_t rows, int64_t nvec) {
+    int64_t s = (kAutoBlocks + rows - 1) / rows;
+    const int64_t by_len = nvec / kReduceThreads;    // at least one vector per lane
+    if (s > by_len) s = by_len;
+    if (s > COSPEC_MAX_SPLITS) s = COSPEC_MAX_SPLITS;
+    if (s < 1) s = 1;
+    return static_cast<int32_t>(s);
+}
+
+bool feats_aligned(const cospec_features *f) {
+    if (!f) return true;
+    const void *p4[] = {f->tgt_argmax, f->tgt_max, f->tgt_lse, f->tgt_entropy, f->drf_argmax, f->drf_max,
+                        f->drf_lse, f->drf_entropy, f->logp_tgt, f->logp_drf, f->z_tilde, f->policy};
+    for (const void *p : p4)
+        if (p && !aligned(p, 4)) return false;
+    return true;
+}
+
+struct Common {
+    const void *tgt, *drf;
+    cospec_dtype dt;
+    int64_t ld;
+    const void *hidden;
+    const cospec_head *head;
+    float lambda;
+    int32_t B, V;
+    int64_t RT, RD, D;          // per sequence
+    int is_tree;
+    const int32_t *parent, *tokens;
+    const cospec_features *feats;
+    const cospec_options *opts;
+    void *ws;
+    size_t ws_bytes;
+    hipStream_t stream;
+};
+
+cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int32_t *out_path) {
+    const int eb = elem_bytes(c.dt);
+    const int64_t rows = static_cast<int64_t>(c.B) * (c.RT + c.RD);
+    const int64_t nvec = static_cast<int64_t>(c.V) * eb / 16;
+    int32_t splits = auto_splits(rows, nvec);
+    if (c.opts && c.opts->splits) {
+        if (c.opts->splits < 0 || c.opts->splits > COSPEC_MAX_SPLITS) return COSPEC_ERR_UNSUPPORTED;
+        splits = c.opts->splits;
+    }
+    const Layout L = layout(rows, c.B, c.RT, c.D, c.head);
+    if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    if (!c.ws || !aligned(c.ws, kAlign) || c.ws_bytes < L.total) return COSPEC_ERR_WORKSPACE;
+
+    char *ws = static_cast<char *>(c.ws);
+    float4 *partials = reinterpret_cast<float4 *>(ws + L.partials);
+    int32_t *tgt_arg = reinterpret_cast<int32_t *>(ws + L.tgt_arg);
+    uint8_t *state = reinterpret_cast<uint8_t *>(ws + L.state);
+    int32_t *listpos = reinterpret_cast<int32_t *>(ws + L.listpos);
+    int32_t *list = reinterpret_cast<int32_t *>(ws + L.list);
+    int32_t *count = reinterpret_cast<int32_t *>(ws + L.count);
+    float *zpart = reinterpret_cast<float *>(ws + L.zpart);
+
+    const cospec_features F = c.feats ? *c.feats : cospec_features{};
+    const bool decisions = c.B > 0 && (c.is_tree ? c.D > 1 : c.D > 0);
+    const bool lambda_decides = !(c.lambda >= 0.0f && c.lambda < 1.0f);
+    const bool want_scores = F.z_tilde || F.policy;
+    const bool head = decisions && (!lambda_decides || want_scores);
+
+    ReduceArgs ra{};
+    ra.tgt = static_cast<const char *>(c.tgt);
+    ra.drf = static_cast<const char *>(c.drf);
+    ra.ld_bytes = c.ld * eb;
+    ra.V = c.V;
+    ra.n_tgt_rows = static_cast<int32_t>(c.B * c.RT);
+    ra.n_drf_rows = static_cast<int32_t>(c.B * c.RD);
+    ra.parent = c.is_tree ? c.parent : nullptr;
+    ra.N = static_cast<int32_t>(c.RT);
+    ra.splits = splits;
+    ra.vec_per_split = static_cast<int32_t>((nvec + splits - 1) / splits);
+    ra.partials = partials;
+    ra.reset_counter = count;
+
+    hipError_t e;
+    if (c.opts && c.opts->reduce_begin && (e = hipEventRecord(c.opts->reduce_begin, c.stream)) != hipSuccess)
+        return COSPEC_ERR_HIP;
+    if ((e = launch_reduce(static_cast<Dtype>(c.dt), ra, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+    if (c.opts && c.opts->reduce_end && (e = hipEventRecord(c.opts->reduce_end, c.stream)) != hipSuccess)
+        return COSPEC_ERR_HIP;
+
+    DecideArgs da{};
+    da.tgt = ra.tgt;
+    da.drf = ra.drf;
+    da.ld_bytes = ra.ld_bytes;
+    da.V = c.V;
+    da.B = c.B;
+    da.RT = static_cast<int32_t>(c.RT);
+    da.RD = static_cast<int32_t>(c.RD);
+    da.D = static_cast<int32_t>(c.D);
+    da.is_tree = c.is_tree;
+    da.parent = c.parent;
+    da.tokens = c.tokens;
+    da.partials = partials;
+    da.splits = splits;
+    da.score_mismatch = head;
+    da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
+    da.drf_argmax = F.drf_argmax; da.drf_max = F.drf_max; da.drf_lse = F.drf_lse; da.drf_ent = F.drf_entropy;
+    da.logp_tgt = F.logp_tgt; da.logp_drf = F.logp_drf; da.delta = F.delta;
+    da.ws_tgt_arg = tgt_arg;
+    da.ws_state = state;
+    da.ws_listpos = listpos;
+    da.ws_list = list;
+    da.ws_count = count;
+    if ((e = launch_decide(static_cast<Dtype>(c.dt), da, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+
+    const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
+    if (head) {
+        HeadArgs ha{};
+        ha.hidden = c.hidden;
+        ha.n_rows = m_cap;
+        ha.list = list;
+        ha.count_dev = count;
+        ha.count_host = 0;
+        ha.m_cap = m_cap;
+        ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2;
+        ha.d = c.head->d; ha.h = c.head->h;
+        ha.zpart = zpart;
+        if ((e = launch_head(static_cast<Dtype>(c.head->dtype), ha, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+    }
+
+    if (c.is_tree) {
+        TreeScanArgs ta{};
+        ta.B = c.B; ta.N = static_cast<int32_t>(c.RT);
+        ta.parent = c.parent; ta.node_tokens = c.tokens;
+        ta.ws_state = state; ta.ws_listpos = listpos;
+        ta.zpart = zpart; ta.n_htiles = n_htiles(c.head); ta.m_cap = m_cap;
+        ta.head_ran = head; ta.b2 = c.head->b2; ta.lambda = c.lambda;
+        ta.ws_tgt_arg = tgt_arg;
+        ta.accept_len = accept_len; ta.out_tokens = out_tokens; ta.out_path = out_path;
+        ta.z_tilde = F.z_tilde; ta.policy = F.policy; ta.accept = F.accept;
+        if ((e = launch_tree_scan(ta, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+    } else {
+        ChainScanArgs sa{};
+        sa.B = c.B; sa.K = static_cast<int32_t>(c.D);
+        sa.ws_state = state; sa.ws_listpos = listpos;
+        sa.zpart = zpart; sa.n_htiles = n_htiles(c.head); sa.m_cap = m_cap;
+        sa.head_ran = head; sa.b2 = c.head->b2; sa.lambda = c.lambda;
+        sa.tokens = c.tokens; sa.ws_tgt_arg = tgt_arg;
+        sa.accept_len = accept_len; sa.out_tokens = out_tokens;
+        sa.z_tilde = F.z_tilde; sa.policy = F.policy; sa.accept = F.accept;
+        if ((e = launch_chain_scan(sa, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+    }
+    return COSPEC_OK;
+}
+
+cospec_status check_logits(const void *p, cospec_dtype dt, int64_t ld, int32_t V) {
+    if (!p || !aligned(p, 16)) return COSPEC_ERR_INVALID_ARG;
+    if (ld < V || (ld * elem_bytes(dt)) % 16 != 0) return COSPEC_ERR_INVALID_ARG;
+    return COSPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cospec_abi_version(void) { return COSPEC_ABI_VERSION; }
+
+const char *cospec_status_string(int32_t status) {
+    switch (status) {
+        case COSPEC_OK: return "ok";
+        case COSPEC_ERR_INVALID_ARG: return "invalid argument";
+        case COSPEC_ERR_UNSUPPORTED: return "unsupported size";
+        case COSPEC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case COSPEC_ERR_HIP: return "HIP error";
+        default: return "unknown status";
+    }
+}
+
+size_t cospec_verify_block_workspace_size(int32_t B, int32_t K, int32_t V, const cospec_head *head) {
+    if (B < 0 || K < 0 || K > COSPEC_MAX_K || V < 1 || check_head(head) != COSPEC_OK) return 0;
+    return layout(static_cast<int64_t>(B) * (2 * K + 1), B, K + 1, K, head).total;
+}
+
+size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const cospec_head *head) {
+    if (B < 0 || N < 1 || N > COSPEC_MAX_N || V < 1 || check_head(head) != COSPEC_OK) return 0;
+    return layout(static_cast<int64_t>(B) * 2 * N, B, N, N, head).total;
+}
+
+cospec_status cospec_verify_block(const void *target_logits, const void *draft_logits,
+                                  cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
+                                  const void *hidden, const cospec_head *head, float lambda, int32_t B,
+                                  int32_t K, int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                  const cospec_features *feats, const cospec_options *opts, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+    if (!dtype_ok(logit_dtype) || B < 0 || K < 0 || V < 1 || isnan(lambda)) return COSPEC_ERR_INVALID_ARG;
+    if (K > COSPEC_MAX_K) return COSPEC_ERR_UNSUPPORTED;
+    cospec_status st = check_head(head);
+    if (st != COSPEC_OK) return st;
+    if (B == 0) return COSPEC_OK;
+    if ((st = check_logits(target_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+    if (K > 0) {
+        if ((st = check_logits(draft_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+        if (!draft_tokens || !aligned(draft_tokens, 4) || !hidden || !aligned(hidden, 16))
+            return COSPEC_ERR_INVALID_ARG;
+    }
+    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4) || !feats_aligned(feats))
+        return COSPEC_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(B) * (2 * K + 1) > INT32_MAX / 2) return COSPEC_ERR_UNSUPPORTED;
+    Common c{};
+    c.tgt = target_logits; c.drf = draft_logits; c.dt = logit_dtype; c.ld = ld;
+    c.hidden = hidden; c.head = head; c.lambda = lambda; c.B = B; c.V = V;
+    c.RT = K + 1; c.RD = K; c.D = K; c.is_tree = 0;
+    c.parent = nullptr; c.tokens = draft_tokens;
+    c.feats = feats; c.opts = opts; c.ws = workspace; c.ws_bytes = workspace_bytes; c.stream = stream;
+    return run(c, accept_len, out_tokens, nullptr);
+}
+
+cospec_status cospec_verify_tree(const void *target_logits, const void *draft_logits,
+                                 cospec_dtype logit_dtype, int64_t ld, const int32_t *parent,
+                                 const int32_t *node_tokens, const void *hidden, const cospec_head *head,
+                                 float lambda, int32_t B, int32_t N, int32_t V, int32_t *accept_len,
+                                 int32_t *out_tokens, int32_t *out_path, const cospec_features *feats,
+                                 const cospec_options *opts, void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+    if (!dtype_ok(logit_dtype) || B < 0 || N < 1 || V < 1 || isnan(lambda)) return COSPEC_ERR_INVALID_ARG;
+    if (N > COSPEC_MAX_N) return COSPEC_ERR_UNSUPPORTED;
+    cospec_status st = check_head(head);
+    if (st != COSPEC_OK) return st;
+    if (B == 0) return COSPEC_OK;
+    if ((st = check_logits(target_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+    if ((st = check_logits(draft_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+    if (!parent || !aligned(parent, 4) || !node_tokens || !aligned(node_tokens, 4) || !hidden || !aligned(hidden, 16))
+        return COSPEC_ERR_INVALID_ARG;
+    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4) ||
+        (out_path && !aligned(out_path, 4)) || !feats_aligned(feats))
+        return COSPEC_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(B) * 2 * N > INT32_MAX / 2) return COSPEC_ERR_UNSUPPORTED;
+    Common c{};
+    c.tgt = target_logits; c.drf = draft_logits; c.dt = logit_dtype; c.ld = ld;
+    c.hidden = hidden; c.head = head; c.lambda = lambda; c.B = B; c.V = V;
+    c.RT = N; c.RD = N; c.D = N; c.is_tree = 1;
+    c.parent = parent; c.tokens = node_tokens;
+    c.feats = feats; c.opts = opts; c.ws = workspace; c.ws_bytes = workspace_bytes; c.stream = stream;
+    return run(c, accept_len, out_tokens, out_path);
+}
+
+size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head) {
+    if (n_sel < 0 || check_head(head) != COSPEC_OK) return 0;
+    return round_up(static_cast<size_t>(n_htiles(head)) * static_cast<size_t>(n_sel) * 4) + kAlign;
+}
+
+cospec_status cospec_arbitrate(const void *hidden, int64_t n_rows, const int32_t *row_index, int64_t n_sel,
+                               const cospec_head *head, float lambda, float *out_z, uint8_t *out_accept,
+                               void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (n_rows < 0 || n_sel < 0 || isnan(lambda)) return COSPEC_ERR_INVALID_ARG;
+    cospec_status st = check_head(head);
+    if (st != COSPEC_OK) return st;
+    if (!row_index && n_sel > n_rows) return COSPEC_ERR_INVALID_ARG;
+    if (n_sel > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    if (n_sel == 0) return COSPEC_OK;
+    if (!hidden || !aligned(hidden, 16) || (row_index && !aligned(row_index, 4)) || (out_z && !aligned(out_z, 4)))
+        return COSPEC_ERR_INVALID_ARG;
+    const size_t need = cospec_arbitrate_workspace_size(n_sel, head);
+    if (!workspace || !aligned(workspace, kAlign) || workspace_bytes < need) return COSPEC_ERR_WORKSPACE;
+
+    float *zpart = static_cast<float *>(workspace);
+    HeadArgs ha{};
+    ha.hidden = hidden; ha.n_rows = n_rows; ha.list = row_index;
+    ha.count_dev = nullptr; ha.count_host = n_sel; ha.m_cap = n_sel;
+    ha.w1 = head->w1; ha.b1 = head->b1; ha.w2 = head->w2; ha.d = head->d; ha.h = head->h;
+    ha.zpart = zpart;
+    if (launch_head(static_cast<Dtype>(head->dtype), ha, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    ArbFinishArgs fa{};
+    fa.n_sel = n_sel; fa.n_rows = n_rows; fa.row_index = row_index;
+    fa.zpart = zpart; fa.n_htiles = n_htiles(head); fa.m_cap = n_sel;
+    fa.b2 = head->b2; fa.lambda = lambda; fa.out_z = out_z; fa.out_accept = out_accept;
+    if (launch_arb_finish(fa, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    return COSPEC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// Internal interface between the C ABI (cospec_api.hip) and the kernel files.
+// Not installed; the public interface is include/cospec.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cospec {
+
+constexpr int kReduceThreads = 256;   // vocabulary-reduction workgroup
+constexpr int kDecideThreads = 256;   // one workgroup per sequence / tree
+constexpr int kHeadTileM = 64;        // head GEMM workgroup tile: rows
+constexpr int kHeadTileN = 64;        //                            columns of W1
+constexpr int kMaxSeqRows = 256;      // rows per sequence / nodes per tree held in LDS
+
+enum Dtype : int32_t { kF32 = 0, kBF16 = 1 };
+
+// Per-decision state byte written by the decide kernel.
+enum : uint8_t { kStateMismatch = 0, kStateMatch = 1, kStateReject = 2 };
+
+struct ReduceArgs {
+    const char *tgt;           // target rows
+    const char *drf;           // draft rows
+    int64_t ld_bytes;          // row stride in bytes (multiple of 16)
+    int32_t V;
+    int32_t n_tgt_rows;        // B * rows-per-sequence of target
+    int32_t n_drf_rows;        // B * rows-per-sequence of draft
+    const int32_t *parent;     // tree: [B][N]; draft rows of leaves are skipped
+    int32_t N;                 // tree nodes per tree
+    int32_t splits;            // workgroups per row
+    int32_t vec_per_split;     // 16-byte vectors per split
+    float4 *partials;          // [rows][splits] {max, argmax bits, S, T}
+    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter)
+};
+
+struct DecideArgs {
+    const char *tgt;
+    const char *drf;
+    int64_t ld_bytes;
+    int32_t V;
+    int32_t B;
+    int32_t RT;                // target rows per sequence (K+1 or N)
+    int32_t RD;                // draft rows per sequence (K or N)
+    int32_t D;                 // decision slots per sequence (K, or N with the root)
+    int32_t is_tree;
+    const int32_t *parent;     // tree only
+    const int32_t *tokens;     // chain [B][K], tree [B][N]
+    const float4 *partials;
+    int32_t splits;
+    int32_t score_mismatch;    // compact mismatches for the head
+    int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent;
+    int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent;
+    float *logp_tgt; float *logp_drf; uint8_t *delta;
+    int32_t *ws_tgt_arg;       // [B*RT]
+    uint8_t *ws_state;         // [B*D]
+    int32_t *ws_listpos;       // [B*D] position in the compacted list or -1
+    int32_t *ws_list;          // [B*D] compacted hidden-row ids
+    int32_t *ws_count;         // compacted length M
+};
+
+struct HeadArgs {
+    const void *hidden;        // [n_rows][d]
+    int64_t n_rows;
+    const int32_t *list;       // selected rows, or null = identity
+    const int32_t *count_dev;  // M on the device, or null
+    int64_t count_host;        // M when count_dev is null
+    int64_t m_cap;             // capacity of the list / zpart row dimension
+    const void *w1; const void *b1; const void *w2;
+    int32_t d, h;
+    float *zpart;              // [ceil(h/64)][m_cap]
+};
+
+struct ChainScanArgs {
+    int32_t B, K;
+    const uint8_t *ws_state;
+    const int32_t *ws_listpos;
+    const float *zpart; int32_t n_htiles; int64_t m_cap;
+    int32_t head_ran;
+    float b2, lambda;
+    const int32_t *tokens;
+    const int32_t *ws_tgt_arg;
+    int32_t *accept_len; int32_t *out_tokens;
+    float *z_tilde; float *policy; uint8_t *accept;
+};
+
+struct TreeScanArgs {
+    int32_t B, N;
+    const int32_t *parent;
+    const int32_t *node_tokens;
+    const uint8_t *ws_state;
+    const int32_t *ws_listpos;
+    const float *zpart; int32_t n_htiles; int64_t m_cap;
+    int32_t head_ran;
+    float b2, lambda;
+    const int32_t *ws_tgt_arg;
+    int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
+    float *z_tilde; float *policy; uint8_t *accept;
+};
+
+struct ArbFinishArgs {
+    int64_t n_sel, n_rows;
+    const int32_t *row_index;
+    const float *zpart; int32_t n_htiles; int64_t m_cap;
+    float b2, lambda;
+    float *out_z; uint8_t *out_accept;
+};
+
+hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
+hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);
+hipError_t launch_chain_scan(const ChainScanArgs &a, hipStream_t s);
+hipError_t launch_tree_scan(const TreeScanArgs &a, hipStream_t s);
+hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
+
+}  // namespace cospec

@@ -1,0 +1,168 @@
+// Accept/stop scans and emission.
+//
+// Chain (Section 3.3, Eq. cospec_length): one wave per sequence, lane i-1 owns
+// decision i.  A matched decision passes (z_tilde = +inf, Eq. policy-prob); a
+// mismatch passes when sigma(z) > lambda (Eq. infer_thre).  The first failing
+// decision is the lowest set bit of a wave ballot, s = its position (1-based)
+// or K+1; the round emits draft tokens 1..s-1 and the target token of row s-1.
+//
+// Tree (the chain rule along root paths): one workgroup per tree, thread n owns
+// node n.  Reachability (every decision on the root path passes) and depth are
+// found by pointer jumping in LDS (log2(depth) rounds), the accepted node is the
+// deepest reachable one with ties to the lowest id (one key max-reduction), and
+// the path is walked back through the parent array.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "launch.h"
+
+namespace cospec {
+namespace {
+
+struct Verdict {
+    bool pass;
+    float z_tilde, policy;
+};
+
+// Verdict of one decision slot from its decide state and the head's partial logits.
+__device__ inline Verdict verdict(uint8_t state, int pos, const float *zpart, int n_htiles,
+                                  int64_t m_cap, int head_ran, float b2, float lambda) {
+    Verdict v;
+    if (state == kStateMatch) {
+        v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f;
+    } else if (state != kStateMismatch) {          // invalid token or parent: always rejected
+        v.pass = false; v.z_tilde = NAN; v.policy = NAN;
+    } else if (!head_ran || pos < 0) {
+        // head skipped: lambda >= 1 or lambda < 0 decides every mismatch by itself
+        v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN;
+    } else {
+        float z = b2;
+        for (int t = 0; t < n_htiles; ++t) z += zpart[static_cast<int64_t>(t) * m_cap + pos];
+        const float pi = 1.0f / (1.0f + expf(-z));
+        v.pass = pi > lambda; v.z_tilde = z; v.policy = pi;
+    }
+    return v;
+}
+
+__global__ __launch_bounds__(256) void k_chain_scan(ChainScanArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (b >= a.B) return;                                  // whole wave leaves together
+    const int K = a.K;
+    bool fail = false;
+    if (lane < K) {
+        const int64_t di = static_cast<int64_t>(b) * K + lane;
+        const uint8_t st = a.ws_state[di];
+        const Verdict v = verdict(st, a.ws_listpos[di], a.zpart, a.n_htiles, a.m_cap, a.head_ran, a.b2, a.lambda);
+        fail = !v.pass;
+        if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
+        if (a.policy) a.policy[di] = v.policy;
+        if (a.accept) a.accept[di] = v.pass;
+    }
+    const uint64_t rej = __ballot(fail);
+    const int s = rej ? __builtin_ctzll(rej) + 1 : K + 1;
+    if (lane == 0) a.accept_len[b] = s;
+    for (int j = lane; j <= K; j += 64) {
+        int tok = -1;
+        if (j < s - 1) tok = a.tokens[static_cast<int64_t>(b) * K + j];
+        else if (j == s - 1) tok = a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + j];
+        a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = tok;
+    }
+}
+
+__global__ __launch_bounds__(kMaxSeqRows) void k_tree_scan(TreeScanArgs a) {
+    const int b = blockIdx.x;
+    const int n = threadIdx.x;
+    const int N = a.N;
+    const int64_t base = static_cast<int64_t>(b) * N;
+    __shared__ int s_anc[2][kMaxSeqRows];
+    __shared__ int s_dep[2][kMaxSeqRows];
+    __shared__ int s_ok[2][kMaxSeqRows];
+    __shared__ int s_par[kMaxSeqRows];
+    __shared__ int s_path[kMaxSeqRows];
+    __shared__ int s_key[kMaxSeqRows / 64];
+
+    int anc = -1, dep = 0, ok = 1, par = -1;
+    if (n < N) {
+        const Verdict v = verdict(a.ws_state[base + n], a.ws_listpos[base + n], a.zpart, a.n_htiles, a.m_cap,
+                                  a.head_ran, a.b2, a.lambda);
+        if (n > 0) {
+            par = a.parent[base + n];
+            const bool valid = par >= 0 && par < n;
+            if (!valid) par = -1;
+            anc = par;
+            dep = 1;
+            ok = valid && v.pass;
+        }
+        if (a.z_tilde) a.z_tilde[base + n] = v.z_tilde;
+        if (a.policy) a.policy[base + n] = v.policy;
+        if (a.accept) a.accept[base + n] = n == 0 ? 1 : v.pass;
+        s_par[n] = par;
+    }
+    // pointer jumping: anc = ancestor 2^k steps up (or -1), dep = distance to it,
+    // ok = every decision from this node up to (not including) anc passes
+    int cur = 0;
+    if (n < N) { s_anc[0][n] = anc; s_dep[0][n] = dep; s_ok[0][n] = ok; }
+    __syncthreads();
+    while (__syncthreads_or(n < N && s_anc[cur][n] >= 0)) {
+        if (n < N) {
+            const int x = s_anc[cur][n];
+            if (x >= 0) {
+                s_anc[cur ^ 1][n] = s_anc[cur][x];
+                s_dep[cur ^ 1][n] = s_dep[cur][n] + s_dep[cur][x];
+                s_ok[cur ^ 1][n] = s_ok[cur][n] & s_ok[cur][x];
+            } else {
+                s_anc[cur ^ 1][n] = -1;
+                s_dep[cur ^ 1][n] = s_dep[cur][n];
+                s_ok[cur ^ 1][n] = s_ok[cur][n];
+            }
+        }
+        cur ^= 1;
+        __syncthreads();
+    }
+    // a node with a broken parent link (anc -1 before the root) is never reachable:
+    // its ok is 0 and so is every descendant's
+    int key = -1;
+    if (n < N && s_ok[cur][n]) key = (s_dep[cur][n] << 9) | (511 - n);
+    for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off));
+    if ((n & 63) == 0) s_key[n >> 6] = key;
+    __syncthreads();
+    if (n == 0) {
+        int k = s_key[0];
+        for (int w = 1; w < kMaxSeqRows / 64; ++w) k = max(k, s_key[w]);
+        const int best = 511 - (k & 511);
+        const int depth = k >> 9;
+        int x = best;
+        for (int d = depth; d >= 0; --d) { s_path[d] = x; x = d > 0 ? s_par[x] : x; }
+        s_key[0] = best;
+        s_key[1] = depth;
+        a.accept_len[b] = depth + 1;
+    }
+    __syncthreads();
+    const int best = s_key[0], depth = s_key[1];
+    if (n < N) {
+        int tok = -1;
+        if (n < depth) tok = a.node_tokens[base + s_path[n + 1]];
+        else if (n == depth) tok = a.ws_tgt_arg[base + best];
+        a.out_tokens[base + n] = tok;
+        if (a.out_path) a.out_path[base + n] = n <= depth ? s_path[n] : -1;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_chain_scan(const ChainScanArgs &a, hipStream_t s) {
+    const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_chain_scan, dim3(blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_tree_scan(const TreeScanArgs &a, hipStream_t s) {
+    if (a.B == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_tree_scan, dim3(static_cast<unsigned>(a.B)), dim3(kMaxSeqRows), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace cospec

@@ -1,0 +1,142 @@
+"""The C ABI without a GPU: libcospec.so loads, exports every function that
+include/cospec.h declares, and rejects invalid host-side arguments before it
+enqueues anything (these calls never reach a kernel launch)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2605_24793_amd as cs
+from paper_2605_24793_amd import binding
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "cospec.h")
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, -1, -2, -3
+FAKE = 0x10000          # an aligned address; validation never dereferences device pointers
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cospec_\w+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = _declared()
+    assert {"cospec_verify_block", "cospec_verify_tree", "cospec_arbitrate"} <= set(names)
+    L = cs.lib()
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in cospec.h but not exported"
+
+
+def test_abi_version_and_status_strings():
+    L = cs.lib()
+    ver = int(re.search(r"#define COSPEC_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert L.cospec_abi_version() == ver
+    for code, word in ((OK, "ok"), (INVALID, "invalid"), (UNSUPPORTED, "unsupported"),
+                       (WORKSPACE, "workspace"), (-4, "HIP"), (7, "unknown")):
+        assert word in binding.status_string(code)
+
+
+def _head(d=512, h=128, dtype=1, w1=FAKE, w2=FAKE, b1=None):
+    return binding._Head(d, h, dtype, w1, b1, w2, 0.0)
+
+
+def test_workspace_sizes():
+    L = cs.lib()
+    hd = _head()
+    sz = L.cospec_verify_block_workspace_size(64, 7, 151936, ctypes.byref(hd))
+    assert sz > 0 and sz % 256 == 0
+    assert L.cospec_verify_block_workspace_size(256, 7, 151936, ctypes.byref(hd)) >= sz
+    assert L.cospec_verify_block_workspace_size(64, 65, 151936, ctypes.byref(hd)) == 0
+    assert L.cospec_verify_block_workspace_size(-1, 7, 100, ctypes.byref(hd)) == 0
+    assert L.cospec_verify_block_workspace_size(1, 7, 0, ctypes.byref(hd)) == 0
+    assert L.cospec_verify_tree_workspace_size(64, 60, 151936, ctypes.byref(hd)) > 0
+    assert L.cospec_verify_tree_workspace_size(64, 257, 151936, ctypes.byref(hd)) == 0
+    assert L.cospec_verify_tree_workspace_size(64, 0, 151936, ctypes.byref(hd)) == 0
+    assert L.cospec_arbitrate_workspace_size(1000, ctypes.byref(hd)) > 0
+    bad = _head(d=12)                                      # 24 bytes: not a 16-byte multiple
+    assert L.cospec_verify_block_workspace_size(1, 4, 100, ctypes.byref(bad)) == 0
+
+
+def _block(L, **kw):
+    a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, toks=FAKE, hid=FAKE, head=_head(), lam=0.5,
+             B=4, K=7, V=151936, alen=FAKE, otok=FAKE, feats=None, opts=None, ws=FAKE, wsb=1 << 30)
+    a.update(kw)
+    return L.cospec_verify_block(a["tgt"], a["drf"], a["dt"], a["ld"], a["toks"], a["hid"],
+                                 ctypes.byref(a["head"]), a["lam"], a["B"], a["K"], a["V"],
+                                 a["alen"], a["otok"], a["feats"], a["opts"], a["ws"], a["wsb"],
+                                 None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(tgt=None), INVALID),
+    (dict(tgt=FAKE + 8), INVALID),                 # logits not 16-byte aligned
+    (dict(drf=None), INVALID),
+    (dict(toks=None), INVALID),
+    (dict(hid=None), INVALID),
+    (dict(alen=None), INVALID),
+    (dict(otok=None), INVALID),
+    (dict(ld=151935), INVALID),                    # ld < V
+    (dict(ld=151940, V=151937), INVALID),          # ld * 2 bytes not a 16-byte multiple
+    (dict(dt=5), INVALID),
+    (dict(B=-1), INVALID),
+    (dict(K=-1), INVALID),
+    (dict(K=65), UNSUPPORTED),
+    (dict(V=0), INVALID),
+    (dict(lam=math.nan), INVALID),
+    (dict(head=_head(d=0)), INVALID),
+    (dict(head=_head(h=0)), INVALID),
+    (dict(head=_head(w1=None)), INVALID),
+    (dict(head=_head(w1=FAKE + 4)), INVALID),
+    (dict(head=_head(dtype=3)), INVALID),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws=FAKE + 64), WORKSPACE),               # not 256-byte aligned
+    (dict(wsb=1024), WORKSPACE),
+    (dict(B=0), OK),                               # empty batch: nothing to enqueue
+])
+def test_verify_block_rejects_before_launch(kw, code):
+    assert _block(cs.lib(), **kw) == code
+
+
+def test_verify_block_split_override_limits():
+    L = cs.lib()
+    assert _block(L, opts=ctypes.byref(binding._Options(None, None, 65))) == UNSUPPORTED
+    assert _block(L, opts=ctypes.byref(binding._Options(None, None, -2))) == UNSUPPORTED
+    # 4 x 15 rows x 64 splits fits the partial buffer; the workspace is checked after
+    assert _block(L, wsb=16, opts=ctypes.byref(binding._Options(None, None, 64))) == WORKSPACE
+
+
+def _tree(L, **kw):
+    a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
+             lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30)
+    a.update(kw)
+    return L.cospec_verify_tree(a["tgt"], a["drf"], a["dt"], a["ld"], a["par"], a["toks"], a["hid"],
+                                ctypes.byref(a["head"]), a["lam"], a["B"], a["N"], a["V"],
+                                a["alen"], a["otok"], a["path"], None, None, a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(par=None), INVALID), (dict(toks=None), INVALID), (dict(drf=None), INVALID),
+    (dict(N=0), INVALID), (dict(N=257), UNSUPPORTED), (dict(path=FAKE + 2), INVALID),
+    (dict(wsb=100), WORKSPACE), (dict(B=0), OK),
+])
+def test_verify_tree_rejects_before_launch(kw, code):
+    assert _tree(cs.lib(), **kw) == code
+
+
+def test_arbitrate_rejects_before_launch():
+    L = cs.lib()
+    hd = _head()
+
+    def call(hid=FAKE, n_rows=10, idx=None, n_sel=10, lam=0.5, ws=FAKE, wsb=1 << 20):
+        return L.cospec_arbitrate(hid, n_rows, idx, n_sel, ctypes.byref(hd), lam, FAKE, FAKE, ws,
+                                  wsb, None)
+    assert call(n_sel=11) == INVALID                       # more rows than exist, no index
+    assert call(hid=None) == INVALID
+    assert call(lam=math.nan) == INVALID
+    assert call(ws=None) == WORKSPACE
+    assert call(wsb=8) == WORKSPACE
+    assert call(n_sel=0) == OK
