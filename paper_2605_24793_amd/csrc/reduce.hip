@@ -81,7 +81,7 @@ __device__ inline void consume(const float *x, int chunk, Lane &st) {
 #pragma unroll
     for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
     if (cm > st.best) { st.best = cm; st.chunk = chunk; }
-    const float cms = cm * kLog2e;
+    const float cms = __fmul_rn(cm, kLog2e);
     const bool up = cms > st.ref + kRescaleMargin;
     // wave-uniform branch: after the first chunk almost no lane ever takes it
     if (__builtin_expect(__ballot(up) != 0, 0)) {
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         float cm = -INFINITY;
         for (int k = 0; k < tail; ++k) cm = fmaxf(cm, E::at(rp, e0 + k));
         if (cm > st.best) { st.best = cm; st.chunk = nvec; }
-        const float cms = cm * kLog2e;
+        const float cms = __fmul_rn(cm, kLog2e);
         if (cms > st.ref + kRescaleMargin) rescale(st, cms);
         for (int k = 0; k < tail; ++k) {
             const float t = fmaf(E::at(rp, e0 + k), kLog2e, -st.ref);
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     }
     __syncthreads();
     const float M = s_M;
-    const float R = M * kLog2e;
+    const float R = __fmul_rn(M, kLog2e);   // the partial's reference: rounded, never contracted
     float S = 0.f, T = 0.f;
     if (st.S > 0.f) {
         const float dr = st.ref - R;
@@ -225,6 +225,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
 
 struct RowStat {
     float max, lse, ent;
+    float log_s;     // ln sum exp(x - max): lse - max without the cancellation
     int arg;
 };
 
@@ -236,22 +237,26 @@ __device__ inline RowStat merge_row(const float4 *p, int splits) {
         const float4 q = p[s];
         if (q.z > 0.f && q.x > M) { M = q.x; arg = __float_as_int(q.y); }   // earlier split wins ties
     }
-    const float R = M * kLog2e;
+    const float R = __fmul_rn(M, kLog2e);
     float S = 0.f, T = 0.f;
     for (int s = 0; s < splits; ++s) {
         const float4 q = p[s];
         if (q.z > 0.f) {
-            const float dr = q.x * kLog2e - R;
+            const float dr = __fmul_rn(q.x, kLog2e) - R;     // the split's reference, as k_vocab_reduce rounded it
             const float f = __builtin_amdgcn_exp2f(dr);
             S += f * q.z;
             T += f * fmaf(dr, q.z, q.w);
         }
     }
+    // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
+    // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
+    const float delta = fmaf(M, kLog2e, -R);
     const float l2s = __log2f(S);
     RowStat r;
     r.max = M;
     r.arg = arg;
-    r.lse = fmaf(l2s, kLn2, M);
+    r.log_s = (l2s - delta) * kLn2;
+    r.lse = M + r.log_s;
     r.ent = (l2s - T / S) * kLn2;
     return r;
 }
@@ -261,9 +266,11 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     using E = Elt<DT>;
     const int b = blockIdx.x;
     const int t = threadIdx.x;
-    __shared__ float s_tlse[kMaxSeqRows];
+    // per row: max and ln S, so that log p(token) = (x - max) - ln S keeps full
+    // precision even when |lse| is large
+    __shared__ float s_tmax[kMaxSeqRows], s_tlogs[kMaxSeqRows];
     __shared__ int s_targ[kMaxSeqRows];
-    __shared__ float s_dlse[kMaxSeqRows];
+    __shared__ float s_dmax[kMaxSeqRows], s_dlogs[kMaxSeqRows];
     __shared__ int s_child[kMaxSeqRows];
     __shared__ int s_wave_cnt[kDecideThreads / 64];
     __shared__ int s_base;
@@ -272,7 +279,8 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     for (int j = t; j < a.RT; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RT + j;
         const RowStat rs = merge_row(a.partials + r * a.splits, a.splits);
-        s_tlse[j] = rs.lse;
+        s_tmax[j] = rs.max;
+        s_tlogs[j] = rs.log_s;
         s_targ[j] = rs.arg;
         a.ws_tgt_arg[r] = rs.arg;
         if (a.tgt_argmax) a.tgt_argmax[r] = rs.arg;
@@ -292,9 +300,10 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     }
     for (int j = t; j < a.RD; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RD + j;
-        RowStat rs{NAN, NAN, NAN, -1};
+        RowStat rs{NAN, NAN, NAN, NAN, -1};
         if (s_child[j]) rs = merge_row(a.partials + (static_cast<int64_t>(a.B) * a.RT + r) * a.splits, a.splits);
-        s_dlse[j] = rs.lse;
+        s_dmax[j] = rs.max;
+        s_dlogs[j] = rs.log_s;
         if (a.drf_argmax) a.drf_argmax[r] = rs.arg;
         if (a.drf_max) a.drf_max[r] = rs.max;
         if (a.drf_lse) a.drf_lse[r] = rs.lse;
@@ -328,8 +337,8 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
                 const bool match = tok == s_targ[p];
                 const char *trow = a.tgt + (static_cast<int64_t>(b) * a.RT + p) * a.ld_bytes;
                 const char *drow = a.drf + (static_cast<int64_t>(b) * a.RD + p) * a.ld_bytes;
-                lpt = E::at(trow, tok) - s_tlse[p];
-                lpd = E::at(drow, tok) - s_dlse[p];
+                lpt = (E::at(trow, tok) - s_tmax[p]) - s_tlogs[p];
+                lpd = (E::at(drow, tok) - s_dmax[p]) - s_dlogs[p];
                 state = match ? kStateMatch : kStateMismatch;
             } else {
                 state = kStateReject;

@@ -296,7 +296,7 @@ def test_empty_and_degenerate_sizes():
                           torch.empty(0, 3, 32, dtype=torch.bfloat16, device=DEV), hd, 0.5)
     assert out["accept_len"].numel() == 0
     # K = 0: the round emits the target's token from row 0
-    t = wl.target[:, :1].to(DEV)
+    t = _padded(wl.target[:, :1].contiguous(), 0)         # rows padded to 16-byte multiples
     out = cs.verify_block(t, t[:, :0], torch.empty(2, 0, dtype=torch.int32, device=DEV),
                           torch.empty(2, 0, 32, dtype=torch.bfloat16, device=DEV), hd, 0.5)
     torch.cuda.synchronize()
