@@ -43,11 +43,20 @@ cospec_status check_head(const cospec_head *hd) {
     return COSPEC_OK;
 }
 
-inline int n_htiles(const cospec_head *hd) { return (hd->h + kHeadTileN - 1) / kHeadTileN; }
+inline int32_t ksplit_for(int64_t m_cap, const cospec_head *hd) {
+    return head_ksplit(m_cap, hd->d, hd->h, elem_bytes(hd->dtype));
+}
+
+// Head scratch: k-slice partial pre-activations and the logits.
+inline size_t head_bytes(int64_t m_cap, const cospec_head *hd) {
+    return round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
+                    static_cast<size_t>(hd->h) * 4) +
+           round_up(static_cast<size_t>(m_cap) * 4);
+}
 
 // Workspace carving shared by the size query and the call.
 struct Layout {
-    size_t partials, tgt_arg, state, listpos, list, count, zpart, total;
+    size_t partials, tgt_arg, state, listpos, list, count, upart, z, total;
     int64_t partial_slots;
 };
 
@@ -61,7 +70,10 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     L.listpos = off;  off += round_up(static_cast<size_t>(B * D) * 4);
     L.list = off;     off += round_up(static_cast<size_t>(B * D) * 4);
     L.count = off;    off += kAlign;
-    L.zpart = off;    off += round_up(static_cast<size_t>(n_htiles(hd)) * static_cast<size_t>(B * D) * 4);
+    const int64_t m_cap = B * D;
+    L.upart = off;    off += round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
+                                      static_cast<size_t>(hd->h) * 4);
+    L.z = off;        off += round_up(static_cast<size_t>(m_cap) * 4);
     L.total = off;
     return L;
 }
@@ -122,7 +134,8 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     int32_t *listpos = reinterpret_cast<int32_t *>(ws + L.listpos);
     int32_t *list = reinterpret_cast<int32_t *>(ws + L.list);
     int32_t *count = reinterpret_cast<int32_t *>(ws + L.count);
-    float *zpart = reinterpret_cast<float *>(ws + L.zpart);
+    float *upart = reinterpret_cast<float *>(ws + L.upart);
+    float *zlog = reinterpret_cast<float *>(ws + L.z);
 
     const cospec_features F = c.feats ? *c.feats : cospec_features{};
     const bool decisions = c.B > 0 && (c.is_tree ? c.D > 1 : c.D > 0);
@@ -185,9 +198,11 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         ha.count_dev = count;
         ha.count_host = 0;
         ha.m_cap = m_cap;
-        ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2;
+        ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2; ha.b2 = c.head->b2;
         ha.d = c.head->d; ha.h = c.head->h;
-        ha.zpart = zpart;
+        ha.ksplit = ksplit_for(m_cap, c.head);
+        ha.upart = upart;
+        ha.z = zlog;
         if ((e = launch_head(static_cast<Dtype>(c.head->dtype), ha, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
     }
 
@@ -196,8 +211,8 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         ta.B = c.B; ta.N = static_cast<int32_t>(c.RT);
         ta.parent = c.parent; ta.node_tokens = c.tokens;
         ta.ws_state = state; ta.ws_listpos = listpos;
-        ta.zpart = zpart; ta.n_htiles = n_htiles(c.head); ta.m_cap = m_cap;
-        ta.head_ran = head; ta.b2 = c.head->b2; ta.lambda = c.lambda;
+        ta.z = zlog;
+        ta.head_ran = head; ta.lambda = c.lambda;
         ta.ws_tgt_arg = tgt_arg;
         ta.accept_len = accept_len; ta.out_tokens = out_tokens; ta.out_path = out_path;
         ta.z_tilde = F.z_tilde; ta.policy = F.policy; ta.accept = F.accept;
@@ -206,8 +221,8 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         ChainScanArgs sa{};
         sa.B = c.B; sa.K = static_cast<int32_t>(c.D);
         sa.ws_state = state; sa.ws_listpos = listpos;
-        sa.zpart = zpart; sa.n_htiles = n_htiles(c.head); sa.m_cap = m_cap;
-        sa.head_ran = head; sa.b2 = c.head->b2; sa.lambda = c.lambda;
+        sa.z = zlog;
+        sa.head_ran = head; sa.lambda = c.lambda;
         sa.tokens = c.tokens; sa.ws_tgt_arg = tgt_arg;
         sa.accept_len = accept_len; sa.out_tokens = out_tokens;
         sa.z_tilde = F.z_tilde; sa.policy = F.policy; sa.accept = F.accept;
@@ -309,7 +324,7 @@ cospec_status cospec_verify_tree(const void *target_logits, const void *draft_lo
 
 size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head) {
     if (n_sel < 0 || check_head(head) != COSPEC_OK) return 0;
-    return round_up(static_cast<size_t>(n_htiles(head)) * static_cast<size_t>(n_sel) * 4) + kAlign;
+    return head_bytes(n_sel, head);
 }
 
 cospec_status cospec_arbitrate(const void *hidden, int64_t n_rows, const int32_t *row_index, int64_t n_sel,
@@ -326,17 +341,21 @@ cospec_status cospec_arbitrate(const void *hidden, int64_t n_rows, const int32_t
     const size_t need = cospec_arbitrate_workspace_size(n_sel, head);
     if (!workspace || !aligned(workspace, kAlign) || workspace_bytes < need) return COSPEC_ERR_WORKSPACE;
 
-    float *zpart = static_cast<float *>(workspace);
+    const int32_t ks = ksplit_for(n_sel, head);
+    float *upart = static_cast<float *>(workspace);
+    float *zlog = reinterpret_cast<float *>(static_cast<char *>(workspace) +
+                                            round_up(static_cast<size_t>(ks) * n_sel * head->h * 4));
     HeadArgs ha{};
     ha.hidden = hidden; ha.n_rows = n_rows; ha.list = row_index;
     ha.count_dev = nullptr; ha.count_host = n_sel; ha.m_cap = n_sel;
-    ha.w1 = head->w1; ha.b1 = head->b1; ha.w2 = head->w2; ha.d = head->d; ha.h = head->h;
-    ha.zpart = zpart;
+    ha.w1 = head->w1; ha.b1 = head->b1; ha.w2 = head->w2; ha.b2 = head->b2; ha.d = head->d; ha.h = head->h;
+    ha.ksplit = ks;
+    ha.upart = upart;
+    ha.z = zlog;
     if (launch_head(static_cast<Dtype>(head->dtype), ha, stream) != hipSuccess) return COSPEC_ERR_HIP;
     ArbFinishArgs fa{};
     fa.n_sel = n_sel; fa.n_rows = n_rows; fa.row_index = row_index;
-    fa.zpart = zpart; fa.n_htiles = n_htiles(head); fa.m_cap = n_sel;
-    fa.b2 = head->b2; fa.lambda = lambda; fa.out_z = out_z; fa.out_accept = out_accept;
+    fa.z = zlog; fa.lambda = lambda; fa.out_z = out_z; fa.out_accept = out_accept;
     if (launch_arb_finish(fa, stream) != hipSuccess) return COSPEC_ERR_HIP;
     return COSPEC_OK;
 }

@@ -9,8 +9,10 @@ namespace cospec {
 
 constexpr int kReduceThreads = 256;   // vocabulary-reduction workgroup
 constexpr int kDecideThreads = 256;   // one workgroup per sequence / tree
-constexpr int kHeadTileM = 64;        // head GEMM workgroup tile: rows
-constexpr int kHeadTileN = 64;        //                            columns of W1
+constexpr int kHeadTileM = 128;       // head GEMM workgroup tile: rows
+constexpr int kHeadTileN = 128;       //                            columns of W1
+constexpr int kHeadTargetBlocks = 256; // k-splits are added until the grid reaches this
+constexpr int kHeadMaxSplit = 8;
 constexpr int kMaxSeqRows = 256;      // rows per sequence / nodes per tree held in LDS
 
 enum Dtype : int32_t { kF32 = 0, kBF16 = 1 };
@@ -64,19 +66,22 @@ struct HeadArgs {
     const int32_t *list;       // selected rows, or null = identity
     const int32_t *count_dev;  // M on the device, or null
     int64_t count_host;        // M when count_dev is null
-    int64_t m_cap;             // capacity of the list / zpart row dimension
+    int64_t m_cap;             // capacity of the list (rows of upart and z)
     const void *w1; const void *b1; const void *w2;
+    float b2;
     int32_t d, h;
-    float *zpart;              // [ceil(h/64)][m_cap]
+    int32_t ksplit;            // slices of d, one workgroup each (head_ksplit)
+    float *upart;              // [ksplit][m_cap][h] partial pre-activations
+    float *z;                  // [m_cap] head logits of the selected rows
 };
 
 struct ChainScanArgs {
     int32_t B, K;
     const uint8_t *ws_state;
     const int32_t *ws_listpos;
-    const float *zpart; int32_t n_htiles; int64_t m_cap;
+    const float *z;            // head logits by compacted position
     int32_t head_ran;
-    float b2, lambda;
+    float lambda;
     const int32_t *tokens;
     const int32_t *ws_tgt_arg;
     int32_t *accept_len; int32_t *out_tokens;
@@ -89,9 +94,9 @@ struct TreeScanArgs {
     const int32_t *node_tokens;
     const uint8_t *ws_state;
     const int32_t *ws_listpos;
-    const float *zpart; int32_t n_htiles; int64_t m_cap;
+    const float *z;
     int32_t head_ran;
-    float b2, lambda;
+    float lambda;
     const int32_t *ws_tgt_arg;
     int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
     float *z_tilde; float *policy; uint8_t *accept;
@@ -100,14 +105,15 @@ struct TreeScanArgs {
 struct ArbFinishArgs {
     int64_t n_sel, n_rows;
     const int32_t *row_index;
-    const float *zpart; int32_t n_htiles; int64_t m_cap;
-    float b2, lambda;
+    const float *z;
+    float lambda;
     float *out_z; uint8_t *out_accept;
 };
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
-hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);
+int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
+hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
 hipError_t launch_chain_scan(const ChainScanArgs &a, hipStream_t s);
 hipError_t launch_tree_scan(const TreeScanArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);

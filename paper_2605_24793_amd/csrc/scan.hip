@@ -25,9 +25,8 @@ struct Verdict {
     float z_tilde, policy;
 };
 
-// Verdict of one decision slot from its decide state and the head's partial logits.
-__device__ inline Verdict verdict(uint8_t state, int pos, const float *zpart, int n_htiles,
-                                  int64_t m_cap, int head_ran, float b2, float lambda) {
+// Verdict of one decision slot from its decide state and the head's logits.
+__device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int head_ran, float lambda) {
     Verdict v;
     if (state == kStateMatch) {
         v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f;
@@ -37,8 +36,7 @@ __device__ inline Verdict verdict(uint8_t state, int pos, const float *zpart, in
         // head skipped: lambda >= 1 or lambda < 0 decides every mismatch by itself
         v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN;
     } else {
-        float z = b2;
-        for (int t = 0; t < n_htiles; ++t) z += zpart[static_cast<int64_t>(t) * m_cap + pos];
+        const float z = zs[pos];
         const float pi = 1.0f / (1.0f + expf(-z));
         v.pass = pi > lambda; v.z_tilde = z; v.policy = pi;
     }
@@ -54,7 +52,7 @@ __global__ __launch_bounds__(256) void k_chain_scan(ChainScanArgs a) {
     if (lane < K) {
         const int64_t di = static_cast<int64_t>(b) * K + lane;
         const uint8_t st = a.ws_state[di];
-        const Verdict v = verdict(st, a.ws_listpos[di], a.zpart, a.n_htiles, a.m_cap, a.head_ran, a.b2, a.lambda);
+        const Verdict v = verdict(st, a.ws_listpos[di], a.z, a.head_ran, a.lambda);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
         if (a.policy) a.policy[di] = v.policy;
@@ -85,8 +83,7 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_scan(TreeScanArgs a) {
 
     int anc = -1, dep = 0, ok = 1, par = -1;
     if (n < N) {
-        const Verdict v = verdict(a.ws_state[base + n], a.ws_listpos[base + n], a.zpart, a.n_htiles, a.m_cap,
-                                  a.head_ran, a.b2, a.lambda);
+        const Verdict v = verdict(a.ws_state[base + n], a.ws_listpos[base + n], a.z, a.head_ran, a.lambda);
         if (n > 0) {
             par = a.parent[base + n];
             const bool valid = par >= 0 && par < n;

@@ -57,6 +57,12 @@ def test_workspace_sizes():
     assert L.cospec_verify_tree_workspace_size(64, 257, 151936, ctypes.byref(hd)) == 0
     assert L.cospec_verify_tree_workspace_size(64, 0, 151936, ctypes.byref(hd)) == 0
     assert L.cospec_arbitrate_workspace_size(1000, ctypes.byref(hd)) > 0
+    # no decision rows at all (empty batch, K = 0, a lone root, no selection)
+    assert L.cospec_verify_block_workspace_size(0, 7, 151936, ctypes.byref(hd)) > 0
+    assert L.cospec_verify_block_workspace_size(5, 0, 151936, ctypes.byref(hd)) > 0
+    assert L.cospec_verify_tree_workspace_size(0, 60, 151936, ctypes.byref(hd)) > 0
+    assert L.cospec_verify_tree_workspace_size(3, 1, 151936, ctypes.byref(hd)) > 0
+    assert L.cospec_arbitrate_workspace_size(0, ctypes.byref(hd)) >= 0
     bad = _head(d=12)                                      # 24 bytes: not a 16-byte multiple
     assert L.cospec_verify_block_workspace_size(1, 4, 100, ctypes.byref(bad)) == 0
 
