@@ -33,7 +33,7 @@ typedef __attribute__((ext_vector_type(4))) float floatx4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStageBytes = 128;                  // bytes of k per row per stage
-constexpr int kLdsRow = kStageBytes + 16;         // padded LDS row
+constexpr int kRing = 4;                          // LDS stages: three in flight while one is used
 constexpr int kWaveTile = 64;
 
 template <int DT> __device__ inline float scalar_at(const void *p, int64_t i);
@@ -57,16 +57,34 @@ template <> __device__ inline floatx4 mma<kF32>(u32x4 a, u32x4 b, floatx4 c) {
     return c;
 }
 
+typedef __attribute__((address_space(3))) char lds_char;
+
+// Waits until at most N vector-memory operations of this wave are outstanding.
+template <int N> __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Workgroup barrier without the memory fence of __syncthreads (which would also wait
+// for the stages still in flight); LDS writes of this wave are drained first and the
+// compiler may not move memory accesses across it.
+__device__ inline void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
     constexpr int BK = kStageBytes / EB;          // elements of k per stage
     constexpr int VE = 16 / EB;                   // elements per 16-byte vector
+    // 1-D grid, k-slice fastest: workgroups are dealt to the 8 XCDs round-robin, so with
+    // 8 slices each XCD owns one slice of the hidden rows and of W1, which fits its L2
+    const int ks = blockIdx.x % a.ksplit;
+    const int tile = blockIdx.x / a.ksplit;
+    const int mtiles = static_cast<int>((a.m_cap + kHeadTileM - 1) / kHeadTileM);
     const int64_t M = a.count_dev ? static_cast<int64_t>(*a.count_dev) : a.count_host;
-    const int64_t m_base = static_cast<int64_t>(blockIdx.x) * kHeadTileM;
+    const int64_t m_base = static_cast<int64_t>(tile % mtiles) * kHeadTileM;
     if (m_base >= M) return;
-    const int n_base = blockIdx.y * kHeadTileN;
-    const int ks = blockIdx.z;
+    const int n_base = (tile / mtiles) * kHeadTileN;
     const int kchunk = ((a.d + a.ksplit - 1) / a.ksplit + BK - 1) / BK * BK;
     const int k0 = ks * kchunk;
     const int k1 = min(a.d, k0 + kchunk);
@@ -76,39 +94,43 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     const int wr = wave >> 1, wc = wave & 1;
     const int g = lane >> 4, l16 = lane & 15;
 
-    __shared__ __attribute__((aligned(16))) char sA[2][kHeadTileM * kLdsRow];
-    __shared__ __attribute__((aligned(16))) char sB[2][kHeadTileN * kLdsRow];
+    // LDS ring of kRing stages; a stage holds 128 rows of A then 128 rows of B, 128 bytes
+    // each, the 16-byte slot s of row r holding k-vector (s ^ (r & 7)) of the stage
+    __shared__ __attribute__((aligned(16))) char ring[kRing][2 * kHeadTileM * kStageBytes];
 
-    // loader: thread t moves 16 bytes of rows (t >> 3) + 32 j, j = 0..3
-    const int lrow = tid >> 3, lcol = (tid & 7) * 16;
+    // async loader: per stage, wave w fills 1 KB blocks w*4+i of A and of B (8 rows each);
+    // lane l brings row 8*(w*4+i) + l/8, k-vector (l%8) ^ (row%8)
+    const int lrow = lane >> 3, lslot = lane & 7;
     const char *ga[4];
     const char *gb[4];
+    int lvec[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        int64_t m = m_base + lrow + 32 * j;
+    for (int i = 0; i < 4; ++i) {
+        const int row = 8 * (wave * 4 + i) + lrow;
+        lvec[i] = lslot ^ (row & 7);
+        int64_t m = m_base + row;
         if (m >= M) m = M - 1;                     // garbage rows are computed, never stored
         int64_t id = a.list ? static_cast<int64_t>(a.list[m]) : m;
         if (id < 0 || id >= a.n_rows) id = 0;
-        ga[j] = static_cast<const char *>(a.hidden) + id * static_cast<int64_t>(a.d) * EB;
-        int n = n_base + lrow + 32 * j;
+        ga[i] = static_cast<const char *>(a.hidden) + id * static_cast<int64_t>(a.d) * EB;
+        int n = n_base + row;
         if (n >= a.h) n = a.h - 1;
-        gb[j] = static_cast<const char *>(a.w1) + static_cast<int64_t>(n) * a.d * EB;
+        gb[i] = static_cast<const char *>(a.w1) + static_cast<int64_t>(n) * a.d * EB;
     }
-    u32x4 ra[4], rb[4];
-    auto fetch = [&](int st) {
-        const int e = k0 + st * BK + (tid & 7) * VE;     // first element of this thread's vector
-        const bool in = e < k1;                          // d is a multiple of VE
+    auto issue = [&](int st) {
+        char *slot = ring[st % kRing];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            ra[j] = in ? *reinterpret_cast<const u32x4 *>(ga[j] + static_cast<int64_t>(e) * EB) : u32x4{0, 0, 0, 0};
-            rb[j] = in ? *reinterpret_cast<const u32x4 *>(gb[j] + static_cast<int64_t>(e) * EB) : u32x4{0, 0, 0, 0};
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            *reinterpret_cast<u32x4 *>(&sA[buf][(lrow + 32 * j) * kLdsRow + lcol]) = ra[j];
-            *reinterpret_cast<u32x4 *>(&sB[buf][(lrow + 32 * j) * kLdsRow + lcol]) = rb[j];
+        for (int i = 0; i < 4; ++i) {
+            const int e = k0 + st * BK + lvec[i] * VE;          // first element of the vector
+            char *la = slot + (wave * 4 + i) * 1024;
+            char *lb = slot + kHeadTileM * kStageBytes + (wave * 4 + i) * 1024;
+            if (e < k1) {                                       // d is a multiple of VE
+                __builtin_amdgcn_global_load_lds(ga[i] + static_cast<int64_t>(e) * EB, (lds_char *)la, 16, 0, 0);
+                __builtin_amdgcn_global_load_lds(gb[i] + static_cast<int64_t>(e) * EB, (lds_char *)lb, 16, 0, 0);
+            } else {                                            // ragged end of d: zeros
+                *reinterpret_cast<u32x4 *>(la + lane * 16) = u32x4{0, 0, 0, 0};
+                *reinterpret_cast<u32x4 *>(lb + lane * 16) = u32x4{0, 0, 0, 0};
+            }
         }
     };
 
@@ -118,30 +140,37 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    if (nst > 0) {
-        fetch(0);
-        stash(0);
-    }
-    __syncthreads();
-    for (int st = 0; st < nst; ++st) {
-        const int buf = st & 1;
-        if (st + 1 < nst) fetch(st + 1);               // next slice in flight during the MFMAs
 #pragma unroll
-        for (int kk = 0; kk < kStageBytes; kk += 64) {
+    for (int st = 0; st < kRing - 1; ++st)
+        if (st < nst) issue(st);
+    for (int st = 0; st < nst; ++st) {
+        // this wave's loads of stage st are done once at most the later stages' remain
+        const int later = min(kRing - 2, nst - 1 - st);
+        if (later >= 2) wait_vm<16>();
+        else if (later == 1) wait_vm<8>();
+        else wait_vm<0>();
+        lds_barrier();                            // every wave's part of stage st has landed
+        if (st + kRing - 1 < nst) issue(st + kRing - 1);   // refills the slot of stage st-1
+        const char *sa = ring[st % kRing];
+        const char *sb = sa + kHeadTileM * kStageBytes;
+#pragma unroll
+        for (int kk = 0; kk < kStageBytes / 16; kk += 4) {
             u32x4 av[4], bv[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                av[r] = *reinterpret_cast<const u32x4 *>(&sA[buf][(wr * kWaveTile + r * 16 + l16) * kLdsRow + kk + g * 16]);
+            for (int r = 0; r < 4; ++r) {
+                const int row = wr * kWaveTile + r * 16 + l16;
+                av[r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+            }
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-                bv[c] = *reinterpret_cast<const u32x4 *>(&sB[buf][(wc * kWaveTile + c * 16 + l16) * kLdsRow + kk + g * 16]);
+            for (int c = 0; c < 4; ++c) {
+                const int row = wc * kWaveTile + c * 16 + l16;
+                bv[c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+            }
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < 4; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
         }
-        if (st + 1 < nst) stash(buf ^ 1);
-        __syncthreads();
     }
 
     // partial U of this k-slice: upart[ks][m][n]
@@ -162,6 +191,8 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
 }
 
 // z[m] = w2 . relu(sum_ks upart[ks][m] + b1) + b2, one wave per row, fixed order.
+// Every partial the lane needs is loaded before any is summed (h <= 64 * kEpiCols).
+constexpr int kEpiCols = 8;
 template <int DT>
 __global__ __launch_bounds__(256) void k_head_epilogue(HeadArgs a) {
     const int64_t M = a.count_dev ? static_cast<int64_t>(*a.count_dev) : a.count_host;
@@ -169,11 +200,27 @@ __global__ __launch_bounds__(256) void k_head_epilogue(HeadArgs a) {
     if (m >= M) return;
     const int lane = threadIdx.x & 63;
     float acc = 0.f;
-    for (int n = lane; n < a.h; n += 64) {
-        float u = 0.f;
-        for (int ks = 0; ks < a.ksplit; ++ks) u += a.upart[(static_cast<int64_t>(ks) * a.m_cap + m) * a.h + n];
-        const float bias = a.b1 ? scalar_at<DT>(a.b1, n) : 0.f;
-        acc += fmaxf(u + bias, 0.f) * scalar_at<DT>(a.w2, n);
+    for (int n0 = 0; n0 < a.h; n0 += 64 * kEpiCols) {
+        float u[kEpiCols][kHeadMaxSplit];
+#pragma unroll
+        for (int i = 0; i < kEpiCols; ++i)
+#pragma unroll
+            for (int ks = 0; ks < kHeadMaxSplit; ++ks) {
+                const int n = n0 + i * 64 + lane;
+                u[i][ks] = (ks < a.ksplit && n < a.h)
+                               ? a.upart[(static_cast<int64_t>(ks) * a.m_cap + m) * a.h + n] : 0.f;
+            }
+#pragma unroll
+        for (int i = 0; i < kEpiCols; ++i) {
+            const int n = n0 + i * 64 + lane;
+            if (n < a.h) {
+                float v = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < kHeadMaxSplit; ++ks) v += u[i][ks];
+                const float bias = a.b1 ? scalar_at<DT>(a.b1, n) : 0.f;
+                acc += fmaxf(v + bias, 0.f) * scalar_at<DT>(a.w2, n);
+            }
+        }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
@@ -203,6 +250,7 @@ int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes) {
     if (mt * nt <= 0) return 1;                        // no rows: nothing to split
     const int64_t stages = (static_cast<int64_t>(d) * elem_bytes + kStageBytes - 1) / kStageBytes;
     int64_t ks = (kHeadTargetBlocks + mt * nt - 1) / (mt * nt);
+    if (ks < kXcds) ks = kXcds;                         // one k-slice per XCD (L2 locality)
     if (ks > kHeadMaxSplit) ks = kHeadMaxSplit;
     if (ks > stages) ks = stages;
     if (ks < 1) ks = 1;
@@ -210,9 +258,8 @@ int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes) {
 }
 
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>((a.m_cap + kHeadTileM - 1) / kHeadTileM),
-                    static_cast<unsigned>((a.h + kHeadTileN - 1) / kHeadTileN),
-                    static_cast<unsigned>(a.ksplit));
+    const int64_t tiles = ((a.m_cap + kHeadTileM - 1) / kHeadTileM) * ((a.h + kHeadTileN - 1) / kHeadTileN);
+    const dim3 grid(static_cast<unsigned>(tiles * a.ksplit));
     if (grid.x == 0) return hipSuccess;
     const dim3 egrid(static_cast<unsigned>((a.m_cap + 3) / 4));
     if (dt == kBF16) {

@@ -63,6 +63,7 @@ template <> struct Elt<kF32> {
 struct Lane {
     float best;      // largest logit seen
     int chunk;       // first chunk (16-byte vector index) holding `best`, -1 if none
+    u32x4 raw;       // that chunk's bits: the exact index is found without a re-read
     float ref;       // reference of S and T, in log2 units
     float S, T;
 };
@@ -76,11 +77,11 @@ __device__ inline void rescale(Lane &st, float new_ref) {
 }
 
 template <int NV>
-__device__ inline void consume(const float *x, int chunk, Lane &st) {
+__device__ inline void consume(const float *x, u32x4 q, int chunk, Lane &st) {
     float cm = -INFINITY;
 #pragma unroll
     for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
-    if (cm > st.best) { st.best = cm; st.chunk = chunk; }
+    if (cm > st.best) { st.best = cm; st.chunk = chunk; st.raw = q; }
     const float cms = __fmul_rn(cm, kLog2e);
     const bool up = cms > st.ref + kRescaleMargin;
     // wave-uniform branch: after the first chunk almost no lane ever takes it
@@ -130,7 +131,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     const int v1 = min(v0 + a.vec_per_split, nvec);
     const u32x4 *rv = reinterpret_cast<const u32x4 *>(rp);
 
-    Lane st{-INFINITY, -1, kFarBelow, 0.f, 0.f};
+    Lane st{-INFINITY, -1, u32x4{0, 0, 0, 0}, kFarBelow, 0.f, 0.f};
     int v = v0 + tid;
     for (; v + (kUnroll - 1) * kReduceThreads < v1; v += kUnroll * kReduceThreads) {
         u32x4 q[kUnroll];
@@ -140,20 +141,28 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
-            consume<NV>(x, v + u * kReduceThreads, st);
+            consume<NV>(x, q[u], v + u * kReduceThreads, st);
         }
     }
     for (; v < v1; v += kReduceThreads) {
         float x[NV];
-        E::unpack(__builtin_nontemporal_load(rv + v), x);
-        consume<NV>(x, v, st);
+        const u32x4 q = __builtin_nontemporal_load(rv + v);
+        E::unpack(q, x);
+        consume<NV>(x, q, v, st);
     }
     // elements past the last whole vector: the last split's first lane
     if (tail > 0 && split == a.splits - 1 && tid == 0) {
         const int64_t e0 = static_cast<int64_t>(nvec) * NV;
         float cm = -INFINITY;
         for (int k = 0; k < tail; ++k) cm = fmaxf(cm, E::at(rp, e0 + k));
-        if (cm > st.best) { st.best = cm; st.chunk = nvec; }
+        if (cm > st.best) {
+            st.best = cm;
+            st.chunk = nvec;
+            uint16_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};      // the partial vector, zero-padded
+            for (int k = 0; k < tail * E::kBytes / 2; ++k) h[k] = reinterpret_cast<const uint16_t *>(rp + e0 * E::kBytes)[k];
+            st.raw = u32x4{h[0] | (uint32_t(h[1]) << 16), h[2] | (uint32_t(h[3]) << 16),
+                           h[4] | (uint32_t(h[5]) << 16), h[6] | (uint32_t(h[7]) << 16)};
+        }
         const float cms = __fmul_rn(cm, kLog2e);
         if (cms > st.ref + kRescaleMargin) rescale(st, cms);
         for (int k = 0; k < tail; ++k) {
@@ -164,14 +173,15 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         }
     }
 
-    // exact first index of the lane's max: re-read the chunk it first appeared in
+    // exact first index of the lane's max, from the saved bits of its first chunk
     int idx = INT_MAX;
     if (st.chunk >= 0) {
+        float x[NV];
+        E::unpack(st.raw, x);
         const int64_t e0 = static_cast<int64_t>(st.chunk) * NV;
-        for (int k = NV - 1; k >= 0; --k) {
-            const int64_t e = e0 + k;
-            if (e < a.V && E::at(rp, e) == st.best) idx = static_cast<int>(e);
-        }
+#pragma unroll
+        for (int k = NV - 1; k >= 0; --k)
+            if (e0 + k < a.V && x[k] == st.best) idx = static_cast<int>(e0 + k);
     }
 
     __shared__ float s_best[kReduceThreads / 64];
