@@ -26,6 +26,21 @@ METRIC = "verified rows/sec (B×(k+1)) and achieved HBM GB/s vs peak, V=151936 b
 HBM_PEAK_GBPS = 8000.0
 
 
+def measured_traffic(kernel_source: str):
+    """HBM bytes per launch of the reduction kernel from the committed rocprofv3 counter
+    summary, or None when that kernel's source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_vocab_reduce_large_chain_traffic.json")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(os.path.join(ROOT, kernel_source), "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("source") != kernel_source or rec.get("source_sha256") != sha:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -167,7 +182,9 @@ def main():
                    "splits": args.splits or "auto", "rows_per_step": rows,
                    "reduced_rows_per_step": reduced_rows},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
+                                 if args.config == 4 and not args.splits else None),
                      "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
                      "algorithmic_bytes_per_launch": logit_bytes},
         "step_hbm_gbps": logit_bytes / (ms_per_step * 1e-3) / 1e9,

@@ -64,8 +64,8 @@ typedef enum {
 typedef enum { COSPEC_F32 = 0, COSPEC_BF16 = 1 } cospec_dtype;
 
 /*
- * Arbitration head g_phi (Section 3.3).  The paper calls it a lightweight
- * binary head on the arbitrator's hidden state without giving its form; this
+ * Arbitration head g_phi (Section 3.3).  The paper gives it no explicit form
+ * beyond a small head on the arbitrator's hidden state with one logit out; this
  * library reads it as a two-layer MLP with a ReLU:
  *     z = w2 . max(W1 h + b1, 0) + b2
  * d must be a multiple of 8 (bf16) or 4 (f32); w1 must be 16-byte aligned.

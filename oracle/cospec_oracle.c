@@ -83,8 +83,8 @@ int64_t oracle_row_stats(const void *rows, int dtype, int64_t ld, int64_t nrows,
 
 /*
  * Arbitration head g_phi applied to selected hidden rows (Section 3.3:
- * z_i = g_phi(h_{l_c+1+i})).  The paper calls g_phi a lightweight binary head
- * without giving its form; it is read here as a two-layer MLP with a ReLU:
+ * z_i = g_phi(h_{l_c+1+i})).  The paper gives g_phi no explicit form beyond a small
+ * head with one logit; it is read here as a two-layer MLP with a ReLU:
  *     u = W1 h + b1   (W1: [hdim][d] row-major, b1: [hdim] or absent = 0)
  *     z = w2 . max(u, 0) + b2
  * Row k of the output uses hidden row rows[k] (which starts at element
