@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (default 4)")
     ap.add_argument("--splits", type=int, default=0, help="workgroups per row (0 = automatic)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the head on a second stream, overlapping the draft-row reduction "
+                         "(slower on the large chain batch: the reduction fills every CU)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     return ap.parse_args()
@@ -76,7 +79,8 @@ def main():
     tgt, drf, hid = wl.target.to(dev), wl.draft.to(dev), wl.hidden.to(dev)
     if tree:
         par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
-        p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits)
+        p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
+                            overlap=args.overlap)
         rows = wl.B * wl.N
         internal = np.zeros((wl.B, wl.N), bool)
         pn = wl.parent.numpy()
@@ -86,11 +90,13 @@ def main():
         reduced_rows = rows + int(internal.sum())
     else:
         tok = wl.draft_tokens.to(dev)
-        p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits)
+        p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
+                             overlap=args.overlap)
         rows = wl.B * (wl.K + 1)
         reduced_rows = wl.B * (2 * wl.K + 1)
     elem = tgt.element_size()
-    logit_bytes = reduced_rows * wl.V * elem       # algorithmic bytes of the reduction launch
+    logit_bytes = reduced_rows * wl.V * elem       # algorithmic bytes of the two reduction launches
+    launch_bytes = logit_bytes / 2.0               # per launch, on average
     torch.cuda.synchronize()
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
@@ -112,21 +118,21 @@ def main():
     total_ms = t0.elapsed_time(t1)
 
     # timed region 2: the same steps with HIP events recorded by the library around
-    # the vocabulary-reduction launch, on the stream it runs on
-    k_begin = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    k_end = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    for e in k_begin + k_end:
+    # the two vocabulary-reduction launches (target rows, draft rows), on the stream
+    # they run on
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for e in (x for row in ev for x in row):
         e.record()                                 # materialise the HIP events
     torch.cuda.synchronize()
     print(f"[bench] timing the reduction kernel over {args.steps} steps", file=sys.stderr, flush=True)
     for i in range(args.steps):
-        p.launch(begin_event=k_begin[i], end_event=k_end[i])
+        p.launch(timing=ev[i])
     torch.cuda.synchronize()
-    k_ms = [b.elapsed_time(e) for b, e in zip(k_begin, k_end)]
-    k_avg = float(np.mean(k_ms))
+    k_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev]
+    k_avg = float(np.mean(k_ms)) / 2.0              # average duration of one launch
     ms_per_step = total_ms / args.steps
     value = rows / (ms_per_step * 1e-3)
-    achieved = logit_bytes / (k_avg * 1e-3) / 1e9
+    achieved = launch_bytes / (k_avg * 1e-3) / 1e9
     res = p.result()
     out = {k: v.cpu() for k, v in res.items()}
 
@@ -179,14 +185,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
-                   "splits": args.splits or "auto", "rows_per_step": rows,
+                   "splits": args.splits or "auto", "head_overlap": args.overlap,
+                   "rows_per_step": rows,
                    "reduced_rows_per_step": reduced_rows},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
                                  if args.config == 4 and not args.splits else None),
                      "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
-                     "algorithmic_bytes_per_launch": logit_bytes},
+                     "launches_per_step": 2, "algorithmic_bytes_per_launch": launch_bytes},
         "step_hbm_gbps": logit_bytes / (ms_per_step * 1e-3) / 1e9,
         "wall_s": wall,
         "mean_accept_len": float(out["accept_len"].float().mean()),

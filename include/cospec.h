@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define COSPEC_ABI_VERSION 1
+#define COSPEC_ABI_VERSION 2
 #define COSPEC_MAX_K 64      /* chain: draft tokens per block              */
 #define COSPEC_MAX_N 256     /* tree: nodes per tree, root included        */
 #define COSPEC_MAX_SPLITS 64 /* workgroups per logit row (tuning override) */
@@ -106,11 +106,29 @@ typedef struct {
     uint8_t *accept;       /* per decision: a_i (1 on matches)                 */
 } cospec_features;
 
-/* Optional tuning and timing hooks; NULL means all defaults. */
+/*
+ * Optional hooks; a NULL options pointer, or zero/NULL members, mean defaults.
+ *
+ * Order of work inside a verify call: (1) reduce the target rows, (2) decide
+ * (verification tokens, Delta, mismatch list), (3) the head on the mismatch
+ * rows, (4) reduce the draft rows, which only feed features, (5) finish
+ * (draft statistics, log p_D, verdicts, first stop, emission).  Steps 3 and 4
+ * are independent.  When `aux_stream` is given, step 3 runs there and overlaps
+ * step 4 on `stream`; `aux_ready` and `aux_done` must then be events created
+ * by the caller on the same device (timing may be disabled); the library
+ * records and waits on them and creates nothing itself.  The call still
+ * completes in `stream` order: work enqueued on `stream` afterwards sees every
+ * output.  Two calls that overlap in time must not share these events.
+ */
 typedef struct {
-    hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ... */
-    hipEvent_t reduce_end;    /* ... and just after the vocabulary-reduction launch */
+    hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ...      */
+    hipEvent_t reduce_end;    /* ... and just after the target-row reduction launch     */
+    hipEvent_t reduce2_begin; /* if non-NULL, recorded on `stream` just before ...      */
+    hipEvent_t reduce2_end;   /* ... and just after the draft-row reduction launch      */
     int32_t splits;           /* workgroups per logit row, 1..COSPEC_MAX_SPLITS; 0 = auto */
+    hipStream_t aux_stream;   /* second stream for the head, or NULL (all on `stream`)  */
+    hipEvent_t aux_ready;     /* required with aux_stream                               */
+    hipEvent_t aux_done;      /* required with aux_stream                               */
 } cospec_options;
 
 /* COSPEC_ABI_VERSION of the built library. */

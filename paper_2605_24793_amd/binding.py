@@ -44,7 +44,16 @@ class _Features(ctypes.Structure):
 
 class _Options(ctypes.Structure):
     _fields_ = [("reduce_begin", ctypes.c_void_p), ("reduce_end", ctypes.c_void_p),
-                ("splits", ctypes.c_int32)]
+                ("reduce2_begin", ctypes.c_void_p), ("reduce2_end", ctypes.c_void_p),
+                ("splits", ctypes.c_int32), ("aux_stream", ctypes.c_void_p),
+                ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p)]
+
+
+def _event_handle(ev) -> int:
+    """Raw hipEvent_t of a torch event (torch creates it at its first record)."""
+    if ev.cuda_event == 0:
+        ev.record()
+    return ev.cuda_event
 
 
 def lib():
@@ -124,25 +133,37 @@ def _stream() -> int:
 
 
 class Prepared:
-    """Pre-marshalled arguments of one verify call: outputs, features and workspace
-    are allocated once, so `launch()` enqueues the step with no allocation."""
+    """Pre-marshalled arguments of one verify call: outputs, features, workspace and
+    (with overlap) the auxiliary stream and its two events are allocated once, so
+    `launch()` enqueues the step with no allocation."""
 
-    def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, opts):
+    def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, splits,
+                 overlap):
         self._fn = fn
         self._args = args_before_feats
         self.outputs = outputs
         self.features = feats
         self._feats = feats_struct
         self.workspace = workspace
-        self._opts = opts
+        self.splits = int(splits)
+        self.aux = None
+        if overlap:
+            dev = workspace.device
+            self.aux = (torch.cuda.Stream(device=dev), torch.cuda.Event(), torch.cuda.Event())
         self._keep = []
 
-    def launch(self, begin_event=None, end_event=None, splits: Optional[int] = None):
-        opts = self._opts
-        if begin_event is not None or end_event is not None or splits is not None:
-            opts = _Options(None if begin_event is None else begin_event.cuda_event,
-                            None if end_event is None else end_event.cuda_event,
-                            int(splits or (self._opts.splits if self._opts else 0)))
+    def _options(self, timing):
+        if timing is None and not self.splits and self.aux is None:
+            return None
+        ev = [None] * 4 if timing is None else [None if e is None else _event_handle(e) for e in timing]
+        aux = (None, None, None) if self.aux is None else (
+            self.aux[0].cuda_stream, _event_handle(self.aux[1]), _event_handle(self.aux[2]))
+        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux)
+
+    def launch(self, timing=None):
+        """Enqueue the step on torch's current stream.  `timing` = four torch events
+        recorded around the target-row and the draft-row reduction launches."""
+        opts = self._options(timing)
         code = self._fn(*self._args, ctypes.byref(self._feats) if self._feats is not None else None,
                         ctypes.byref(opts) if opts is not None else None,
                         _ptr(self.workspace), self.workspace.numel(), _stream())
@@ -169,7 +190,7 @@ def _features(alloc: bool, dev, B, RT, RD, D):
 
 
 def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                  splits: int = 0) -> Prepared:
+                  splits: int = 0, overlap: bool = False) -> Prepared:
     B, R, V = target.shape
     K = R - 1
     ld = _row_stride(target)
@@ -193,14 +214,13 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
             _ptr(draft_tokens) if K > 0 else None, _ptr(hidden) if K > 0 else None,
             ctypes.byref(hs), float(lam), B, K, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]))
-    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace,
-                 _Options(None, None, int(splits)) if splits else None)
+    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits, overlap)
     p._keep = [hs, target, draft, draft_tokens, hidden, head]
     return p
 
 
 def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                 features: bool = True, splits: int = 0) -> Prepared:
+                 features: bool = True, splits: int = 0, overlap: bool = False) -> Prepared:
     B, N, V = target.shape
     ld = _row_stride(target)
     if _row_stride(draft) != ld or tuple(draft.shape) != (B, N, V):
@@ -224,24 +244,24 @@ def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
     args = (_ptr(target), _ptr(draft), _dtype_code(target), ld, _ptr(parent), _ptr(node_tokens),
             _ptr(hidden), ctypes.byref(hs), float(lam), B, N, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]), _ptr(outputs["path"]))
-    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace,
-                 _Options(None, None, int(splits)) if splits else None)
+    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits, overlap)
     p._keep = [hs, target, draft, parent, node_tokens, hidden, head]
     return p
 
 
 def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                 splits: int = 0) -> dict:
+                 splits: int = 0, overlap: bool = False) -> dict:
     """cospec_verify_block on device tensors; returns accept_len, tokens (+ features)."""
-    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits)
+    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits, overlap)
     p.launch()
     return p.result()
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                features: bool = True, splits: int = 0) -> dict:
+                features: bool = True, splits: int = 0, overlap: bool = False) -> dict:
     """cospec_verify_tree on device tensors; returns accept_len, tokens, path (+ features)."""
-    p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits)
+    p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits,
+                     overlap)
     p.launch()
     return p.result()
 

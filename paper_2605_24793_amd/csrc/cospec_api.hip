@@ -2,14 +2,17 @@
 // carving and the launch sequence.  Declared in include/cospec.h.
 //
 // verify_block / verify_tree enqueue, on the caller's stream:
-//   1. k_vocab_reduce   every needed logit row once, split over `splits`
-//                       workgroups per row -> partial (max, argmax, S, T)
-//   2. k_decide         one workgroup per sequence: merge, features, Delta,
-//                       mismatch compaction (device-side count M)
-//   3. k_head           MFMA head over the M compacted rows (skipped when the
+//   1. k_vocab_reduce   the target rows, split over `splits` workgroups per row
+//                       -> partial (max, argmax, S, T); zeroes the list counter
+//   2. k_decide         one workgroup per sequence: target statistics, Delta,
+//                       log p_T, mismatch compaction (device-side count M)
+//   3. k_head_gemm + k_head_epilogue   MFMA head over the M compacted rows
+//                       (on the aux stream when given; skipped when the
 //                       threshold decides every mismatch by itself and no
 //                       score is requested)
-//   4. k_chain_scan / k_tree_scan   verdicts, first stop, emission
+//   4. k_vocab_reduce   the draft rows (tree: nodes with a child)
+//   5. k_chain_finish / k_tree_finish   draft statistics, log p_D, verdicts,
+//                       first stop, emission
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -143,35 +146,41 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     const bool want_scores = F.z_tilde || F.policy;
     const bool head = decisions && (!lambda_decides || want_scores);
 
+    const bool aux = c.opts && c.opts->aux_stream;
+    if (aux && (!c.opts->aux_ready || !c.opts->aux_done || c.opts->aux_stream == c.stream))
+        return COSPEC_ERR_INVALID_ARG;
+
     ReduceArgs ra{};
     ra.tgt = static_cast<const char *>(c.tgt);
     ra.drf = static_cast<const char *>(c.drf);
     ra.ld_bytes = c.ld * eb;
     ra.V = c.V;
     ra.n_tgt_rows = static_cast<int32_t>(c.B * c.RT);
-    ra.n_drf_rows = static_cast<int32_t>(c.B * c.RD);
     ra.parent = c.is_tree ? c.parent : nullptr;
     ra.N = static_cast<int32_t>(c.RT);
     ra.splits = splits;
     ra.vec_per_split = static_cast<int32_t>((nvec + splits - 1) / splits);
     ra.partials = partials;
-    ra.reset_counter = count;
 
-    hipError_t e;
-    if (c.opts && c.opts->reduce_begin && (e = hipEventRecord(c.opts->reduce_begin, c.stream)) != hipSuccess)
-        return COSPEC_ERR_HIP;
-    if ((e = launch_reduce(static_cast<Dtype>(c.dt), ra, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
-    if (c.opts && c.opts->reduce_end && (e = hipEventRecord(c.opts->reduce_end, c.stream)) != hipSuccess)
-        return COSPEC_ERR_HIP;
+    const Dtype dt = static_cast<Dtype>(c.dt);
+    auto record = [&](hipEvent_t ev, hipStream_t s) { return !ev || hipEventRecord(ev, s) == hipSuccess; };
 
+    // 1. target rows
+    ReduceArgs rt = ra;
+    rt.row_offset = 0;
+    rt.n_rows = ra.n_tgt_rows;
+    rt.reset_counter = count;
+    if (!record(c.opts ? c.opts->reduce_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
+    if (launch_reduce(dt, rt, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+    if (!record(c.opts ? c.opts->reduce_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
+
+    // 2. decide
     DecideArgs da{};
     da.tgt = ra.tgt;
-    da.drf = ra.drf;
     da.ld_bytes = ra.ld_bytes;
     da.V = c.V;
     da.B = c.B;
     da.RT = static_cast<int32_t>(c.RT);
-    da.RD = static_cast<int32_t>(c.RD);
     da.D = static_cast<int32_t>(c.D);
     da.is_tree = c.is_tree;
     da.parent = c.parent;
@@ -180,15 +189,15 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     da.splits = splits;
     da.score_mismatch = head;
     da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
-    da.drf_argmax = F.drf_argmax; da.drf_max = F.drf_max; da.drf_lse = F.drf_lse; da.drf_ent = F.drf_entropy;
-    da.logp_tgt = F.logp_tgt; da.logp_drf = F.logp_drf; da.delta = F.delta;
+    da.logp_tgt = F.logp_tgt; da.delta = F.delta;
     da.ws_tgt_arg = tgt_arg;
     da.ws_state = state;
     da.ws_listpos = listpos;
     da.ws_list = list;
     da.ws_count = count;
-    if ((e = launch_decide(static_cast<Dtype>(c.dt), da, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+    if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
 
+    // 3. head, on the aux stream when given
     const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
     if (head) {
         HeadArgs ha{};
@@ -203,31 +212,53 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         ha.ksplit = ksplit_for(m_cap, c.head);
         ha.upart = upart;
         ha.z = zlog;
-        if ((e = launch_head(static_cast<Dtype>(c.head->dtype), ha, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
+        hipStream_t hs = c.stream;
+        if (aux) {
+            if (hipEventRecord(c.opts->aux_ready, c.stream) != hipSuccess ||
+                hipStreamWaitEvent(c.opts->aux_stream, c.opts->aux_ready, 0) != hipSuccess)
+                return COSPEC_ERR_HIP;
+            hs = c.opts->aux_stream;
+        }
+        if (launch_head(static_cast<Dtype>(c.head->dtype), ha, hs) != hipSuccess) return COSPEC_ERR_HIP;
+        if (aux && hipEventRecord(c.opts->aux_done, hs) != hipSuccess) return COSPEC_ERR_HIP;
     }
 
-    if (c.is_tree) {
-        TreeScanArgs ta{};
-        ta.B = c.B; ta.N = static_cast<int32_t>(c.RT);
-        ta.parent = c.parent; ta.node_tokens = c.tokens;
-        ta.ws_state = state; ta.ws_listpos = listpos;
-        ta.z = zlog;
-        ta.head_ran = head; ta.lambda = c.lambda;
-        ta.ws_tgt_arg = tgt_arg;
-        ta.accept_len = accept_len; ta.out_tokens = out_tokens; ta.out_path = out_path;
-        ta.z_tilde = F.z_tilde; ta.policy = F.policy; ta.accept = F.accept;
-        if ((e = launch_tree_scan(ta, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
-    } else {
-        ChainScanArgs sa{};
-        sa.B = c.B; sa.K = static_cast<int32_t>(c.D);
-        sa.ws_state = state; sa.ws_listpos = listpos;
-        sa.z = zlog;
-        sa.head_ran = head; sa.lambda = c.lambda;
-        sa.tokens = c.tokens; sa.ws_tgt_arg = tgt_arg;
-        sa.accept_len = accept_len; sa.out_tokens = out_tokens;
-        sa.z_tilde = F.z_tilde; sa.policy = F.policy; sa.accept = F.accept;
-        if ((e = launch_chain_scan(sa, c.stream)) != hipSuccess) return COSPEC_ERR_HIP;
-    }
+    // 4. draft rows (features only)
+    ReduceArgs rd = ra;
+    rd.row_offset = ra.n_tgt_rows;
+    rd.n_rows = static_cast<int32_t>(c.B * c.RD);
+    rd.reset_counter = nullptr;
+    if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
+    if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+    if (!record(c.opts ? c.opts->reduce2_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
+    if (head && aux && hipStreamWaitEvent(c.stream, c.opts->aux_done, 0) != hipSuccess) return COSPEC_ERR_HIP;
+
+    // 5. finish
+    FinishArgs fa{};
+    fa.drf = ra.drf;
+    fa.ld_bytes = ra.ld_bytes;
+    fa.V = c.V;
+    fa.B = c.B;
+    fa.RT = static_cast<int32_t>(c.RT);
+    fa.RD = static_cast<int32_t>(c.RD);
+    fa.D = static_cast<int32_t>(c.D);
+    fa.is_tree = c.is_tree;
+    fa.parent = c.parent;
+    fa.tokens = c.tokens;
+    fa.partials = partials;
+    fa.splits = splits;
+    fa.drf_row0 = static_cast<int64_t>(c.B) * c.RT;
+    fa.ws_state = state;
+    fa.ws_listpos = listpos;
+    fa.z = zlog;
+    fa.head_ran = head;
+    fa.lambda = c.lambda;
+    fa.ws_tgt_arg = tgt_arg;
+    fa.accept_len = accept_len; fa.out_tokens = out_tokens; fa.out_path = out_path;
+    fa.drf_argmax = F.drf_argmax; fa.drf_max = F.drf_max; fa.drf_lse = F.drf_lse; fa.drf_ent = F.drf_entropy;
+    fa.logp_drf = F.logp_drf;
+    fa.z_tilde = F.z_tilde; fa.policy = F.policy; fa.accept = F.accept;
+    if (launch_finish(dt, fa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     return COSPEC_OK;
 }
 

@@ -26,25 +26,24 @@ struct ReduceArgs {
     const char *drf;           // draft rows
     int64_t ld_bytes;          // row stride in bytes (multiple of 16)
     int32_t V;
-    int32_t n_tgt_rows;        // B * rows-per-sequence of target
-    int32_t n_drf_rows;        // B * rows-per-sequence of draft
+    int32_t n_tgt_rows;        // B * target rows per sequence; rows past it are draft rows
+    int32_t row_offset;        // first row of this launch (target rows, then draft rows)
+    int32_t n_rows;            // rows in this launch
     const int32_t *parent;     // tree: [B][N]; draft rows of leaves are skipped
     int32_t N;                 // tree nodes per tree
     int32_t splits;            // workgroups per row
     int32_t vec_per_split;     // 16-byte vectors per split
     float4 *partials;          // [rows][splits] {max, argmax bits, S, T}
-    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter)
+    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter), or null
 };
 
 struct DecideArgs {
     const char *tgt;
-    const char *drf;
     int64_t ld_bytes;
     int32_t V;
     int32_t B;
     int32_t RT;                // target rows per sequence (K+1 or N)
-    int32_t RD;                // draft rows per sequence (K or N)
-    int32_t D;                 // decision slots per sequence (K, or N with the root)
+    int32_t D;                 // decision slots per sequence (K, or N with the root); <= 256
     int32_t is_tree;
     const int32_t *parent;     // tree only
     const int32_t *tokens;     // chain [B][K], tree [B][N]
@@ -52,8 +51,7 @@ struct DecideArgs {
     int32_t splits;
     int32_t score_mismatch;    // compact mismatches for the head
     int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent;
-    int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent;
-    float *logp_tgt; float *logp_drf; uint8_t *delta;
+    float *logp_tgt; uint8_t *delta;
     int32_t *ws_tgt_arg;       // [B*RT]
     uint8_t *ws_state;         // [B*D]
     int32_t *ws_listpos;       // [B*D] position in the compacted list or -1
@@ -76,30 +74,27 @@ struct HeadArgs {
     float *z;                  // [m_cap] head logits of the selected rows
 };
 
-struct ChainScanArgs {
-    int32_t B, K;
+// Finish: draft-row statistics, log p_D, verdicts, first stop, emission.
+struct FinishArgs {
+    const char *drf;
+    int64_t ld_bytes;
+    int32_t V;
+    int32_t B;
+    int32_t RT, RD, D;         // target rows, draft rows, decision slots per sequence
+    int32_t is_tree;
+    const int32_t *parent;     // tree only
+    const int32_t *tokens;     // chain [B][K], tree [B][N]
+    const float4 *partials;
+    int32_t splits;
+    int64_t drf_row0;          // partial-row index of draft row 0 (= B * RT)
     const uint8_t *ws_state;
     const int32_t *ws_listpos;
     const float *z;            // head logits by compacted position
     int32_t head_ran;
     float lambda;
-    const int32_t *tokens;
-    const int32_t *ws_tgt_arg;
-    int32_t *accept_len; int32_t *out_tokens;
-    float *z_tilde; float *policy; uint8_t *accept;
-};
-
-struct TreeScanArgs {
-    int32_t B, N;
-    const int32_t *parent;
-    const int32_t *node_tokens;
-    const uint8_t *ws_state;
-    const int32_t *ws_listpos;
-    const float *z;
-    int32_t head_ran;
-    float lambda;
     const int32_t *ws_tgt_arg;
     int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
+    int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent; float *logp_drf;
     float *z_tilde; float *policy; uint8_t *accept;
 };
 
@@ -115,8 +110,7 @@ hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
-hipError_t launch_chain_scan(const ChainScanArgs &a, hipStream_t s);
-hipError_t launch_tree_scan(const TreeScanArgs &a, hipStream_t s);
+hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
 
 }  // namespace cospec

@@ -1,4 +1,4 @@
-// Vocabulary reductions and per-sequence decisions.
+// Vocabulary reductions and the per-sequence decision step.
 //
 // k_vocab_reduce streams every logit row once (the step's HBM traffic) and
 // produces, per (row, split), the partial statistics the softmax quantities
@@ -10,55 +10,28 @@
 // Milakov & Gimelshein (2018, "Online normalizer calculation for softmax"),
 // extended with the first moment T; the reference is only raised when a chunk
 // max exceeds it by more than 2^32, so the rescale is almost never taken.
+// One launch covers a contiguous range of rows: the target rows first (the
+// decision needs only them), the draft rows in a second launch.
 //
-// k_decide merges the partials of one sequence's rows in fixed split order,
-// takes the target's greedy verification tokens (argmax, ties to the lowest
-// index), sets Delta = 1[draft token == verification token] (Section 3.1),
-// gathers the draft token's logits for log p_T and log p_D (Section 3.4), and
-// compacts the mismatch decisions into one list for the head with a wave
-// ballot and a prefix over the workgroup's waves.
+// k_decide merges the partials of one sequence's target rows in fixed split
+// order, takes the target's greedy verification tokens (argmax, ties to the
+// lowest index), sets Delta = 1[draft token == verification token]
+// (Section 3.1), gathers the draft token's target logit for log p_T
+// (Section 3.4), and compacts the mismatch decisions into one list for the
+// head with a wave ballot and a prefix over the workgroup's waves.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
 
 #include "launch.h"
+#include "rowstat.h"
 
 namespace cospec {
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleMargin = 32.0f;   // log2 units of headroom above the reference
 constexpr float kFarBelow = -1.0e30f;     // initial reference: any finite logit rescales
 constexpr int kUnroll = 4;                // 16-byte loads in flight per lane
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-template <int DT> struct Elt;
-template <> struct Elt<kBF16> {
-    static constexpr int kPerVec = 8;
-    static constexpr int kBytes = 2;
-    __device__ static inline void unpack(u32x4 q, float *x) {
-        x[0] = __uint_as_float(q.x << 16); x[1] = __uint_as_float(q.x & 0xffff0000u);
-        x[2] = __uint_as_float(q.y << 16); x[3] = __uint_as_float(q.y & 0xffff0000u);
-        x[4] = __uint_as_float(q.z << 16); x[5] = __uint_as_float(q.z & 0xffff0000u);
-        x[6] = __uint_as_float(q.w << 16); x[7] = __uint_as_float(q.w & 0xffff0000u);
-    }
-    __device__ static inline float at(const char *row, int64_t i) {
-        return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t *>(row)[i]) << 16);
-    }
-};
-template <> struct Elt<kF32> {
-    static constexpr int kPerVec = 4;
-    static constexpr int kBytes = 4;
-    __device__ static inline void unpack(u32x4 q, float *x) {
-        x[0] = __uint_as_float(q.x); x[1] = __uint_as_float(q.y);
-        x[2] = __uint_as_float(q.z); x[3] = __uint_as_float(q.w);
-    }
-    __device__ static inline float at(const char *row, int64_t i) {
-        return reinterpret_cast<const float *>(row)[i];
-    }
-};
 
 struct Lane {
     float best;      // largest logit seen
@@ -107,8 +80,8 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     const int tid = threadIdx.x;
-    const int row = blockIdx.x / a.splits;
-    const int split = blockIdx.x - row * a.splits;
+    const int row = a.row_offset + static_cast<int>(blockIdx.x) / a.splits;
+    const int split = static_cast<int>(blockIdx.x) % a.splits;
     if (blockIdx.x == 0 && tid == 0 && a.reset_counter) *a.reset_counter = 0;
 
     const char *rp;
@@ -233,59 +206,36 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     }
 }
 
-struct RowStat {
-    float max, lse, ent;
-    float log_s;     // ln sum exp(x - max): lse - max without the cancellation
-    int arg;
-};
-
-// Fixed-order merge of one row's split partials.
-__device__ inline RowStat merge_row(const float4 *p, int splits) {
-    float M = -INFINITY;
-    int arg = INT_MAX;
-    for (int s = 0; s < splits; ++s) {
-        const float4 q = p[s];
-        if (q.z > 0.f && q.x > M) { M = q.x; arg = __float_as_int(q.y); }   // earlier split wins ties
-    }
-    const float R = __fmul_rn(M, kLog2e);
-    float S = 0.f, T = 0.f;
-    for (int s = 0; s < splits; ++s) {
-        const float4 q = p[s];
-        if (q.z > 0.f) {
-            const float dr = __fmul_rn(q.x, kLog2e) - R;     // the split's reference, as k_vocab_reduce rounded it
-            const float f = __builtin_amdgcn_exp2f(dr);
-            S += f * q.z;
-            T += f * fmaf(dr, q.z, q.w);
-        }
-    }
-    // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
-    // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
-    const float delta = fmaf(M, kLog2e, -R);
-    const float l2s = __log2f(S);
-    RowStat r;
-    r.max = M;
-    r.arg = arg;
-    r.log_s = (l2s - delta) * kLn2;
-    r.lse = M + r.log_s;
-    r.ent = (l2s - T / S) * kLn2;
-    return r;
-}
-
 template <int DT>
 __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     using E = Elt<DT>;
     const int b = blockIdx.x;
     const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
     // per row: max and ln S, so that log p(token) = (x - max) - ln S keeps full
     // precision even when |lse| is large
     __shared__ float s_tmax[kMaxSeqRows], s_tlogs[kMaxSeqRows];
     __shared__ int s_targ[kMaxSeqRows];
-    __shared__ float s_dmax[kMaxSeqRows], s_dlogs[kMaxSeqRows];
-    __shared__ int s_child[kMaxSeqRows];
     __shared__ int s_wave_cnt[kDecideThreads / 64];
     __shared__ int s_base;
 
-    // target rows of this sequence
+    // this thread's decision slot (D <= kDecideThreads): chain slot t is decision t+1,
+    // verified by target row t; tree slot t is node t, verified by its parent's row.
+    // Its token and the target logit at it are fetched while the partials merge.
+    const int slot = t;
+    const int64_t di = static_cast<int64_t>(b) * a.D + slot;
+    const bool decides = slot < a.D && !(a.is_tree && slot == 0);
+    int p = 0;
+    bool valid = false;
+    float xt = 0.f;
+    if (decides) {
+        p = a.is_tree ? a.parent[di] : slot;
+        const int tok = a.tokens[di];
+        valid = (!a.is_tree || (p >= 0 && p < slot)) && tok >= 0 && tok < a.V;
+        if (valid) {
+            xt = E::at(a.tgt + (static_cast<int64_t>(b) * a.RT + p) * a.ld_bytes, tok);
+        }
+    }
     for (int j = t; j < a.RT; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RT + j;
         const RowStat rs = merge_row(a.partials + r * a.splits, a.splits);
@@ -298,93 +248,46 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
         if (a.tgt_lse) a.tgt_lse[r] = rs.lse;
         if (a.tgt_ent) a.tgt_ent[r] = rs.ent;
     }
-    // which draft rows were reduced: every chain row; tree nodes with a child
-    for (int j = t; j < a.RD; j += kDecideThreads) s_child[j] = a.is_tree ? 0 : 1;
-    __syncthreads();
-    if (a.is_tree) {
-        for (int n = 1 + t; n < a.RD; n += kDecideThreads) {
-            const int p = a.parent[static_cast<int64_t>(b) * a.RD + n];
-            if (p >= 0 && p < n) s_child[p] = 1;
-        }
-        __syncthreads();
-    }
-    for (int j = t; j < a.RD; j += kDecideThreads) {
-        const int64_t r = static_cast<int64_t>(b) * a.RD + j;
-        RowStat rs{NAN, NAN, NAN, NAN, -1};
-        if (s_child[j]) rs = merge_row(a.partials + (static_cast<int64_t>(a.B) * a.RT + r) * a.splits, a.splits);
-        s_dmax[j] = rs.max;
-        s_dlogs[j] = rs.log_s;
-        if (a.drf_argmax) a.drf_argmax[r] = rs.arg;
-        if (a.drf_max) a.drf_max[r] = rs.max;
-        if (a.drf_lse) a.drf_lse[r] = rs.lse;
-        if (a.drf_ent) a.drf_ent[r] = rs.ent;
-    }
     __syncthreads();
 
-    // decisions: chain slot t is decision t+1 (verified by row t); tree slot t is node t
-    const int lane = t & 63, wave = t >> 6;
-    for (int base_slot = 0; base_slot < a.D; base_slot += kDecideThreads) {
-        const int slot = base_slot + t;
-        const bool active = slot < a.D;
-        uint8_t state = kStateMatch;
-        float lpt = NAN, lpd = NAN;
-        int hrow = 0;
-        const int64_t di = static_cast<int64_t>(b) * a.D + slot;
-        if (active && !(a.is_tree && slot == 0)) {
-            int p;
-            bool valid = true;
-            if (a.is_tree) {
-                p = a.parent[di];
-                valid = p >= 0 && p < slot;
-                hrow = static_cast<int>(di);
-            } else {
-                p = slot;
-                hrow = static_cast<int>(di);
-            }
-            const int tok = a.tokens[di];
-            valid = valid && tok >= 0 && tok < a.V;
-            if (valid) {
-                const bool match = tok == s_targ[p];
-                const char *trow = a.tgt + (static_cast<int64_t>(b) * a.RT + p) * a.ld_bytes;
-                const char *drow = a.drf + (static_cast<int64_t>(b) * a.RD + p) * a.ld_bytes;
-                lpt = (E::at(trow, tok) - s_tmax[p]) - s_tlogs[p];
-                lpd = (E::at(drow, tok) - s_dmax[p]) - s_dlogs[p];
-                state = match ? kStateMatch : kStateMismatch;
-            } else {
-                state = kStateReject;
-            }
+    uint8_t state = kStateMatch;
+    float lpt = NAN;
+    if (decides) {
+        if (valid) {
+            state = a.tokens[di] == s_targ[p] ? kStateMatch : kStateMismatch;
+            lpt = (xt - s_tmax[p]) - s_tlogs[p];
+        } else {
+            state = kStateReject;
         }
-        const bool need = active && state == kStateMismatch && a.score_mismatch;
-        const uint64_t m = __ballot(need);
-        if (lane == 0) s_wave_cnt[wave] = __popcll(m);
-        __syncthreads();
-        if (t == 0) {
-            int tot = 0;
-            for (int w = 0; w < kDecideThreads / 64; ++w) { const int c = s_wave_cnt[w]; s_wave_cnt[w] = tot; tot += c; }
-            s_base = tot ? atomicAdd(a.ws_count, tot) : 0;
+    }
+    const bool need = decides && state == kStateMismatch && a.score_mismatch;
+    const uint64_t m = __ballot(need);
+    if (lane == 0) s_wave_cnt[wave] = __popcll(m);
+    __syncthreads();
+    if (t == 0) {
+        int tot = 0;
+        for (int w = 0; w < kDecideThreads / 64; ++w) { const int c = s_wave_cnt[w]; s_wave_cnt[w] = tot; tot += c; }
+        s_base = tot ? atomicAdd(a.ws_count, tot) : 0;
+    }
+    __syncthreads();
+    if (slot < a.D) {
+        int pos = -1;
+        if (need) {
+            pos = s_base + s_wave_cnt[wave] + __popcll(m & ((1ull << lane) - 1ull));
+            a.ws_list[pos] = static_cast<int>(di);          // hidden row of the decision
         }
-        __syncthreads();
-        if (active) {
-            int pos = -1;
-            if (need) {
-                pos = s_base + s_wave_cnt[wave] + __popcll(m & ((1ull << lane) - 1ull));
-                a.ws_list[pos] = hrow;
-            }
-            a.ws_listpos[di] = pos;
-            a.ws_state[di] = state;
-            if (a.delta) a.delta[di] = state == kStateMatch;
-            if (a.logp_tgt) a.logp_tgt[di] = lpt;
-            if (a.logp_drf) a.logp_drf[di] = lpd;
-        }
-        __syncthreads();
+        a.ws_listpos[di] = pos;
+        a.ws_state[di] = state;
+        if (a.delta) a.delta[di] = state == kStateMatch;
+        if (a.logp_tgt) a.logp_tgt[di] = lpt;
     }
 }
 
 }  // namespace
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
-    const int64_t rows = static_cast<int64_t>(a.n_tgt_rows) + a.n_drf_rows;
-    const dim3 grid(static_cast<unsigned>(rows * a.splits));
+    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(a.n_rows) * a.splits));
+    if (grid.x == 0) return hipSuccess;
     if (dt == kBF16) hipLaunchKernelGGL(k_vocab_reduce<kBF16>, grid, dim3(kReduceThreads), 0, s, a);
     else hipLaunchKernelGGL(k_vocab_reduce<kF32>, grid, dim3(kReduceThreads), 0, s, a);
     return hipGetLastError();

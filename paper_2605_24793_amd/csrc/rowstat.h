@@ -1,0 +1,82 @@
+// Device helpers shared by the reduction, decide and finish kernels: element
+// access for bf16/fp32 rows and the fixed-order merge of a row's split partials.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "launch.h"
+
+namespace cospec {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <int DT> struct Elt;
+template <> struct Elt<kBF16> {
+    static constexpr int kPerVec = 8;
+    static constexpr int kBytes = 2;
+    __device__ static inline void unpack(u32x4 q, float *x) {
+        x[0] = __uint_as_float(q.x << 16); x[1] = __uint_as_float(q.x & 0xffff0000u);
+        x[2] = __uint_as_float(q.y << 16); x[3] = __uint_as_float(q.y & 0xffff0000u);
+        x[4] = __uint_as_float(q.z << 16); x[5] = __uint_as_float(q.z & 0xffff0000u);
+        x[6] = __uint_as_float(q.w << 16); x[7] = __uint_as_float(q.w & 0xffff0000u);
+    }
+    __device__ static inline float at(const char *row, int64_t i) {
+        return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t *>(row)[i]) << 16);
+    }
+};
+template <> struct Elt<kF32> {
+    static constexpr int kPerVec = 4;
+    static constexpr int kBytes = 4;
+    __device__ static inline void unpack(u32x4 q, float *x) {
+        x[0] = __uint_as_float(q.x); x[1] = __uint_as_float(q.y);
+        x[2] = __uint_as_float(q.z); x[3] = __uint_as_float(q.w);
+    }
+    __device__ static inline float at(const char *row, int64_t i) {
+        return reinterpret_cast<const float *>(row)[i];
+    }
+};
+
+struct RowStat {
+    float max, lse, ent;
+    float log_s;     // ln sum exp(x - max): lse - max without the cancellation
+    int arg;
+};
+
+// Fixed-order merge of one row's split partials.
+__device__ inline RowStat merge_row(const float4 *p, int splits) {
+    float M = -INFINITY;
+    int arg = INT_MAX;
+    for (int s = 0; s < splits; ++s) {
+        const float4 q = p[s];
+        if (q.z > 0.f && q.x > M) { M = q.x; arg = __float_as_int(q.y); }   // earlier split wins ties
+    }
+    const float R = __fmul_rn(M, kLog2e);
+    float S = 0.f, T = 0.f;
+    for (int s = 0; s < splits; ++s) {
+        const float4 q = p[s];
+        if (q.z > 0.f) {
+            const float dr = __fmul_rn(q.x, kLog2e) - R;     // the split's reference, as k_vocab_reduce rounded it
+            const float f = __builtin_amdgcn_exp2f(dr);
+            S += f * q.z;
+            T += f * fmaf(dr, q.z, q.w);
+        }
+    }
+    // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
+    // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
+    const float delta = fmaf(M, kLog2e, -R);
+    const float l2s = __log2f(S);
+    RowStat r;
+    r.max = M;
+    r.arg = arg;
+    r.log_s = (l2s - delta) * kLn2;
+    r.lse = M + r.log_s;
+    r.ent = (l2s - T / S) * kLn2;
+    return r;
+}
+
+}  // namespace cospec

@@ -1,10 +1,17 @@
-// Accept/stop scans and emission.
+// Finish of the verify step: draft-row statistics and log p_D, the per-decision
+// verdicts, the first stop and the emitted tokens.
+//
+// The draft rows are needed only for features (log p_D of the draft token, the
+// draft entropy); the decision itself needs the target rows alone.  So the
+// draft rows are reduced after the decide kernel, while the head may run on a
+// second stream, and merged here.
 //
 // Chain (Section 3.3, Eq. cospec_length): one wave per sequence, lane i-1 owns
-// decision i.  A matched decision passes (z_tilde = +inf, Eq. policy-prob); a
-// mismatch passes when sigma(z) > lambda (Eq. infer_thre).  The first failing
-// decision is the lowest set bit of a wave ballot, s = its position (1-based)
-// or K+1; the round emits draft tokens 1..s-1 and the target token of row s-1.
+// decision i and draft row i-1.  A matched decision passes (z_tilde = +inf,
+// Eq. policy-prob); a mismatch passes when sigma(z) > lambda (Eq. infer_thre).
+// The first failing decision is the lowest set bit of a wave ballot, s = its
+// position (1-based) or K+1; the round emits draft tokens 1..s-1 and the target
+// token of row s-1.
 //
 // Tree (the chain rule along root paths): one workgroup per tree, thread n owns
 // node n.  Reachability (every decision on the root path passes) and depth are
@@ -16,6 +23,7 @@
 #include <stdint.h>
 
 #include "launch.h"
+#include "rowstat.h"
 
 namespace cospec {
 namespace {
@@ -43,15 +51,29 @@ __device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int h
     return v;
 }
 
-__global__ __launch_bounds__(256) void k_chain_scan(ChainScanArgs a) {
+__device__ inline void write_drf(const FinishArgs &a, int64_t r, const RowStat &rs) {
+    if (a.drf_argmax) a.drf_argmax[r] = rs.arg;
+    if (a.drf_max) a.drf_max[r] = rs.max;
+    if (a.drf_lse) a.drf_lse[r] = rs.lse;
+    if (a.drf_ent) a.drf_ent[r] = rs.ent;
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
+    using E = Elt<DT>;
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= a.B) return;                                  // whole wave leaves together
-    const int K = a.K;
+    const int K = a.D;
     bool fail = false;
     if (lane < K) {
-        const int64_t di = static_cast<int64_t>(b) * K + lane;
+        const int64_t di = static_cast<int64_t>(b) * K + lane;        // decision lane+1, draft row lane
         const uint8_t st = a.ws_state[di];
+        const bool valid = st != kStateReject;
+        const float xd = valid ? E::at(a.drf + di * a.ld_bytes, a.tokens[di]) : 0.f;
+        const RowStat rs = merge_row(a.partials + (a.drf_row0 + di) * a.splits, a.splits);
+        write_drf(a, di, rs);
+        if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
         const Verdict v = verdict(st, a.ws_listpos[di], a.z, a.head_ran, a.lambda);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
@@ -69,33 +91,65 @@ __global__ __launch_bounds__(256) void k_chain_scan(ChainScanArgs a) {
     }
 }
 
-__global__ __launch_bounds__(kMaxSeqRows) void k_tree_scan(TreeScanArgs a) {
+template <int DT>
+__global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
+    using E = Elt<DT>;
     const int b = blockIdx.x;
     const int n = threadIdx.x;
-    const int N = a.N;
+    const int N = a.D;
     const int64_t base = static_cast<int64_t>(b) * N;
     __shared__ int s_anc[2][kMaxSeqRows];
     __shared__ int s_dep[2][kMaxSeqRows];
     __shared__ int s_ok[2][kMaxSeqRows];
     __shared__ int s_par[kMaxSeqRows];
     __shared__ int s_path[kMaxSeqRows];
+    __shared__ int s_child[kMaxSeqRows];
+    __shared__ float s_dmax[kMaxSeqRows], s_dlogs[kMaxSeqRows];
     __shared__ int s_key[kMaxSeqRows / 64];
 
-    int anc = -1, dep = 0, ok = 1, par = -1;
+    // node n's parent, state and the draft logit of its token in the parent's row
+    int par = -1;
+    uint8_t st = kStateMatch;
+    float xd = 0.f;
     if (n < N) {
-        const Verdict v = verdict(a.ws_state[base + n], a.ws_listpos[base + n], a.z, a.head_ran, a.lambda);
+        s_child[n] = 0;
+        st = a.ws_state[base + n];
         if (n > 0) {
             par = a.parent[base + n];
-            const bool valid = par >= 0 && par < n;
-            if (!valid) par = -1;
+            if (!(par >= 0 && par < n)) par = -1;
+            if (st != kStateReject && par >= 0)
+                xd = E::at(a.drf + (base + par) * a.ld_bytes, a.tokens[base + n]);
+        }
+        s_par[n] = par;
+    }
+    __syncthreads();
+    if (n < N && par >= 0) s_child[par] = 1;
+    __syncthreads();
+    // draft rows were reduced for nodes with a child only
+    if (n < N) {
+        RowStat rs{NAN, NAN, NAN, NAN, -1};
+        if (s_child[n]) rs = merge_row(a.partials + (a.drf_row0 + base + n) * a.splits, a.splits);
+        write_drf(a, base + n, rs);
+        s_dmax[n] = rs.max;
+        s_dlogs[n] = rs.log_s;
+    }
+    __syncthreads();
+
+    int anc = -1, dep = 0, ok = 1;
+    if (n < N) {
+        const Verdict v = verdict(st, a.ws_listpos[base + n], a.z, a.head_ran, a.lambda);
+        if (n > 0) {
             anc = par;
             dep = 1;
-            ok = valid && v.pass;
+            ok = par >= 0 && v.pass;
+            if (a.logp_drf)
+                a.logp_drf[base + n] = (st != kStateReject && par >= 0) ? (xd - s_dmax[par]) - s_dlogs[par] : NAN;
+        } else if (a.logp_drf) {
+            a.logp_drf[base] = NAN;
         }
         if (a.z_tilde) a.z_tilde[base + n] = v.z_tilde;
         if (a.policy) a.policy[base + n] = v.policy;
         if (a.accept) a.accept[base + n] = n == 0 ? 1 : v.pass;
-        s_par[n] = par;
     }
     // pointer jumping: anc = ancestor 2^k steps up (or -1), dep = distance to it,
     // ok = every decision from this node up to (not including) anc passes
@@ -140,7 +194,7 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_scan(TreeScanArgs a) {
     const int best = s_key[0], depth = s_key[1];
     if (n < N) {
         int tok = -1;
-        if (n < depth) tok = a.node_tokens[base + s_path[n + 1]];
+        if (n < depth) tok = a.tokens[base + s_path[n + 1]];
         else if (n == depth) tok = a.ws_tgt_arg[base + best];
         a.out_tokens[base + n] = tok;
         if (a.out_path) a.out_path[base + n] = n <= depth ? s_path[n] : -1;
@@ -149,16 +203,16 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_scan(TreeScanArgs a) {
 
 }  // namespace
 
-hipError_t launch_chain_scan(const ChainScanArgs &a, hipStream_t s) {
-    const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
-    if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_chain_scan, dim3(blocks), dim3(256), 0, s, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_tree_scan(const TreeScanArgs &a, hipStream_t s) {
+hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s) {
     if (a.B == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_tree_scan, dim3(static_cast<unsigned>(a.B)), dim3(kMaxSeqRows), 0, s, a);
+    if (a.is_tree) {
+        if (dt == kBF16) hipLaunchKernelGGL(k_tree_finish<kBF16>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
+        else hipLaunchKernelGGL(k_tree_finish<kF32>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
+    } else {
+        const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
+        if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish<kBF16>, dim3(blocks), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(k_chain_finish<kF32>, dim3(blocks), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -109,10 +109,17 @@ def test_verify_block_rejects_before_launch(kw, code):
 
 def test_verify_block_split_override_limits():
     L = cs.lib()
-    assert _block(L, opts=ctypes.byref(binding._Options(None, None, 65))) == UNSUPPORTED
-    assert _block(L, opts=ctypes.byref(binding._Options(None, None, -2))) == UNSUPPORTED
+    assert _block(L, opts=ctypes.byref(binding._Options(splits=65))) == UNSUPPORTED
+    assert _block(L, opts=ctypes.byref(binding._Options(splits=-2))) == UNSUPPORTED
     # 4 x 15 rows x 64 splits fits the partial buffer; the workspace is checked after
-    assert _block(L, wsb=16, opts=ctypes.byref(binding._Options(None, None, 64))) == WORKSPACE
+    assert _block(L, wsb=16, opts=ctypes.byref(binding._Options(splits=64))) == WORKSPACE
+
+
+def test_verify_block_aux_stream_needs_its_events():
+    L = cs.lib()
+    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE))) == INVALID
+    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE, aux_ready=FAKE))) == INVALID
+    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE, aux_done=FAKE))) == INVALID
 
 
 def _tree(L, **kw):

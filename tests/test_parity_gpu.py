@@ -45,10 +45,10 @@ def _padded(t, pad):
     return big[:, :, :V]
 
 
-def _gpu_block(wl, lam, splits=0, pad=0, features=True):
+def _gpu_block(wl, lam, splits=0, pad=0, features=True, overlap=False):
     out = cs.verify_block(_padded(wl.target, pad), _padded(wl.draft, pad), wl.draft_tokens.to(DEV),
                           wl.hidden.to(DEV), _head_dev(wl.head), lam, features=features,
-                          splits=splits)
+                          splits=splits, overlap=overlap)
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
 
@@ -58,10 +58,10 @@ def _ref_block(wl, lam):
                                _conv(wl.hidden), _head_np(wl.head), lam)
 
 
-def _gpu_tree(tr, lam, splits=0, pad=0):
+def _gpu_tree(tr, lam, splits=0, pad=0, overlap=False):
     out = cs.verify_tree(_padded(tr.target, pad), _padded(tr.draft, pad), tr.parent.to(DEV),
                          tr.node_tokens.to(DEV), tr.hidden.to(DEV), _head_dev(tr.head), lam,
-                         splits=splits)
+                         splits=splits, overlap=overlap)
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
 
@@ -92,7 +92,7 @@ def test_config_full(cfg):
 def test_config3_full_lambda_sweep():
     wl = workloads.make_config(3)
     for lam in wl.lambdas:
-        gpu = _gpu_block(wl, lam)
+        gpu = _gpu_block(wl, lam, overlap=True)
         stats = parity.check_block(gpu, _ref_block(wl, lam))
         _report(f"config 3 lambda {lam}", stats, gpu)
 
@@ -105,7 +105,7 @@ def _sample(B, n, seed):
 def test_config4_full_size_sampled():
     wl = workloads.make_config(4)
     lam = wl.lambdas[0]
-    gpu = _gpu_block(wl, lam)
+    gpu = _gpu_block(wl, lam, overlap=True)
     seqs = _sample(wl.B, 32, 40)
     sub = {k: v[seqs] for k, v in gpu.items()}
     stats = parity.check_block(sub, _ref_block(wl.take(seqs), lam))
@@ -116,7 +116,7 @@ def test_config4_full_size_sampled():
 def test_config5_full_size_sampled():
     tr = workloads.make_config(5)
     lam = tr.lambdas[0]
-    gpu = _gpu_tree(tr, lam)
+    gpu = _gpu_tree(tr, lam, overlap=True)
     seqs = _sample(tr.B, 12, 50)
     sub = {k: v[seqs] for k, v in gpu.items()}
     stats = parity.check_tree(sub, _ref_tree(tr.take(seqs), lam))
@@ -273,6 +273,21 @@ def test_always_accept_on_gpu(lam):
     gpu = _gpu_block(wl, lam, features=False)
     assert (gpu["accept_len"] == wl.K + 1).all()
     assert torch.equal(gpu["tokens"][:, : wl.K], wl.draft_tokens)
+
+
+def test_overlap_stream_gives_identical_results():
+    wl = workloads.make_chain(B=40, K=7, V=30001, d=256, h=128, seed=12, bias=True, noise=1.2)
+    a = _gpu_block(wl, 0.5)
+    b = _gpu_block(wl, 0.5, overlap=True)
+    for k in a:
+        assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
+                           b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
+    tr = workloads.make_random_tree(B=6, N=40, V=3001, d=64, h=32, seed=13, bias=True)
+    a = _gpu_tree(tr, 0.5)
+    b = _gpu_tree(tr, 0.5, overlap=True)
+    for k in a:
+        assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
+                           b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
 
 
 def test_splits_and_repeat_are_deterministic():
