@@ -31,13 +31,13 @@ namespace {
 
 constexpr float kRescaleMargin = 32.0f;   // log2 units of headroom above the reference
 constexpr float kFarBelow = -1.0e30f;     // initial reference: any finite logit rescales
-constexpr int kUnroll = 4;                // 16-byte loads in flight per lane
+constexpr int kUnroll = 8;                // 16-byte loads in flight per lane
 
 struct Lane {
     float best;      // largest logit seen
     int chunk;       // first chunk (16-byte vector index) holding `best`, -1 if none
-    u32x4 raw;       // that chunk's bits: the exact index is found without a re-read
     float ref;       // reference of S and T, in log2 units
+    float thresh;    // logits above this need a larger reference: (ref + margin) / log2e
     float S, T;
 };
 
@@ -47,19 +47,21 @@ __device__ inline void rescale(Lane &st, float new_ref) {
     st.T = f * fmaf(dr, st.S, st.T);
     st.S = f * st.S;
     st.ref = new_ref;
+    st.thresh = (new_ref + kRescaleMargin) * kLn2;
 }
 
 template <int NV>
-__device__ inline void consume(const float *x, u32x4 q, int chunk, Lane &st) {
+__device__ inline void consume(const float *x, int chunk, Lane &st) {
     float cm = -INFINITY;
 #pragma unroll
     for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
-    if (cm > st.best) { st.best = cm; st.chunk = chunk; st.raw = q; }
-    const float cms = __fmul_rn(cm, kLog2e);
-    const bool up = cms > st.ref + kRescaleMargin;
-    // wave-uniform branch: after the first chunk almost no lane ever takes it
+    if (cm > st.best) { st.best = cm; st.chunk = chunk; }
+    // wave-uniform branch: after the first chunk almost no lane ever takes it.  The
+    // test is in the logit domain; the threshold is conservative by its rounding,
+    // which only makes a rescale slightly more likely.
+    const bool up = cm > st.thresh;
     if (__builtin_expect(__ballot(up) != 0, 0)) {
-        if (up) rescale(st, cms);
+        if (up) rescale(st, __fmul_rn(cm, kLog2e));
     }
     const float nref = -st.ref;
 #pragma unroll
@@ -69,10 +71,6 @@ __device__ inline void consume(const float *x, u32x4 q, int chunk, Lane &st) {
         st.S += e;
         st.T = fmaf(e, t, st.T);
     }
-}
-
-__device__ inline bool better(float v, int i, float bv, int bi) {
-    return v > bv || (v == bv && i < bi);
 }
 
 template <int DT>
@@ -104,7 +102,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     const int v1 = min(v0 + a.vec_per_split, nvec);
     const u32x4 *rv = reinterpret_cast<const u32x4 *>(rp);
 
-    Lane st{-INFINITY, -1, u32x4{0, 0, 0, 0}, kFarBelow, 0.f, 0.f};
+    Lane st{-INFINITY, -1, kFarBelow, -INFINITY, 0.f, 0.f};   // the first chunk always rescales
     int v = v0 + tid;
     for (; v + (kUnroll - 1) * kReduceThreads < v1; v += kUnroll * kReduceThreads) {
         u32x4 q[kUnroll];
@@ -114,30 +112,21 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
-            consume<NV>(x, q[u], v + u * kReduceThreads, st);
+            consume<NV>(x, v + u * kReduceThreads, st);
         }
     }
     for (; v < v1; v += kReduceThreads) {
         float x[NV];
-        const u32x4 q = __builtin_nontemporal_load(rv + v);
-        E::unpack(q, x);
-        consume<NV>(x, q, v, st);
+        E::unpack(__builtin_nontemporal_load(rv + v), x);
+        consume<NV>(x, v, st);
     }
     // elements past the last whole vector: the last split's first lane
     if (tail > 0 && split == a.splits - 1 && tid == 0) {
         const int64_t e0 = static_cast<int64_t>(nvec) * NV;
         float cm = -INFINITY;
         for (int k = 0; k < tail; ++k) cm = fmaxf(cm, E::at(rp, e0 + k));
-        if (cm > st.best) {
-            st.best = cm;
-            st.chunk = nvec;
-            uint16_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};      // the partial vector, zero-padded
-            for (int k = 0; k < tail * E::kBytes / 2; ++k) h[k] = reinterpret_cast<const uint16_t *>(rp + e0 * E::kBytes)[k];
-            st.raw = u32x4{h[0] | (uint32_t(h[1]) << 16), h[2] | (uint32_t(h[3]) << 16),
-                           h[4] | (uint32_t(h[5]) << 16), h[6] | (uint32_t(h[7]) << 16)};
-        }
-        const float cms = __fmul_rn(cm, kLog2e);
-        if (cms > st.ref + kRescaleMargin) rescale(st, cms);
+        if (cm > st.best) { st.best = cm; st.chunk = nvec; }
+        if (cm > st.thresh) rescale(st, __fmul_rn(cm, kLog2e));
         for (int k = 0; k < tail; ++k) {
             const float t = fmaf(E::at(rp, e0 + k), kLog2e, -st.ref);
             const float e = __builtin_amdgcn_exp2f(t);
@@ -146,42 +135,48 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         }
     }
 
-    // exact first index of the lane's max, from the saved bits of its first chunk
-    int idx = INT_MAX;
-    if (st.chunk >= 0) {
-        float x[NV];
-        E::unpack(st.raw, x);
-        const int64_t e0 = static_cast<int64_t>(st.chunk) * NV;
-#pragma unroll
-        for (int k = NV - 1; k >= 0; --k)
-            if (e0 + k < a.V && x[k] == st.best) idx = static_cast<int>(e0 + k);
-    }
-
     __shared__ float s_best[kReduceThreads / 64];
     __shared__ int s_idx[kReduceThreads / 64];
     __shared__ float s_S[kReduceThreads / 64], s_T[kReduceThreads / 64];
     __shared__ float s_M;
     const int lane = tid & 63, wave = tid >> 6;
 
+    // the workgroup's max, then its first index: only lanes that hold the max look
+    // again at the first chunk where they saw it (one 16-byte load, usually one lane)
     float bv = st.best;
-    int bi = idx;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const float ov = __shfl_xor(bv, off);
-        const int oi = __shfl_xor(bi, off);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (lane == 0) { s_best[wave] = bv; s_idx[wave] = bi; }
+    for (int off = 32; off >= 1; off >>= 1) bv = fmaxf(bv, __shfl_xor(bv, off));
+    if (lane == 0) s_best[wave] = bv;
     __syncthreads();
     if (tid == 0) {
         float M = s_best[0];
-        int I = s_idx[0];
-        for (int w = 1; w < kReduceThreads / 64; ++w)
-            if (better(s_best[w], s_idx[w], M, I)) { M = s_best[w]; I = s_idx[w]; }
+        for (int w = 1; w < kReduceThreads / 64; ++w) M = fmaxf(M, s_best[w]);
         s_M = M;
-        s_idx[0] = I;
     }
     __syncthreads();
+    int idx = INT_MAX;
+    if (st.chunk >= 0 && st.best == s_M) {
+        const int64_t e0 = static_cast<int64_t>(st.chunk) * NV;
+        float x[NV];
+        if (st.chunk < nvec) {
+            E::unpack(__builtin_nontemporal_load(rv + st.chunk), x);
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) x[k] = e0 + k < a.V ? E::at(rp, e0 + k) : -INFINITY;
+        }
+#pragma unroll
+        for (int k = NV - 1; k >= 0; --k)
+            if (e0 + k < a.V && x[k] == st.best) idx = static_cast<int>(e0 + k);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) idx = min(idx, __shfl_xor(idx, off));
+    if (lane == 0) s_idx[wave] = idx;
+    __syncthreads();
+    if (tid == 0) {
+        int I = s_idx[0];
+        for (int w = 1; w < kReduceThreads / 64; ++w) I = min(I, s_idx[w]);
+        s_idx[0] = I;
+    }
     const float M = s_M;
     const float R = __fmul_rn(M, kLog2e);   // the partial's reference: rounded, never contracted
     float S = 0.f, T = 0.f;
