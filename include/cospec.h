@@ -109,22 +109,23 @@ typedef struct {
 /*
  * Optional hooks; a NULL options pointer, or zero/NULL members, mean defaults.
  *
- * Order of work inside a verify call: (1) reduce the target rows, (2) decide
+ * Order of work inside a verify call: (1) reduce the logit rows, (2) decide
  * (verification tokens, Delta, mismatch list), (3) the head on the mismatch
- * rows, (4) reduce the draft rows, which only feed features, (5) finish
- * (draft statistics, log p_D, verdicts, first stop, emission).  Steps 3 and 4
- * are independent.  When `aux_stream` is given, step 3 runs there and overlaps
- * step 4 on `stream`; `aux_ready` and `aux_done` must then be events created
+ * rows, (4) finish (draft statistics, log p_D, verdicts, first stop, emission).
+ * The draft rows only feed features, so the decision needs the target rows
+ * alone.  When `aux_stream` is given, step 1 reduces only the target rows and
+ * the draft rows are reduced on `stream` while step 3 runs on `aux_stream`;
+ * `aux_ready` and `aux_done` must then be events created
  * by the caller on the same device (timing may be disabled); the library
  * records and waits on them and creates nothing itself.  The call still
  * completes in `stream` order: work enqueued on `stream` afterwards sees every
  * output.  Two calls that overlap in time must not share these events.
  */
 typedef struct {
-    hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ...      */
-    hipEvent_t reduce_end;    /* ... and just after the target-row reduction launch     */
-    hipEvent_t reduce2_begin; /* if non-NULL, recorded on `stream` just before ...      */
-    hipEvent_t reduce2_end;   /* ... and just after the draft-row reduction launch      */
+    hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ...        */
+    hipEvent_t reduce_end;    /* ... and just after the first reduction launch            */
+    hipEvent_t reduce2_begin; /* if non-NULL, recorded on `stream` just before ...        */
+    hipEvent_t reduce2_end;   /* ... and after the draft-row launch (back to back if none) */
     int32_t splits;           /* workgroups per logit row, 1..COSPEC_MAX_SPLITS; 0 = auto */
     hipStream_t aux_stream;   /* second stream for the head, or NULL (all on `stream`)  */
     hipEvent_t aux_ready;     /* required with aux_stream                               */

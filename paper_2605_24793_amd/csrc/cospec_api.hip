@@ -2,15 +2,18 @@
 // carving and the launch sequence.  Declared in include/cospec.h.
 //
 // verify_block / verify_tree enqueue, on the caller's stream:
-//   1. k_vocab_reduce   the target rows, split over `splits` workgroups per row
-//                       -> partial (max, argmax, S, T); zeroes the list counter
+//   1. k_vocab_reduce   the target and draft rows (only the target rows when the
+//                       head overlaps step 4 on the aux stream), split over
+//                       `splits` workgroups per row -> partial (max, argmax, S, T);
+//                       zeroes the list counter
 //   2. k_decide         one workgroup per sequence: target statistics, Delta,
 //                       log p_T, mismatch compaction (device-side count M)
 //   3. k_head_gemm + k_head_epilogue   MFMA head over the M compacted rows
 //                       (on the aux stream when given; skipped when the
 //                       threshold decides every mismatch by itself and no
 //                       score is requested)
-//   4. k_vocab_reduce   the draft rows (tree: nodes with a child)
+//   4. k_vocab_reduce   with the aux stream only: the draft rows (tree: nodes with
+//                       a child)
 //   5. k_chain_finish / k_tree_finish   draft statistics, log p_D, verdicts,
 //                       first stop, emission
 #include <hip/hip_runtime.h>
@@ -165,10 +168,12 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     const Dtype dt = static_cast<Dtype>(c.dt);
     auto record = [&](hipEvent_t ev, hipStream_t s) { return !ev || hipEventRecord(ev, s) == hipSuccess; };
 
-    // 1. target rows
+    // 1. target rows; the draft rows too in the same launch unless the head overlaps
+    //    their reduction on the aux stream (one launch is cheaper than two)
+    const bool split_reduce = aux && head;
     ReduceArgs rt = ra;
     rt.row_offset = 0;
-    rt.n_rows = ra.n_tgt_rows;
+    rt.n_rows = split_reduce ? ra.n_tgt_rows : static_cast<int32_t>(c.B * (c.RT + c.RD));
     rt.reset_counter = count;
     if (!record(c.opts ? c.opts->reduce_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rt, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
@@ -223,10 +228,10 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         if (aux && hipEventRecord(c.opts->aux_done, hs) != hipSuccess) return COSPEC_ERR_HIP;
     }
 
-    // 4. draft rows (features only)
+    // 4. draft rows (features only), when they were not reduced with the target rows
     ReduceArgs rd = ra;
     rd.row_offset = ra.n_tgt_rows;
-    rd.n_rows = static_cast<int32_t>(c.B * c.RD);
+    rd.n_rows = split_reduce ? static_cast<int32_t>(c.B * c.RD) : 0;
     rd.reset_counter = nullptr;
     if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
