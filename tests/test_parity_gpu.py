@@ -290,6 +290,21 @@ def test_overlap_stream_gives_identical_results():
                            b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
 
 
+@pytest.mark.parametrize("logit_dtype,head_dtype", [("bf16", "f32"), ("f32", "bf16")])
+def test_mixed_logit_and_head_dtypes(logit_dtype, head_dtype):
+    wl = workloads.make_chain(B=9, K=6, V=5003, d=128, h=96, dtype=logit_dtype, seed=31, bias=True)
+    wl.head = workloads.make_head(31, 128, 96, head_dtype, bias=True)
+    wl.hidden = wl.hidden.to(wl.head.w1.dtype)
+    gpu = _gpu_block(wl, 0.5)
+    stats = parity.check_block(gpu, _ref_block(wl, 0.5))
+    _report(f"mixed logits {logit_dtype} head {head_dtype}", stats, gpu)
+    tr = workloads.make_random_tree(B=3, N=20, V=3001, d=128, h=96, dtype=logit_dtype, seed=32)
+    tr.head = workloads.make_head(32, 128, 96, head_dtype, bias=True)
+    tr.hidden = tr.hidden.to(tr.head.w1.dtype)
+    gpu = _gpu_tree(tr, 0.5)
+    parity.check_tree(gpu, _ref_tree(tr, 0.5))
+
+
 def test_splits_and_repeat_are_deterministic():
     wl = workloads.make_chain(B=6, K=5, V=40000, d=128, h=64, seed=8, bias=True)
     runs = [_gpu_block(wl, 0.5, splits=s) for s in (1, 1, 4, 17)]
