@@ -10,8 +10,9 @@
 // Milakov & Gimelshein (2018, "Online normalizer calculation for softmax"),
 // extended with the first moment T; the reference is only raised when a chunk
 // max exceeds it by more than 2^32, so the rescale is almost never taken.
-// One launch covers a contiguous range of rows: the target rows first (the
-// decision needs only them), the draft rows in a second launch.
+// One launch covers a contiguous range of rows, target rows before draft rows
+// (normally all of them; the draft rows get a launch of their own when the
+// head overlaps them on a second stream).
 //
 // k_decide merges the partials of one sequence's target rows in fixed split
 // order, takes the target's greedy verification tokens (argmax, ties to the
