@@ -19,6 +19,9 @@ Readings of the paper used here (each also listed with the design notes):
     precision the GPU path takes it in; decisions with |sigma(z) - lambda| <= 1e-3
     (in fp64) are flagged ambiguous;
   * every mismatch decision is scored, not only those before the stop;
+  * at temperature 1 the target's verification candidate of a row is a sample
+    of softmax(row), taken by inversion of a caller-supplied uniform u: the
+    smallest v whose cumulative probability (index order) exceeds u;
   * trees: node 0 is the root; child c of p is verified by target row p and
     scored on hidden row c; the accepted node is the deepest node whose whole
     root path passes (match or accepted), ties to the lowest node id.
@@ -39,7 +42,8 @@ import numpy as np
 __all__ = [
     "F32", "BF16", "AMBIGUITY_BAND", "build", "row_stats", "element", "head_logits",
     "policy_accept", "chain_length", "chain_tokens", "tree_select", "verify_block",
-    "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats",
+    "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats", "sample_rows",
+    "cdf_at", "candidates",
 ]
 
 F32, BF16 = 0, 1
@@ -70,6 +74,10 @@ def _load():
         I64 = ctypes.c_int64
         lib.oracle_row_stats.restype = I64
         lib.oracle_row_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P]
+        lib.oracle_sample_rows.restype = I64
+        lib.oracle_sample_rows.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
+        lib.oracle_cdf_at.restype = I64
+        lib.oracle_cdf_at.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P]
         lib.oracle_head.restype = None
         lib.oracle_head.argtypes = [P, ctypes.c_int, I64, P, I64, P, P, P, ctypes.c_double, I64,
                                     I64, P]
@@ -121,6 +129,61 @@ def row_stats(rows: np.ndarray) -> RowStats:
         if rc != 0:
             raise ValueError(f"non-finite logit in row {-rc - 1}")
     return RowStats(mx.reshape(shape), arg.reshape(shape), lse.reshape(shape), ent.reshape(shape))
+
+
+def sample_rows(rows: np.ndarray, u):
+    """Temperature-1 samples of every row of a [..., V] array by inversion (see
+    oracle_sample_rows): the smallest v with P(v) > u, P the cumulative softmax in
+    index order.  Returns (index, P(index-1), P(index)) with the rows' shape."""
+    rows = np.ascontiguousarray(rows)
+    shape = rows.shape[:-1]
+    V = rows.shape[-1]
+    n = int(np.prod(shape)) if shape else 1
+    uu = np.ascontiguousarray(np.asarray(u, dtype=np.float64).reshape(n))
+    idx = np.empty(n, np.int64)
+    lo = np.empty(n, np.float64)
+    hi = np.empty(n, np.float64)
+    work = np.empty(max(V, 1), np.float64)
+    if n:
+        rc = _load().oracle_sample_rows(_ptr(rows), _code(rows), V, n, V, _ptr(uu), _ptr(work),
+                                        _ptr(idx), _ptr(lo), _ptr(hi))
+        if rc != 0:
+            raise ValueError(f"non-finite logit in row {-rc - 1}")
+    return idx.reshape(shape), lo.reshape(shape), hi.reshape(shape)
+
+
+def cdf_at(rows: np.ndarray, idx):
+    """(P(idx-1), P(idx)) of every row for given candidate indices: the interval of
+    uniforms that inversion sampling maps to idx."""
+    rows = np.ascontiguousarray(rows)
+    shape = rows.shape[:-1]
+    V = rows.shape[-1]
+    n = int(np.prod(shape)) if shape else 1
+    ii = np.ascontiguousarray(np.asarray(idx, dtype=np.int64).reshape(n))
+    lo = np.empty(n, np.float64)
+    hi = np.empty(n, np.float64)
+    work = np.empty(max(V, 1), np.float64)
+    if n:
+        rc = _load().oracle_cdf_at(_ptr(rows), _code(rows), V, n, V, _ptr(ii), _ptr(work),
+                                   _ptr(lo), _ptr(hi))
+        if rc == -(n + 1):
+            raise IndexError("candidate index out of range")
+        if rc != 0:
+            raise ValueError(f"non-finite logit in row {-rc - 1}")
+    return lo.reshape(shape), hi.reshape(shape)
+
+
+def candidates(target, stats: "RowStats", sample_u=None, override=None):
+    """The target's verification candidate of every target row: the argmax at
+    T = 0 (Section 3.1), a temperature-1 sample by inversion of the uniform
+    `sample_u` at T = 1 (Section 2, Appendix C.3).  `override` replaces the
+    computed candidates (a test passes another implementation's candidates
+    after checking each against cdf_at)."""
+    if override is not None:
+        return np.asarray(override, dtype=np.int64).reshape(stats.arg.shape)
+    if sample_u is None:
+        return stats.arg
+    return sample_rows(target, sample_u)[0]
 
 
 def head_logits(hidden: np.ndarray, rows, w1: np.ndarray, b1: Optional[np.ndarray],
@@ -221,14 +284,17 @@ def _head_arrays(head):
     return w1, b1, w2, float(b2)
 
 
-def verify_block(target, draft, draft_tokens, hidden, head, lam: float) -> dict:
+def verify_block(target, draft, draft_tokens, hidden, head, lam: float, sample_u=None,
+                 cand_override=None) -> dict:
     """Oracle of one chain verify step.
 
     target [B, K+1, V], draft [B, K, V] (float32 or bf16 bits), draft_tokens int
     [B, K], hidden [B, K, d], head = (W1 [h, d], b1 [h] or None, w2 [h], b2).
-    Decision i (1..K) compares draft token i with the argmax of target row i-1
-    (Section 3.1, Delta_i), scores mismatches with the head (Section 3.3), and the
-    round stops at the first rejected mismatch (Eq. cospec_length).
+    Decision i (1..K) compares draft token i with the target's candidate from row
+    i-1 (Section 3.1, Delta_i): its argmax, or with sample_u [B, K+1] its
+    temperature-1 sample (see candidates()).  Mismatches are scored with the head
+    (Section 3.3) and the round stops at the first rejected mismatch
+    (Eq. cospec_length), emitting the candidate of row s-1 last.
     """
     B, K1, V = target.shape
     K = K1 - 1
@@ -238,7 +304,8 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float) -> dict:
         raise ValueError("draft token out of range")
     ts = row_stats(target)
     ds = row_stats(draft)
-    ytil = ts.arg[:, :K]                                   # ytilde_i = argmax of row i-1
+    cand = candidates(target, ts, sample_u, cand_override)
+    ytil = cand[:, :K]                                     # ytilde_i = candidate of row i-1
     delta = (toks == ytil)
     logp_tgt = _gather(target[:, :K, :], toks) - ts.lse[:, :K]
     logp_drf = _gather(draft, toks) - ds.lse
@@ -259,9 +326,9 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float) -> dict:
     for b in range(B):
         s = chain_length(delta[b], accept[b])
         accept_len[b] = s
-        tokens[b] = chain_tokens(s, toks[b], ts.arg[b])
-        outcomes.append(chain_outcomes(delta[b], accept[b], ambiguous[b], toks[b], ts.arg[b]))
-    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent,
+        tokens[b] = chain_tokens(s, toks[b], cand[b])
+        outcomes.append(chain_outcomes(delta[b], accept[b], ambiguous[b], toks[b], cand[b]))
+    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent, tgt_cand=cand,
                 drf_max=ds.max, drf_arg=ds.arg, drf_lse=ds.lse, drf_ent=ds.ent,
                 delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z, z_tilde=z_tilde,
                 pi=pi, accept=accept, ambiguous=ambiguous, accept_len=accept_len,
@@ -295,13 +362,15 @@ def _internal(parent) -> np.ndarray:
     return has_child
 
 
-def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float) -> dict:
+def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float, sample_u=None,
+                cand_override=None) -> dict:
     """Oracle of one tree verify step (tree reading of Section 3.1/3.3).
 
     target, draft [B, N, V]; parent int [B, N] (parent[0] = -1, parent[n] < n);
     node_tokens int [B, N]; hidden [B, N, d].  Only draft rows of nodes with a
     child are reduced (leaf draft rows verify nothing); their statistics are NaN /
-    -1 for leaves.  Node 0 carries no decision.
+    -1 for leaves.  Node 0 carries no decision.  With sample_u [B, N] the
+    candidate of each target row is its temperature-1 sample (see candidates()).
     """
     B, N, V = target.shape
     par = np.asarray(parent, dtype=np.int64)
@@ -312,6 +381,7 @@ def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float) ->
     if N > 1 and (toks[:, 1:].min() < 0 or toks[:, 1:].max() >= V):
         raise ValueError("node token out of range")
     ts = row_stats(target)
+    cand = candidates(target, ts, sample_u, cand_override)
     internal = np.stack([_internal(par[b]) for b in range(B)])
     drf_max = np.full((B, N), np.nan)
     drf_arg = np.full((B, N), -1, np.int64)
@@ -329,7 +399,7 @@ def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float) ->
         for n in range(1, N):
             p = par[b, n]
             t = toks[b, n]
-            delta[b, n] = t == ts.arg[b, p]
+            delta[b, n] = t == cand[b, p]
             logp_tgt[b, n] = element(target[b, p, t:t + 1])[0] - ts.lse[b, p]
             logp_drf[b, n] = element(draft[b, p, t:t + 1])[0] - drf_lse[b, p]
     w1, b1, w2, b2 = _head_arrays(head)
@@ -350,10 +420,10 @@ def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float) ->
         passed = delta[b] | accept[b]
         best, depth, pth = tree_select(par[b], passed)
         accept_len[b] = depth[best] + 1
-        tokens[b], path[b] = _tree_emit(best, pth, toks[b], ts.arg[b], N)
+        tokens[b], path[b] = _tree_emit(best, pth, toks[b], cand[b], N)
         outcomes.append(tree_outcomes(par[b], delta[b], accept[b], ambiguous[b], toks[b],
-                                      ts.arg[b]))
-    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent,
+                                      cand[b]))
+    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent, tgt_cand=cand,
                 drf_max=drf_max, drf_arg=drf_arg, drf_lse=drf_lse, drf_ent=drf_ent,
                 internal=internal, delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z,
                 z_tilde=z_tilde, pi=pi, accept=accept, ambiguous=ambiguous,

@@ -108,3 +108,88 @@ void oracle_head(const void *hidden, int dtype, int64_t ld_h, const int64_t *row
         out_z[k] = z;
     }
 }
+
+/*
+ * Probabilities p[v] = exp(x[v] - lse) of one row, lse from oracle_row_stats.
+ * Returns 0, or -1 for a non-finite entry.
+ */
+static int oracle_softmax_row(const void *row, int dtype, int64_t V, double *p)
+{
+    double m, lse, h;
+    int64_t arg;
+    if (oracle_row_stats(row, dtype, V, 1, V, &m, &arg, &lse, &h))
+        return -1;
+    for (int64_t v = 0; v < V; ++v)
+        p[v] = exp(oracle_elem(row, dtype, v) - lse);
+    return 0;
+}
+
+/*
+ * Sampling at temperature 1 (Section 2, stochastic decoding; Appendix C.3: at
+ * T = 1 the target's verification candidate is a sample from its next-token
+ * distribution).  The sample is taken by inversion: given a uniform u in [0, 1)
+ * for row r, the candidate is the smallest v whose cumulative probability
+ * P(v) = p[0] + ... + p[v] (in index order, p = softmax(x)) exceeds u.  When
+ * rounding leaves P(V-1) <= u, the candidate is the last v with p[v] > 0.
+ * Writes the candidate and P(v-1), P(v) around it.  `work` holds V doubles.
+ * Returns 0, or -(r+1) when row r holds a non-finite entry.
+ */
+int64_t oracle_sample_rows(const void *rows, int dtype, int64_t ld, int64_t nrows, int64_t V,
+                           const double *u, double *work, int64_t *out_idx, double *out_lo,
+                           double *out_hi)
+{
+    size_t esz = dtype == ORACLE_F32 ? 4 : 2;
+    for (int64_t r = 0; r < nrows; ++r) {
+        const void *row = (const char *)rows + (size_t)r * (size_t)ld * esz;
+        if (oracle_softmax_row(row, dtype, V, work))
+            return -(r + 1);
+        double before = 0.0, at = 0.0;
+        int64_t pick = -1, last = 0;
+        for (int64_t v = 0; v < V; ++v) {
+            at = before + work[v];
+            if (work[v] > 0.0)
+                last = v;
+            if (at > u[r]) {
+                pick = v;
+                break;
+            }
+            before = at;
+        }
+        if (pick < 0) {            /* u at or above the rounded total */
+            pick = last;
+            before = 0.0;
+            for (int64_t v = 0; v < pick; ++v)
+                before += work[v];
+            at = before + work[pick];
+        }
+        out_idx[r] = pick;
+        out_lo[r] = before;
+        out_hi[r] = at;
+    }
+    return 0;
+}
+
+/*
+ * Cumulative probabilities P(idx[r]-1) and P(idx[r]) of row r (the interval of
+ * u values that inversion maps to idx[r]), for checking a candidate another
+ * implementation chose.  Returns 0, -(r+1) for a non-finite entry in row r, or
+ * -(nrows+1) for an index outside [0, V).
+ */
+int64_t oracle_cdf_at(const void *rows, int dtype, int64_t ld, int64_t nrows, int64_t V,
+                      const int64_t *idx, double *work, double *out_lo, double *out_hi)
+{
+    size_t esz = dtype == ORACLE_F32 ? 4 : 2;
+    for (int64_t r = 0; r < nrows; ++r) {
+        const void *row = (const char *)rows + (size_t)r * (size_t)ld * esz;
+        if (idx[r] < 0 || idx[r] >= V)
+            return -(nrows + 1);
+        if (oracle_softmax_row(row, dtype, V, work))
+            return -(r + 1);
+        double before = 0.0;
+        for (int64_t v = 0; v < idx[r]; ++v)
+            before += work[v];
+        out_lo[r] = before;
+        out_hi[r] = before + work[idx[r]];
+    }
+    return 0;
+}

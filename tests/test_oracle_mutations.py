@@ -28,7 +28,14 @@ MUTATIONS = [
     ("cospec_oracle.c", "double z = b2;", "double z = 0.0;"),                  # dropped b2
     ("__init__.py", "if not delta[i - 1] and not accept[i - 1]]", "if not delta[i - 1] and accept[i - 1]]"),
     ("__init__.py", "[int(target_argmax[s - 1])]", "[int(target_argmax[s])]"),   # wrong emitted row
-    ("__init__.py", "ytil = ts.arg[:, :K]", "ytil = ts.arg[:, 1:]"),            # verify against wrong row
+    ("__init__.py", "ytil = cand[:, :K]", "ytil = cand[:, 1:]"),                # verify against wrong row
+    ("__init__.py", "ytil = cand[:, :K]", "ytil = ts.arg[:, :K]"),              # T = 1 sample ignored
+    ("__init__.py", "tokens[b] = chain_tokens(s, toks[b], cand[b])",
+     "tokens[b] = chain_tokens(s, toks[b], ts.arg[b])"),                        # emits the argmax at T = 1
+    ("cospec_oracle.c", "p[v] = exp(oracle_elem(row, dtype, v) - lse);",
+     "p[v] = exp(oracle_elem(row, dtype, v));"),                                # unnormalised probabilities
+    ("cospec_oracle.c", "pick = v;\n", "pick = v + 1 < V ? v + 1 : v;\n"),     # one past the crossing
+    ("cospec_oracle.c", "at = before + work[v];", "at = work[v];"),              # not cumulative
     ("__init__.py", "logp_tgt = _gather(target[:, :K, :], toks)", "logp_tgt = _gather(target[:, 1:, :], toks)"),
     ("__init__.py", "if ok[n] and depth[n] > depth[best]:", "if ok[n] and depth[n] >= depth[best]:"),
     ("__init__.py", "accept = pi32 > lam32", "accept = pi32 >= lam32"),        # non-strict threshold

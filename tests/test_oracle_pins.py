@@ -149,6 +149,70 @@ def test_nonfinite_rejected():
         oracle.row_stats(x)
 
 
+# ---------------------------------------------------------------- temperature-1 sampling
+
+@pytest.mark.parametrize("V,c", [(1, 0.0), (7, 2.0), (1000, -5.5)])
+def test_sample_constant_row_closed_form(V, c):
+    # p = 1/V everywhere: inversion maps u to floor(u V), with P(k-1) = k/V, P(k) = (k+1)/V
+    k = np.arange(V)
+    u = (k + 0.5) / V
+    idx, lo, hi = oracle.sample_rows(np.full((V, V), c, np.float32), u)
+    np.testing.assert_array_equal(idx, k)
+    np.testing.assert_allclose(lo, k / V, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(hi, (k + 1) / V, rtol=0, atol=1e-13)
+
+
+def test_sample_grid_counts_match_softmax():
+    # inversion of the quasi-uniform grid u_k = (k + 1/2)/N hits index v exactly
+    # #{k : P(v-1) <= u_k < P(v)} times, which is within 1 of N p_v
+    rng = np.random.default_rng(41)
+    V, N = 40, 20000
+    x = (rng.normal(size=V) * 3).astype(np.float32)
+    p = scipy.special.softmax(x.astype(np.float64))
+    idx, _, _ = oracle.sample_rows(np.tile(x, (N, 1)), (np.arange(N) + 0.5) / N)
+    counts = np.bincount(idx, minlength=V)
+    assert np.abs(counts - N * p).max() <= 1.0 + 1e-9
+    assert (np.diff(idx) >= 0).all()                 # monotone in u
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sample_against_cumsum_searchsorted(dtype):
+    rng = np.random.default_rng(43)
+    rows, V = 64, 3001
+    x = torch.from_numpy((rng.normal(size=(rows, V)) * 4).astype(np.float32))
+    if dtype == "bf16":
+        arr = workloads.bf16_bits(x.to(torch.bfloat16))
+    else:
+        arr = x.numpy()
+    u = rng.random(rows).astype(np.float32).astype(np.float64)
+    idx, lo, hi = oracle.sample_rows(arr, u)
+    cdf = np.cumsum(scipy.special.softmax(oracle.element(arr), axis=-1), axis=-1)
+    want = np.array([np.searchsorted(cdf[r], u[r], side="right") for r in range(rows)])
+    np.testing.assert_array_equal(idx, want)
+    r = np.arange(rows)
+    np.testing.assert_allclose(hi, cdf[r, idx], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lo, np.where(idx > 0, cdf[r, np.maximum(idx - 1, 0)], 0.0), rtol=0,
+                               atol=1e-12)
+    assert ((lo <= u) & (u < hi)).all()
+    lo2, hi2 = oracle.cdf_at(arr, want)
+    np.testing.assert_allclose(lo2, lo, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(hi2, hi, rtol=0, atol=1e-12)
+
+
+def test_sample_peaked_and_edge_uniforms():
+    V = 1000
+    x = np.zeros((4, V), np.float32)
+    x[:, 321] = 60.0                                  # every other index carries < 1e-23 of the mass
+    idx, _, _ = oracle.sample_rows(x, [1e-9, 0.25, 0.5, 1 - 1e-9])
+    assert (idx == 321).all()
+    y = np.zeros((2, 5), np.float32)
+    idx, lo, _ = oracle.sample_rows(y, [0.0, np.nextafter(1.0, 0.0)])
+    assert idx[0] == 0 and lo[0] == 0.0
+    assert idx[1] == 4
+    with pytest.raises(IndexError):
+        oracle.cdf_at(y, [0, 5])
+
+
 # ---------------------------------------------------------------- head
 
 def test_head_identity_block_closed_form():
@@ -427,3 +491,50 @@ def test_tree_config_structure():
         assert par[b, 0] == -1 and all(0 <= par[b, n] < n for n in range(1, 60))
         _, depth, _ = oracle.tree_select(par[b], [1] * 60)
         assert max(depth) == 6
+
+
+def _sampled_spd(target64, draft_tokens, u):
+    """Exact-match speculative decoding whose target candidates are temperature-1
+    samples (inversion of u through numpy's cumulative softmax), position by position."""
+    K = len(draft_tokens)
+    cand = [int(np.searchsorted(np.cumsum(scipy.special.softmax(target64[i])), u[i], side="right"))
+            for i in range(K + 1)]
+    out = []
+    for i in range(K):
+        if cand[i] != int(draft_tokens[i]):
+            return len(out) + 1, out + [cand[i]], cand
+        out.append(int(draft_tokens[i]))
+    return K + 1, out + [cand[K]], cand
+
+
+def test_sampled_candidates_always_defer_is_sampled_spd():
+    wl = _small_chain(B=12, K=5, V=400, noise=0.5)
+    t, d, toks, hid, head = _np_chain(wl)
+    rng = np.random.default_rng(47)
+    u = rng.random((wl.B, wl.K + 1)).astype(np.float32).astype(np.float64)
+    r = oracle.verify_block(t, d, toks, hid, head, 1.0, sample_u=u)
+    t64 = oracle.element(t)
+    differs = 0
+    for b in range(wl.B):
+        s, out, cand = _sampled_spd(t64[b], toks[b], u[b])
+        assert list(r["tgt_cand"][b]) == cand
+        assert r["accept_len"][b] == s
+        assert list(r["tokens"][b][:s]) == out
+        differs += int(cand != list(np.argmax(t64[b], axis=-1)))
+    assert differs > 0                      # the samples are not the argmax everywhere
+
+
+def test_sampled_candidates_on_peaked_rows_equal_greedy():
+    wl = _small_chain(B=6, K=4, V=500, noise=0.8)
+    t, d, toks, hid, head = _np_chain(wl)
+    t = t.copy()
+    t64 = oracle.element(t)
+    am = np.argmax(t64, axis=-1)
+    # lift each row's argmax by 64: every other entry keeps less than 1e-25 of the mass
+    bits = workloads.bf16_bits(torch.from_numpy(t64 + 64.0 * (np.arange(t.shape[-1]) == am[..., None]))
+                               .to(torch.bfloat16))
+    u = np.random.default_rng(3).uniform(1e-6, 1 - 1e-6, size=(wl.B, wl.K + 1))
+    r1 = oracle.verify_block(bits, d, toks, hid, head, 0.5, sample_u=u)
+    r0 = oracle.verify_block(bits, d, toks, hid, head, 0.5)
+    np.testing.assert_array_equal(r1["tgt_cand"], r0["tgt_arg"])
+    np.testing.assert_array_equal(r1["tokens"], r0["tokens"])
