@@ -10,6 +10,8 @@ Prints one JSON line: rows/s (B*(K+1) verified rows per second), the roofline
 of the dominant kernel (the vocabulary reduction, timed with HIP events on the
 stream it runs on), and the CPU oracle timed on a bounded sample of the same
 workload on this host, with a parity re-check of the timed outputs.
+`--sample` times the temperature-1 variant (candidates sampled by inversion of
+seeded uniforms) instead of the greedy one.
 """
 from __future__ import annotations
 
@@ -51,6 +53,9 @@ def parse():
     ap.add_argument("--overlap", action="store_true",
                     help="run the head on a second stream, overlapping the draft-row reduction "
                          "(slower on the large chain batch: the reduction fills every CU)")
+    ap.add_argument("--sample", action="store_true",
+                    help="temperature-1 target candidates (inversion of seeded uniforms) instead "
+                         "of the greedy argmax")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     return ap.parse_args()
@@ -77,10 +82,15 @@ def main():
     head = workloads.Head(wl.head.w1.to(dev), None if wl.head.b1 is None else wl.head.b1.to(dev),
                           wl.head.w2.to(dev), wl.head.b2)
     tgt, drf, hid = wl.target.to(dev), wl.draft.to(dev), wl.hidden.to(dev)
+    u_host = None
+    if args.sample:
+        R = wl.N if tree else wl.K + 1
+        u_host = torch.rand((wl.B, R), generator=torch.Generator().manual_seed(2024))
+    u_dev = None if u_host is None else u_host.to(dev)
     if tree:
         par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
         p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
-                            overlap=args.overlap)
+                            overlap=args.overlap, sample_u=u_dev)
         rows = wl.B * wl.N
         internal = np.zeros((wl.B, wl.N), bool)
         pn = wl.parent.numpy()
@@ -91,7 +101,7 @@ def main():
     else:
         tok = wl.draft_tokens.to(dev)
         p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
-                             overlap=args.overlap)
+                             overlap=args.overlap, sample_u=u_dev)
         rows = wl.B * (wl.K + 1)
         reduced_rows = wl.B * (2 * wl.K + 1)
     elem = tgt.element_size()
@@ -159,15 +169,27 @@ def main():
         while done < wl.B and spent < args.cpu_seconds:
             seqs = list(range(done, min(wl.B, done + chunk)))
             sub = wl.take(seqs)
+            us = None if u_host is None else u_host[seqs].double().numpy()
             c0 = time.perf_counter()
             if tree:
                 ref = oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
-                                         sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam)
+                                         sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam,
+                                         sample_u=us)
             else:
                 ref = oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
-                                          conv(sub.hidden), head_np, lam)
+                                          conv(sub.hidden), head_np, lam, sample_u=us)
             spent += time.perf_counter() - c0
             gsub = {k: v[seqs] for k, v in out.items()}
+            if us is not None:
+                # candidates at a cumulative boundary may differ; the check validates
+                # them and the rest of the step is compared on the GPU's candidates
+                cand = parity.check_candidates(gsub["tgt_candidate"], conv(sub.target), us)
+                if not np.array_equal(cand, ref["tgt_cand"]):
+                    fn = oracle.verify_tree if tree else oracle.verify_block
+                    ref = (fn(conv(sub.target), conv(sub.draft), sub.parent.numpy(), sub.node_tokens.numpy(),
+                              conv(sub.hidden), head_np, lam, sample_u=us, cand_override=cand) if tree else
+                           fn(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(), conv(sub.hidden),
+                              head_np, lam, sample_u=us, cand_override=cand))
             (parity.check_tree if tree else parity.check_block)(gsub, ref)
             checked += len(seqs)
             done += len(seqs)
@@ -193,12 +215,14 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
                    "splits": args.splits or "auto", "head_overlap": args.overlap,
+                   "temperature": 1 if args.sample else 0,
                    "rows_per_step": rows,
                    "reduced_rows_per_step": reduced_rows},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
-                                 if args.config == 4 and not args.splits else None),
+                                 if args.config == 4 and not args.splits and not args.sample
+                                 else None),
                      "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
                      "event_interval_ms": k_raw, "empty_event_interval_ms": ev_overhead,
                      "launches_per_step": launches, "algorithmic_bytes_per_launch": launch_bytes},

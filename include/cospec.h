@@ -13,6 +13,11 @@
  * mismatch (Eq. cospec_length): it emits the draft tokens before that position
  * and the target token there, or all K draft tokens plus the bonus token.
  *
+ * At temperature 1 (Section 2, stochastic decoding; Appendix C.3) the target's
+ * verification candidate is a sample of softmax(target row) instead of its
+ * argmax; the same arbitration rule then applies to the pair.  The library takes
+ * that sample by inversion of a caller-supplied uniform (cospec_options).
+ *
  * This library computes that step on the GPU from logits, draft tokens,
  * arbitrator hidden states and head weights, and returns accept lengths and the
  * emitted tokens, plus optional per-row and per-decision features.
@@ -48,7 +53,7 @@
 extern "C" {
 #endif
 
-#define COSPEC_ABI_VERSION 2
+#define COSPEC_ABI_VERSION 3
 #define COSPEC_MAX_K 64      /* chain: draft tokens per block              */
 #define COSPEC_MAX_N 256     /* tree: nodes per tree, root included        */
 #define COSPEC_MAX_SPLITS 64 /* workgroups per logit row (tuning override) */
@@ -104,6 +109,8 @@ typedef struct {
     float *z_tilde;        /* per decision: head logit, +inf on matches        */
     float *policy;         /* per decision: sigma(z_tilde)                     */
     uint8_t *accept;       /* per decision: a_i (1 on matches)                 */
+    int32_t *tgt_candidate; /* per target row: the verification candidate used
+                              (the argmax, or the temperature-1 sample)        */
 } cospec_features;
 
 /*
@@ -130,6 +137,17 @@ typedef struct {
     hipStream_t aux_stream;   /* second stream for the head, or NULL (all on `stream`)  */
     hipEvent_t aux_ready;     /* required with aux_stream                               */
     hipEvent_t aux_done;      /* required with aux_stream                               */
+    /*
+     * Temperature-1 target candidates.  NULL: the candidate of every target row
+     * is its argmax (greedy decoding).  Otherwise a device array with one
+     * uniform per target row ([B][K+1] chain, [B][N] tree): the candidate of
+     * row r is the smallest v whose cumulative softmax probability
+     * p[0] + ... + p[v] exceeds sample_uniform[r] (inversion sampling).  Values
+     * below 0 or NaN act as 0, values at or above 1 as the largest float below
+     * 1.  Sums are fp32: a uniform within about 1e-5 of a cumulative boundary
+     * may select either neighbour.
+     */
+    const float *sample_uniform;
 } cospec_options;
 
 /* COSPEC_ABI_VERSION of the built library. */
@@ -180,12 +198,13 @@ size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const 
  * One tree verify step over B token trees of N nodes.  Trees are not in the
  * paper; this applies its chain rule along every root path:
  *  - node 0 is the root (the last verified token) and carries no decision;
- *  - child c of node p is verified against argmax(target row p), its
+ *  - child c of node p is verified against the candidate of target row p
+ *    (its argmax, or its temperature-1 sample), its
  *    log-probabilities come from rows p, and its head input is hidden row c;
  *  - a node is reachable when every decision on its root path passes (a match,
  *    or a mismatch whose draft token is accepted); the round accepts the
  *    deepest reachable node n* (ties to the lowest node id) and emits the node
- *    tokens along the path, then argmax(target row n*).
+ *    tokens along the path, then the candidate of target row n*.
  * On a path-shaped tree this is exactly the chain rule.
  *
  *  target_logits, draft_logits  [B][N] rows each (row n = distributions after
@@ -195,7 +214,8 @@ size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const 
  *  hidden         [B][N][d] (row 0 ignored).
  *  B >= 0, 1 <= N <= COSPEC_MAX_N, V >= 1.
  *  accept_len     [B] out: depth(n*) + 1.
- *  out_tokens     [B][N] out: path tokens then argmax(target row n*), then -1.
+ *  out_tokens     [B][N] out: path tokens then the candidate of target row
+ *                 n*, then -1.
  *  out_path       [B][N] out, nullable: node ids 0..n* along the path, then -1.
  *
  * A node whose parent index breaks 0 <= parent[n] < n, or whose token is

@@ -16,6 +16,9 @@ from __future__ import annotations
 import numpy as np
 
 CONTRACT_RTOL = 2e-3
+# fp32 cumulative sums over up to ~300 segment masses and 512 elements: a few ulp
+# each, so 5e-5 in probability covers the worst accumulation with margin
+CDF_TOL = 5e-5
 # (rtol, atol) per feature for the tighter check
 TIGHT = dict(max=(0.0, 0.0), lse=(1e-5, 1e-5), ent=(1e-5, 1e-4), logp=(1e-5, 1e-4),
              z=(1e-4, 1e-4), pi=(0.0, 2e-5))
@@ -101,10 +104,33 @@ def _outcomes(got_len, got_tok, got_path, ref, stats):
     stats["sequences_with_ambiguity"] = n_amb_seq
 
 
+def check_candidates(got, rows, u, stats: dict = None):
+    """Temperature-1 candidates chosen on the GPU against the oracle's inversion of
+    the same uniforms.  rows [..., V] (the logits the GPU read), u [...].  Returns
+    the GPU's candidates (each one checked) for the oracle's downstream steps."""
+    from . import sample_rows, cdf_at
+    got = _np(got).astype(np.int64)
+    u = np.asarray(u, dtype=np.float64)
+    ref, _, _ = sample_rows(rows, u)
+    diff = got != ref
+    if diff.any():
+        lo, hi = cdf_at(rows[diff], got[diff])
+        ud = u[diff]
+        ok = (lo - CDF_TOL <= ud) & (ud < hi + CDF_TOL)
+        if not ok.all():
+            i = int(np.flatnonzero(~ok)[0])
+            raise ParityError(f"temperature-1 candidate {got[diff][i]} (oracle {ref[diff][i]}) does not "
+                              f"invert u={ud[i]!r}: its interval is [{lo[i]!r}, {hi[i]!r})")
+    if stats is not None:
+        stats["candidates_at_boundary"] = int(diff.sum())
+    return got
+
+
 def check_block(gpu: dict, ref: dict) -> dict:
     """GPU result of cospec_verify_block (features included) against oracle.verify_block."""
     stats = {}
     _exact("tgt_argmax", gpu["tgt_argmax"], ref["tgt_arg"])
+    _exact("tgt_candidate", gpu["tgt_candidate"], ref["tgt_cand"])
     _exact("drf_argmax", gpu["drf_argmax"], ref["drf_arg"])
     _close("tgt_max", gpu["tgt_max"], ref["tgt_max"], "max", stats)
     _close("drf_max", gpu["drf_max"], ref["drf_max"], "max", stats)
@@ -122,6 +148,7 @@ def check_tree(gpu: dict, ref: dict) -> dict:
     """GPU result of cospec_verify_tree (features included) against oracle.verify_tree."""
     stats = {}
     _exact("tgt_argmax", gpu["tgt_argmax"], ref["tgt_arg"])
+    _exact("tgt_candidate", gpu["tgt_candidate"], ref["tgt_cand"])
     _close("tgt_max", gpu["tgt_max"], ref["tgt_max"], "max", stats)
     _close("tgt_lse", gpu["tgt_lse"], ref["tgt_lse"], "lse", stats)
     _close("tgt_entropy", gpu["tgt_entropy"], ref["tgt_ent"], "ent", stats)

@@ -35,7 +35,7 @@ class _Head(ctypes.Structure):
 
 _FEATURE_FIELDS = ["tgt_argmax", "tgt_max", "tgt_lse", "tgt_entropy", "drf_argmax", "drf_max",
                    "drf_lse", "drf_entropy", "logp_tgt", "logp_drf", "delta", "z_tilde", "policy",
-                   "accept"]
+                   "accept", "tgt_candidate"]
 
 
 class _Features(ctypes.Structure):
@@ -46,7 +46,8 @@ class _Options(ctypes.Structure):
     _fields_ = [("reduce_begin", ctypes.c_void_p), ("reduce_end", ctypes.c_void_p),
                 ("reduce2_begin", ctypes.c_void_p), ("reduce2_end", ctypes.c_void_p),
                 ("splits", ctypes.c_int32), ("aux_stream", ctypes.c_void_p),
-                ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p)]
+                ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p),
+                ("sample_uniform", ctypes.c_void_p)]
 
 
 def _event_handle(ev) -> int:
@@ -138,7 +139,7 @@ class Prepared:
     `launch()` enqueues the step with no allocation."""
 
     def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, splits,
-                 overlap):
+                 overlap, uniform=None):
         self._fn = fn
         self._args = args_before_feats
         self.outputs = outputs
@@ -146,6 +147,7 @@ class Prepared:
         self._feats = feats_struct
         self.workspace = workspace
         self.splits = int(splits)
+        self.uniform = uniform
         self.aux = None
         if overlap:
             dev = workspace.device
@@ -153,12 +155,12 @@ class Prepared:
         self._keep = []
 
     def _options(self, timing):
-        if timing is None and not self.splits and self.aux is None:
+        if timing is None and not self.splits and self.aux is None and self.uniform is None:
             return None
         ev = [None] * 4 if timing is None else [None if e is None else _event_handle(e) for e in timing]
         aux = (None, None, None) if self.aux is None else (
             self.aux[0].cuda_stream, _event_handle(self.aux[1]), _event_handle(self.aux[2]))
-        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux)
+        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux, _ptr(self.uniform))
 
     def launch(self, timing=None):
         """Enqueue the step on torch's current stream.  `timing` = four torch events
@@ -183,14 +185,25 @@ def _features(alloc: bool, dev, B, RT, RD, D):
                   tgt_entropy=((B, RT), f32), drf_argmax=((B, RD), i32), drf_max=((B, RD), f32),
                   drf_lse=((B, RD), f32), drf_entropy=((B, RD), f32), logp_tgt=((B, D), f32),
                   logp_drf=((B, D), f32), delta=((B, D), u8), z_tilde=((B, D), f32),
-                  policy=((B, D), f32), accept=((B, D), u8))
+                  policy=((B, D), f32), accept=((B, D), u8), tgt_candidate=((B, RT), i32))
     feats = {k: torch.empty(s, dtype=t, device=dev) for k, (s, t) in shapes.items()}
     st = _Features(*[_ptr(feats[f]) for f in _FEATURE_FIELDS])
     return feats, st
 
 
+def _uniforms(u: Optional[torch.Tensor], B: int, RT: int):
+    if u is None:
+        return None
+    if tuple(u.shape) != (B, RT) or u.dtype != torch.float32 or not u.is_contiguous() or not u.is_cuda:
+        raise ValueError("sample_u must be a contiguous float32 device tensor [B, target rows]")
+    return u
+
+
 def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                  splits: int = 0, overlap: bool = False) -> Prepared:
+                  splits: int = 0, overlap: bool = False,
+                  sample_u: Optional[torch.Tensor] = None) -> Prepared:
+    """sample_u: one uniform per target row [B, K+1] for temperature-1 candidates
+    (cospec_options.sample_uniform); None for the greedy argmax."""
     B, R, V = target.shape
     K = R - 1
     ld = _row_stride(target)
@@ -214,13 +227,16 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
             _ptr(draft_tokens) if K > 0 else None, _ptr(hidden) if K > 0 else None,
             ctypes.byref(hs), float(lam), B, K, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]))
-    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits, overlap)
+    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits, overlap,
+                 _uniforms(sample_u, B, K + 1))
     p._keep = [hs, target, draft, draft_tokens, hidden, head]
     return p
 
 
 def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                 features: bool = True, splits: int = 0, overlap: bool = False) -> Prepared:
+                 features: bool = True, splits: int = 0, overlap: bool = False,
+                 sample_u: Optional[torch.Tensor] = None) -> Prepared:
+    """sample_u: one uniform per target row [B, N] for temperature-1 candidates."""
     B, N, V = target.shape
     ld = _row_stride(target)
     if _row_stride(draft) != ld or tuple(draft.shape) != (B, N, V):
@@ -244,24 +260,28 @@ def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
     args = (_ptr(target), _ptr(draft), _dtype_code(target), ld, _ptr(parent), _ptr(node_tokens),
             _ptr(hidden), ctypes.byref(hs), float(lam), B, N, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]), _ptr(outputs["path"]))
-    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits, overlap)
+    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits, overlap,
+                 _uniforms(sample_u, B, N))
     p._keep = [hs, target, draft, parent, node_tokens, hidden, head]
     return p
 
 
 def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                 splits: int = 0, overlap: bool = False) -> dict:
+                 splits: int = 0, overlap: bool = False,
+                 sample_u: Optional[torch.Tensor] = None) -> dict:
     """cospec_verify_block on device tensors; returns accept_len, tokens (+ features)."""
-    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits, overlap)
+    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits, overlap,
+                      sample_u)
     p.launch()
     return p.result()
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                features: bool = True, splits: int = 0, overlap: bool = False) -> dict:
+                features: bool = True, splits: int = 0, overlap: bool = False,
+                sample_u: Optional[torch.Tensor] = None) -> dict:
     """cospec_verify_tree on device tensors; returns accept_len, tokens, path (+ features)."""
     p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits,
-                     overlap)
+                     overlap, sample_u)
     p.launch()
     return p.result()
 

@@ -6,6 +6,9 @@
 //                       head overlaps step 4 on the aux stream), split over
 //                       `splits` workgroups per row -> partial (max, argmax, S, T);
 //                       zeroes the list counter
+//   1b. k_sample        temperature 1 only: one wave per target row samples the
+//                       candidate by inversion of its uniform (segment masses
+//                       written by step 1, then one segment re-read)
 //   2. k_decide         one workgroup per sequence: target statistics, Delta,
 //                       log p_T, mismatch compaction (device-side count M)
 //   3. k_head_gemm + k_head_epilogue   MFMA head over the M compacted rows
@@ -62,15 +65,30 @@ inline size_t head_bytes(int64_t m_cap, const cospec_head *hd) {
 
 // Workspace carving shared by the size query and the call.
 struct Layout {
-    size_t partials, tgt_arg, state, listpos, list, count, upart, z, total;
+    size_t partials, seg, tgt_arg, state, listpos, list, count, upart, z, total;
     int64_t partial_slots;
 };
 
-Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head *hd) {
+// Probability-mass segments of one logit row for temperature-1 sampling: one per
+// kSegVecs 16-byte vectors, plus one for the elements past the last whole vector.
+inline int64_t n_segments(int32_t V, int eb) {
+    const int64_t nvec = static_cast<int64_t>(V) * eb / 16;
+    const int64_t tail = V - nvec * (16 / eb);
+    return (nvec + kSegVecs - 1) / kSegVecs + (tail > 0 ? 1 : 0);
+}
+
+// The size queries do not know the logit dtype: reserve for the larger count.
+inline int64_t n_segments_any(int32_t V) {
+    const int64_t a = n_segments(V, 2), b = n_segments(V, 4);
+    return a > b ? a : b;
+}
+
+Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head *hd, int32_t V) {
     Layout L{};
     L.partial_slots = rows > kMinPartialSlots ? rows : kMinPartialSlots;
     size_t off = 0;
     L.partials = off; off += round_up(static_cast<size_t>(L.partial_slots) * 16);
+    L.seg = off;      off += round_up(static_cast<size_t>(B * RT) * static_cast<size_t>(n_segments_any(V)) * 8);
     L.tgt_arg = off;  off += round_up(static_cast<size_t>(B * RT) * 4);
     L.state = off;    off += round_up(static_cast<size_t>(B * D));
     L.listpos = off;  off += round_up(static_cast<size_t>(B * D) * 4);
@@ -96,7 +114,8 @@ int32_t auto_splits(int64_t rows, int64_t nvec) {
 bool feats_aligned(const cospec_features *f) {
     if (!f) return true;
     const void *p4[] = {f->tgt_argmax, f->tgt_max, f->tgt_lse, f->tgt_entropy, f->drf_argmax, f->drf_max,
-                        f->drf_lse, f->drf_entropy, f->logp_tgt, f->logp_drf, f->z_tilde, f->policy};
+                        f->drf_lse, f->drf_entropy, f->logp_tgt, f->logp_drf, f->z_tilde, f->policy,
+                        f->tgt_candidate};
     for (const void *p : p4)
         if (p && !aligned(p, 4)) return false;
     return true;
@@ -129,12 +148,15 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
         if (c.opts->splits < 0 || c.opts->splits > COSPEC_MAX_SPLITS) return COSPEC_ERR_UNSUPPORTED;
         splits = c.opts->splits;
     }
-    const Layout L = layout(rows, c.B, c.RT, c.D, c.head);
+    const Layout L = layout(rows, c.B, c.RT, c.D, c.head, c.V);
+    const float *uniform = c.opts ? c.opts->sample_uniform : nullptr;
+    if (uniform && !aligned(uniform, 4)) return COSPEC_ERR_INVALID_ARG;
     if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
     if (!c.ws || !aligned(c.ws, kAlign) || c.ws_bytes < L.total) return COSPEC_ERR_WORKSPACE;
 
     char *ws = static_cast<char *>(c.ws);
     float4 *partials = reinterpret_cast<float4 *>(ws + L.partials);
+    float2 *seg = reinterpret_cast<float2 *>(ws + L.seg);
     int32_t *tgt_arg = reinterpret_cast<int32_t *>(ws + L.tgt_arg);
     uint8_t *state = reinterpret_cast<uint8_t *>(ws + L.state);
     int32_t *listpos = reinterpret_cast<int32_t *>(ws + L.listpos);
@@ -162,8 +184,12 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     ra.parent = c.is_tree ? c.parent : nullptr;
     ra.N = static_cast<int32_t>(c.RT);
     ra.splits = splits;
-    ra.vec_per_split = static_cast<int32_t>((nvec + splits - 1) / splits);
+    int64_t vps = (nvec + splits - 1) / splits;
+    if (uniform) vps = (vps + kSegVecs - 1) / kSegVecs * kSegVecs;   // segments never straddle splits
+    ra.vec_per_split = static_cast<int32_t>(vps);
     ra.partials = partials;
+    ra.seg = uniform ? seg : nullptr;
+    ra.nseg = static_cast<int32_t>(n_segments(c.V, eb));
 
     const Dtype dt = static_cast<Dtype>(c.dt);
     auto record = [&](hipEvent_t ev, hipStream_t s) { return !ev || hipEventRecord(ev, s) == hipSuccess; };
@@ -179,6 +205,22 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     if (launch_reduce(dt, rt, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (!record(c.opts ? c.opts->reduce_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
 
+    // 1b. temperature-1 candidates
+    if (uniform) {
+        SampleArgs sa{};
+        sa.tgt = ra.tgt;
+        sa.ld_bytes = ra.ld_bytes;
+        sa.V = c.V;
+        sa.n_rows = ra.n_tgt_rows;
+        sa.partials = partials;
+        sa.splits = splits;
+        sa.seg = seg;
+        sa.nseg = ra.nseg;
+        sa.uniform = uniform;
+        sa.cand = tgt_arg;
+        if (launch_sample(dt, sa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+    }
+
     // 2. decide
     DecideArgs da{};
     da.tgt = ra.tgt;
@@ -193,7 +235,9 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     da.partials = partials;
     da.splits = splits;
     da.score_mismatch = head;
+    da.sampled = uniform != nullptr;
     da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
+    da.tgt_cand = F.tgt_candidate;
     da.logp_tgt = F.logp_tgt; da.delta = F.delta;
     da.ws_tgt_arg = tgt_arg;
     da.ws_state = state;
@@ -292,12 +336,12 @@ const char *cospec_status_string(int32_t status) {
 
 size_t cospec_verify_block_workspace_size(int32_t B, int32_t K, int32_t V, const cospec_head *head) {
     if (B < 0 || K < 0 || K > COSPEC_MAX_K || V < 1 || check_head(head) != COSPEC_OK) return 0;
-    return layout(static_cast<int64_t>(B) * (2 * K + 1), B, K + 1, K, head).total;
+    return layout(static_cast<int64_t>(B) * (2 * K + 1), B, K + 1, K, head, V).total;
 }
 
 size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const cospec_head *head) {
     if (B < 0 || N < 1 || N > COSPEC_MAX_N || V < 1 || check_head(head) != COSPEC_OK) return 0;
-    return layout(static_cast<int64_t>(B) * 2 * N, B, N, N, head).total;
+    return layout(static_cast<int64_t>(B) * 2 * N, B, N, N, head, V).total;
 }
 
 cospec_status cospec_verify_block(const void *target_logits, const void *draft_logits,

@@ -15,6 +15,7 @@ constexpr int kHeadTargetBlocks = 512; // k-splits are added until the grid reac
 constexpr int kHeadMaxSplit = 8;
 constexpr int kXcds = 8;             // MI355X: 8 XCDs, each with its own L2
 constexpr int kMaxSeqRows = 256;      // rows per sequence / nodes per tree held in LDS
+constexpr int kSegVecs = 64;          // 16-byte vectors per probability-mass segment (one wave load)
 
 enum Dtype : int32_t { kF32 = 0, kBF16 = 1 };
 
@@ -35,6 +36,24 @@ struct ReduceArgs {
     int32_t vec_per_split;     // 16-byte vectors per split
     float4 *partials;          // [rows][splits] {max, argmax bits, S, T}
     int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter), or null
+    float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
+                               // target row, or null; needs vec_per_split % kSegVecs == 0
+    int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
+};
+
+// Temperature-1 candidates: one wave per target row inverts its uniform through
+// the segment masses, then through the elements of the segment it lands in.
+struct SampleArgs {
+    const char *tgt;
+    int64_t ld_bytes;
+    int32_t V;
+    int32_t n_rows;            // target rows
+    const float4 *partials;
+    int32_t splits;
+    const float2 *seg;
+    int32_t nseg;
+    const float *uniform;      // [n_rows]
+    int32_t *cand;             // [n_rows] out
 };
 
 struct DecideArgs {
@@ -50,9 +69,10 @@ struct DecideArgs {
     const float4 *partials;
     int32_t splits;
     int32_t score_mismatch;    // compact mismatches for the head
-    int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent;
+    int32_t sampled;           // ws_tgt_arg already holds the candidates (k_sample)
+    int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent; int32_t *tgt_cand;
     float *logp_tgt; uint8_t *delta;
-    int32_t *ws_tgt_arg;       // [B*RT]
+    int32_t *ws_tgt_arg;       // [B*RT] verification candidate per target row
     uint8_t *ws_state;         // [B*D]
     int32_t *ws_listpos;       // [B*D] position in the compacted list or -1
     int32_t *ws_list;          // [B*D] compacted hidden-row ids
@@ -107,6 +127,7 @@ struct ArbFinishArgs {
 };
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_sample(Dtype dt, const SampleArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue

@@ -15,8 +15,9 @@
 // head overlaps them on a second stream).
 //
 // k_decide merges the partials of one sequence's target rows in fixed split
-// order, takes the target's greedy verification tokens (argmax, ties to the
-// lowest index), sets Delta = 1[draft token == verification token]
+// order, takes the target's verification candidates (the greedy argmax, ties to
+// the lowest index, or the temperature-1 samples of k_sample), sets
+// Delta = 1[draft token == candidate]
 // (Section 3.1), gathers the draft token's target logit for log p_T
 // (Section 3.4), and compacts the mismatch decisions into one list for the
 // head with a wave ballot and a prefix over the workgroup's waves.
@@ -74,7 +75,145 @@ __device__ inline void consume(const float *x, int chunk, Lane &st) {
     }
 }
 
+// Eight per-lane values m[0..7] -> lane L returns the wave's sum of m[L >> 3].
+// Each exchange halves the values a lane carries (xor 32, 16, 8), then the eight
+// lanes that share bits 3..5 add up (xor 4, 2, 1): 10 shuffles instead of 48.
+__device__ inline float transpose_sum8(const float (&m)[8], int lane) {
+    const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+    float r4[4], r2[2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float send = b5 ? m[j] : m[j + 4];
+        r4[j] = (b5 ? m[j + 4] : m[j]) + __shfl_xor(send, 32);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const float send = b4 ? r4[j] : r4[j + 2];
+        r2[j] = (b4 ? r4[j + 2] : r4[j]) + __shfl_xor(send, 16);
+    }
+    const float send = b3 ? r2[0] : r2[1];
+    float r = (b3 ? r2[1] : r2[0]) + __shfl_xor(send, 8);
+    r += __shfl_xor(r, 4);
+    r += __shfl_xor(r, 2);
+    r += __shfl_xor(r, 1);
+    return r;
+}
+
+// Plain streaming of vectors [v0, v1) of a row: lane `tid` takes v0 + tid, then
+// every kReduceThreads-th vector.
 template <int DT>
+__device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, Lane &st) {
+    using E = Elt<DT>;
+    constexpr int NV = E::kPerVec;
+    int v = v0 + tid;
+    for (; v + (kUnroll - 1) * kReduceThreads < v1; v += kUnroll * kReduceThreads) {
+        u32x4 q[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            float x[NV];
+            E::unpack(q[u], x);
+            consume<NV>(x, v + u * kReduceThreads, st);
+        }
+    }
+    for (; v < v1; v += kReduceThreads) {
+        float x[NV];
+        E::unpack(__builtin_nontemporal_load(rv + v), x);
+        consume<NV>(x, v, st);
+    }
+}
+
+// Wave-wide rescale to the reference of the wave's largest chunk max; returns the
+// factor applied to S.
+__device__ inline float rescale_wave(Lane &st, float cm) {
+    const float nr = __fmul_rn(wave_max(cm), kLog2e);
+    const float dr = st.ref - nr;
+    const float f = __builtin_amdgcn_exp2f(dr);
+    st.T = f * fmaf(dr, st.S, st.T);
+    st.S = f * st.S;
+    st.ref = nr;
+    st.thresh = (nr + kRescaleMargin) * kLn2;
+    return f;
+}
+
+// The same streaming, for rows that are sampled at temperature 1: it also writes
+// the probability mass of every segment of kSegVecs vectors (one wave load, so the
+// segments of a row are contiguous and in vocabulary order) as {sum 2^(x*log2e -
+// ref), ref}.  Every lane of a wave shares one reference, raised for the whole
+// wave when any lane needs it, so a segment's mass is one wave sum.  Requires v0 to
+// be a multiple of kSegVecs.
+template <int DT>
+__device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid, Lane &st, float2 *seg) {
+    using E = Elt<DT>;
+    constexpr int NV = E::kPerVec;
+    static_assert(kUnroll == 8 && kReduceThreads % kSegVecs == 0, "segment sums assume 8 loads per lane");
+    const int lane = tid & 63;
+    int w = v0 + (tid & ~63);                      // this wave's first vector
+    for (; w + (kUnroll - 1) * kReduceThreads + 63 < v1; w += kUnroll * kReduceThreads) {
+        u32x4 q[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+        float m[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            float x[NV];
+            E::unpack(q[u], x);
+            float cm = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
+            if (cm > st.best) { st.best = cm; st.chunk = w + u * kReduceThreads + lane; }
+            if (__builtin_expect(__ballot(cm > st.thresh) != 0, 0)) {
+                const float f = rescale_wave(st, cm);
+#pragma unroll
+                for (int j = 0; j < u; ++j) m[j] *= f;
+            }
+            const float nref = -st.ref;
+            float mu = 0.f;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                const float t = fmaf(x[k], kLog2e, nref);
+                const float e = __builtin_amdgcn_exp2f(t);
+                mu += e;
+                st.T = fmaf(e, t, st.T);
+            }
+            m[u] = mu;
+            st.S += mu;
+        }
+        const float tot = transpose_sum8(m, lane);
+        if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, st.ref);
+    }
+    for (; w < v1; w += kReduceThreads) {
+        const bool ok = w + lane < v1;
+        float x[NV];
+        if (ok) {
+            E::unpack(__builtin_nontemporal_load(rv + w + lane), x);
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) x[k] = -INFINITY;
+        }
+        float cm = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
+        if (cm > st.best) { st.best = cm; st.chunk = w + lane; }
+        if (__ballot(cm > st.thresh) != 0) rescale_wave(st, cm);
+        const float nref = -st.ref;
+        float mu = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            // lanes past the end add exp2(-huge) = 0 and 0 * (finite t) = 0
+            const float t = fmaf(ok ? x[k] : kFarBelow, kLog2e, nref);
+            const float e = __builtin_amdgcn_exp2f(t);
+            mu += e;
+            st.T = fmaf(e, t, st.T);
+        }
+        st.S += mu;
+        const float tot = wave_sum(mu);
+        if (lane == 0) seg[w / kSegVecs] = make_float2(tot, st.ref);
+    }
+}
+
+template <int DT, bool SEG>
 __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
@@ -104,36 +243,27 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     const u32x4 *rv = reinterpret_cast<const u32x4 *>(rp);
 
     Lane st{-INFINITY, -1, kFarBelow, -INFINITY, 0.f, 0.f};   // the first chunk always rescales
-    int v = v0 + tid;
-    for (; v + (kUnroll - 1) * kReduceThreads < v1; v += kUnroll * kReduceThreads) {
-        u32x4 q[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            float x[NV];
-            E::unpack(q[u], x);
-            consume<NV>(x, v + u * kReduceThreads, st);
-        }
-    }
-    for (; v < v1; v += kReduceThreads) {
-        float x[NV];
-        E::unpack(__builtin_nontemporal_load(rv + v), x);
-        consume<NV>(x, v, st);
-    }
-    // elements past the last whole vector: the last split's first lane
+    float2 *seg = nullptr;
+    if (SEG && row < a.n_tgt_rows) seg = a.seg + static_cast<int64_t>(row) * a.nseg;
+    if (SEG && seg) stream_segmented<DT>(rv, v0, v1, tid, st, seg);
+    else stream_plain<DT>(rv, v0, v1, tid, st);
+    // elements past the last whole vector: the last split's first lane (their own
+    // segment, the row's last, when segments are written)
     if (tail > 0 && split == a.splits - 1 && tid == 0) {
         const int64_t e0 = static_cast<int64_t>(nvec) * NV;
         float cm = -INFINITY;
         for (int k = 0; k < tail; ++k) cm = fmaxf(cm, E::at(rp, e0 + k));
         if (cm > st.best) { st.best = cm; st.chunk = nvec; }
         if (cm > st.thresh) rescale(st, __fmul_rn(cm, kLog2e));
+        float mu = 0.f;
         for (int k = 0; k < tail; ++k) {
             const float t = fmaf(E::at(rp, e0 + k), kLog2e, -st.ref);
             const float e = __builtin_amdgcn_exp2f(t);
-            st.S += e;
+            mu += e;
             st.T = fmaf(e, t, st.T);
         }
+        st.S += mu;
+        if (SEG && seg) seg[a.nseg - 1] = make_float2(mu, st.ref);
     }
 
     __shared__ float s_best[kReduceThreads / 64];
@@ -235,10 +365,14 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     for (int j = t; j < a.RT; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RT + j;
         const RowStat rs = merge_row(a.partials + r * a.splits, a.splits);
+        // the verification candidate: the argmax, or the temperature-1 sample
+        // k_sample left in ws_tgt_arg
+        const int cand = a.sampled ? a.ws_tgt_arg[r] : rs.arg;
         s_tmax[j] = rs.max;
         s_tlogs[j] = rs.log_s;
-        s_targ[j] = rs.arg;
-        a.ws_tgt_arg[r] = rs.arg;
+        s_targ[j] = cand;
+        if (!a.sampled) a.ws_tgt_arg[r] = cand;
+        if (a.tgt_cand) a.tgt_cand[r] = cand;
         if (a.tgt_argmax) a.tgt_argmax[r] = rs.arg;
         if (a.tgt_max) a.tgt_max[r] = rs.max;
         if (a.tgt_lse) a.tgt_lse[r] = rs.lse;
@@ -284,8 +418,14 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(a.n_rows) * a.splits));
     if (grid.x == 0) return hipSuccess;
-    if (dt == kBF16) hipLaunchKernelGGL(k_vocab_reduce<kBF16>, grid, dim3(kReduceThreads), 0, s, a);
-    else hipLaunchKernelGGL(k_vocab_reduce<kF32>, grid, dim3(kReduceThreads), 0, s, a);
+    const bool seg = a.seg && a.row_offset < a.n_tgt_rows;
+    if (dt == kBF16) {
+        if (seg) hipLaunchKernelGGL((k_vocab_reduce<kBF16, true>), grid, dim3(kReduceThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_vocab_reduce<kBF16, false>), grid, dim3(kReduceThreads), 0, s, a);
+    } else {
+        if (seg) hipLaunchKernelGGL((k_vocab_reduce<kF32, true>), grid, dim3(kReduceThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_vocab_reduce<kF32, false>), grid, dim3(kReduceThreads), 0, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -1,5 +1,6 @@
-// Device helpers shared by the reduction, decide and finish kernels: element
-// access for bf16/fp32 rows and the fixed-order merge of a row's split partials.
+// Device helpers shared by the reduction, sampling, decide and finish kernels:
+// element access for bf16/fp32 rows, wave reductions and the fixed-order merge of
+// a row's split partials.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -40,6 +41,18 @@ template <> struct Elt<kF32> {
         return reinterpret_cast<const float *>(row)[i];
     }
 };
+
+__device__ inline float wave_max(float x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+    return x;
+}
+
+__device__ inline float wave_sum(float x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+    return x;
+}
 
 struct RowStat {
     float max, lse, ent;

@@ -122,6 +122,13 @@ def test_verify_block_aux_stream_needs_its_events():
     assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE, aux_done=FAKE))) == INVALID
 
 
+def test_verify_block_sample_uniform_alignment():
+    L = cs.lib()
+    assert _block(L, opts=ctypes.byref(binding._Options(sample_uniform=FAKE + 2))) == INVALID
+    f = binding._Features(tgt_candidate=FAKE + 1)
+    assert _block(L, feats=ctypes.byref(f)) == INVALID
+
+
 def _tree(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
              lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30)

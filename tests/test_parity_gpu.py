@@ -45,30 +45,33 @@ def _padded(t, pad):
     return big[:, :, :V]
 
 
-def _gpu_block(wl, lam, splits=0, pad=0, features=True, overlap=False):
+def _gpu_block(wl, lam, splits=0, pad=0, features=True, overlap=False, u=None):
     out = cs.verify_block(_padded(wl.target, pad), _padded(wl.draft, pad), wl.draft_tokens.to(DEV),
                           wl.hidden.to(DEV), _head_dev(wl.head), lam, features=features,
-                          splits=splits, overlap=overlap)
+                          splits=splits, overlap=overlap,
+                          sample_u=None if u is None else u.to(DEV))
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
 
 
-def _ref_block(wl, lam):
+def _ref_block(wl, lam, u=None, cand=None):
     return oracle.verify_block(_conv(wl.target), _conv(wl.draft), wl.draft_tokens.numpy(),
-                               _conv(wl.hidden), _head_np(wl.head), lam)
+                               _conv(wl.hidden), _head_np(wl.head), lam,
+                               sample_u=None if u is None else u.double().numpy(), cand_override=cand)
 
 
-def _gpu_tree(tr, lam, splits=0, pad=0, overlap=False):
+def _gpu_tree(tr, lam, splits=0, pad=0, overlap=False, u=None):
     out = cs.verify_tree(_padded(tr.target, pad), _padded(tr.draft, pad), tr.parent.to(DEV),
                          tr.node_tokens.to(DEV), tr.hidden.to(DEV), _head_dev(tr.head), lam,
-                         splits=splits, overlap=overlap)
+                         splits=splits, overlap=overlap, sample_u=None if u is None else u.to(DEV))
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
 
 
-def _ref_tree(tr, lam):
+def _ref_tree(tr, lam, u=None, cand=None):
     return oracle.verify_tree(_conv(tr.target), _conv(tr.draft), tr.parent.numpy(),
-                              tr.node_tokens.numpy(), _conv(tr.hidden), _head_np(tr.head), lam)
+                              tr.node_tokens.numpy(), _conv(tr.hidden), _head_np(tr.head), lam,
+                              sample_u=None if u is None else u.double().numpy(), cand_override=cand)
 
 
 def _report(name, stats, gpu):
@@ -370,3 +373,132 @@ def test_arbitrate_matches_oracle():
         a = out["accept"].cpu().numpy().astype(bool)[valid.numpy()]
         firm = ~ref["ambiguous"]
         assert np.array_equal(a[firm], ref["accept"][firm])
+
+
+# ------------------------------------------------------------------ temperature 1
+
+def _uniforms(shape, seed):
+    return torch.rand(shape, generator=torch.Generator().manual_seed(seed), dtype=torch.float32)
+
+
+def _t1_block(wl, lam, seed, **kw):
+    """GPU chain step with temperature-1 candidates against the oracle: the candidates
+    are checked against inversion of the same uniforms, then the oracle runs the rest
+    of the step on them."""
+    u = _uniforms((wl.B, wl.K + 1), seed)
+    gpu = _gpu_block(wl, lam, u=u, **kw)
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(wl.target), u.double().numpy(), stats)
+    stats.update(parity.check_block(gpu, _ref_block(wl, lam, u, cand)))
+    return gpu, stats
+
+
+def _t1_tree(tr, lam, seed, **kw):
+    u = _uniforms((tr.B, tr.N), seed)
+    gpu = _gpu_tree(tr, lam, u=u, **kw)
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(tr.target), u.double().numpy(), stats)
+    stats.update(parity.check_tree(gpu, _ref_tree(tr, lam, u, cand)))
+    return gpu, stats
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_t1_configs_full(cfg):
+    wl = workloads.make_config(cfg)
+    gpu, stats = _t1_block(wl, wl.lambdas[0], 100 + cfg)
+    _report(f"T=1 config {cfg}", stats, gpu)
+    assert (gpu["tgt_candidate"] != gpu["tgt_argmax"]).any()
+
+
+def test_t1_config4_full_size_sampled():
+    wl = workloads.make_config(4)
+    u = _uniforms((wl.B, wl.K + 1), 104)
+    gpu = _gpu_block(wl, wl.lambdas[0], u=u)
+    seqs = _sample(wl.B, 16, 41)
+    sub = {k: v[seqs] for k, v in gpu.items()}
+    ws = wl.take(seqs)
+    stats = {}
+    cand = parity.check_candidates(sub["tgt_candidate"], _conv(ws.target), u[seqs].double().numpy(), stats)
+    stats.update(parity.check_block(sub, _ref_block(ws, wl.lambdas[0], u[seqs], cand)))
+    _report("T=1 config 4 (16 sampled sequences of 256)", stats, sub)
+
+
+def test_t1_config5_full_size_sampled():
+    tr = workloads.make_config(5)
+    u = _uniforms((tr.B, tr.N), 105)
+    gpu = _gpu_tree(tr, tr.lambdas[0], u=u)
+    seqs = _sample(tr.B, 6, 51)
+    sub = {k: v[seqs] for k, v in gpu.items()}
+    ts = tr.take(seqs)
+    stats = {}
+    cand = parity.check_candidates(sub["tgt_candidate"], _conv(ts.target), u[seqs].double().numpy(), stats)
+    stats.update(parity.check_tree(sub, _ref_tree(ts, tr.lambdas[0], u[seqs], cand)))
+    _report("T=1 config 5 (6 sampled trees of 64)", stats, sub)
+
+
+T1_FUZZ = [
+    # (B, K, V, dtype, pad, splits): tails, rows shorter than one vector, split rounding
+    (2, 3, 1, "bf16", 0, 0), (3, 2, 7, "f32", 4, 0), (2, 4, 9, "bf16", 0, 3),
+    (4, 5, 4095, "bf16", 8, 3), (5, 6, 4097, "f32", 0, 7), (3, 7, 32001, "bf16", 24, 0),
+    (2, 9, 50001, "f32", 0, 64), (40, 3, 513, "bf16", 0, 0), (2, 3, 151936, "bf16", 0, 13),
+]
+
+
+@pytest.mark.parametrize("B,K,V,dtype,pad,splits", T1_FUZZ)
+def test_t1_fuzz_chain(B, K, V, dtype, pad, splits):
+    wl = workloads.make_chain(B=B, K=K, V=V, d=64, h=32, dtype=dtype, seed=7 * B + V % 89, bias=True,
+                              noise=0.7, peaked=0.2)
+    gpu, stats = _t1_block(wl, 0.5, V + splits, splits=splits, pad=pad)
+    _report(f"T=1 fuzz B={B} K={K} V={V} {dtype} pad={pad} splits={splits}", stats, gpu)
+
+
+@pytest.mark.parametrize("shape,N", [("random", 60), ("star", 17), ("path", 9)])
+def test_t1_fuzz_tree(shape, N):
+    tr = workloads.make_random_tree(B=4, N=N, V=3001, d=64, h=48, shape=shape, seed=N + 1, bias=True,
+                                    noise=0.5)
+    gpu, stats = _t1_tree(tr, 0.4, N, pad=8)
+    _report(f"T=1 tree {shape} N={N}", stats, gpu)
+
+
+def test_t1_adversarial_rows_and_edge_uniforms():
+    B, K, V = 4, 5, 16391
+    wl = workloads.make_chain(B=B, K=K, V=V, d=64, h=32, dtype="bf16", seed=78, bias=True)
+    wl.target = _adversarial_rows(B, K + 1, V, 3).to(torch.bfloat16)
+    wl.draft_tokens = torch.argmax(wl.draft.float(), -1).to(torch.int32)
+    u = _uniforms((B, K + 1), 9)
+    u[0, :] = torch.tensor([0.0, -1.0, float("nan"), 1.0, 2.0, 0.9999999])
+    gpu = _gpu_block(wl, 0.5, splits=5, u=u)
+    uc = u.double().numpy()
+    uc = np.where(np.isnan(uc) | (uc < 0), 0.0, np.minimum(uc, float(np.nextafter(np.float32(1), np.float32(0)))))
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(wl.target), uc, stats)
+    stats.update(parity.check_block(gpu, _ref_block(wl, 0.5, torch.from_numpy(uc), cand)))
+    _report("T=1 adversarial rows", stats, gpu)
+    assert gpu["tgt_candidate"][0, 0] == 0 and gpu["tgt_candidate"][0, 1] == 0
+
+
+def test_t1_grid_counts_follow_softmax():
+    # every target row is the same logit row; inverting the grid u_k = (k + 1/2)/n
+    # must hit index v within a rounding step of n * p_v times
+    V, B, K = 1000, 512, 7
+    row = torch.randn(V, generator=torch.Generator().manual_seed(12)) * 2
+    wl = workloads.make_chain(B=B, K=K, V=V, d=64, h=32, dtype="f32", seed=1)
+    wl.target = row.expand(B, K + 1, V).contiguous()
+    n = B * (K + 1)
+    u = ((torch.arange(n, dtype=torch.float64) + 0.5) / n).float().reshape(B, K + 1)
+    gpu = _gpu_block(wl, 0.5, u=u)
+    counts = np.bincount(gpu["tgt_candidate"].numpy().ravel(), minlength=V)
+    p = torch.softmax(row.double(), 0).numpy()
+    assert np.abs(counts - n * p).max() <= 2.0
+
+
+def test_t1_greedy_path_unchanged_and_deterministic():
+    wl = workloads.make_config(3, B=8)
+    g0 = _gpu_block(wl, 0.5)
+    assert torch.equal(g0["tgt_candidate"], g0["tgt_argmax"])
+    u = _uniforms((wl.B, wl.K + 1), 33)
+    a = _gpu_block(wl, 0.5, u=u)
+    b = _gpu_block(wl, 0.5, u=u)
+    for k in a:
+        assert torch.equal(a[k], b[k]) or (a[k].dtype.is_floating_point and
+                                           torch.equal(torch.nan_to_num(a[k]), torch.nan_to_num(b[k]))), k
