@@ -75,27 +75,69 @@ __device__ inline void consume(const float *x, int chunk, Lane &st) {
     }
 }
 
+// Lane exchanges that stay in the VALU (no LDS round trip): DPP patterns inside
+// rows of 16 lanes and the gfx950 permlane swaps across rows.
+constexpr int kDppXor1 = 0xB1;    // quad_perm [1,0,3,2]: lane i <-> i ^ 1
+constexpr int kDppXor2 = 0x4E;    // quad_perm [2,3,0,1]: i <-> i ^ 2
+constexpr int kDppXor7 = 0x141;   // row_half_mirror:     i <-> i ^ 7 within 8 lanes
+constexpr int kDppXor15 = 0x140;  // row_mirror:          i <-> i ^ 15 within 16 lanes
+constexpr int kDppXor8 = 0x128;   // row_ror:8:           i <-> i ^ 8 within 16 lanes
+
+template <int CTRL>
+__device__ inline float dpp(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// permlane32_swap(x, y): lanes 0..31 of the results hold (x[l], x[l + 32]), lanes
+// 32..63 hold (y[l - 32], y[l]); permlane16_swap does the same between the even and
+// odd rows of 16 lanes.  Their sum pairs lane l with l ^ 32 (or l ^ 16), taking x in
+// the lower and y in the upper half.
+__device__ inline float swap32_sum(float x, float y) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+__device__ inline float swap16_sum(float x, float y) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+// Whole-wave sum in every lane.
+__device__ inline float wave_sum_valu(float x) {
+    x += dpp<kDppXor1>(x);
+    x += dpp<kDppXor2>(x);
+    x += dpp<kDppXor7>(x);
+    x += dpp<kDppXor15>(x);
+    x = swap16_sum(x, x);
+    return swap32_sum(x, x);
+}
+
+__device__ inline float wave_max_valu(float x) {
+    x = fmaxf(x, dpp<kDppXor1>(x));
+    x = fmaxf(x, dpp<kDppXor2>(x));
+    x = fmaxf(x, dpp<kDppXor7>(x));
+    x = fmaxf(x, dpp<kDppXor15>(x));
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+    const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+
 // Eight per-lane values m[0..7] -> lane L returns the wave's sum of m[L >> 3].
-// Each exchange halves the values a lane carries (xor 32, 16, 8), then the eight
-// lanes that share bits 3..5 add up (xor 4, 2, 1): 10 shuffles instead of 48.
+// Each exchange halves the values a lane carries (lane bits 5, 4, 3), then the
+// eight lanes that share bits 3..5 add up (bits 0..2): 7 exchanges + 3 DPP adds.
 __device__ inline float transpose_sum8(const float (&m)[8], int lane) {
-    const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
     float r4[4], r2[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const float send = b5 ? m[j] : m[j + 4];
-        r4[j] = (b5 ? m[j + 4] : m[j]) + __shfl_xor(send, 32);
-    }
+    for (int j = 0; j < 4; ++j) r4[j] = swap32_sum(m[j], m[j + 4]);     // value j + 4 * bit5
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const float send = b4 ? r4[j] : r4[j + 2];
-        r2[j] = (b4 ? r4[j + 2] : r4[j]) + __shfl_xor(send, 16);
-    }
+    for (int j = 0; j < 2; ++j) r2[j] = swap16_sum(r4[j], r4[j + 2]);   // j + 2 * bit4 + 4 * bit5
+    const bool b3 = lane & 8;
     const float send = b3 ? r2[0] : r2[1];
-    float r = (b3 ? r2[1] : r2[0]) + __shfl_xor(send, 8);
-    r += __shfl_xor(r, 4);
-    r += __shfl_xor(r, 2);
-    r += __shfl_xor(r, 1);
+    float r = (b3 ? r2[1] : r2[0]) + dpp<kDppXor8>(send);              // bit3 + 2 * bit4 + 4 * bit5
+    r += dpp<kDppXor1>(r);
+    r += dpp<kDppXor2>(r);
+    r += dpp<kDppXor7>(r);
     return r;
 }
 
@@ -127,7 +169,7 @@ __device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, La
 // Wave-wide rescale to the reference of the wave's largest chunk max; returns the
 // factor applied to S.
 __device__ inline float rescale_wave(Lane &st, float cm) {
-    const float nr = __fmul_rn(wave_max(cm), kLog2e);
+    const float nr = __fmul_rn(wave_max_valu(cm), kLog2e);
     const float dr = st.ref - nr;
     const float f = __builtin_amdgcn_exp2f(dr);
     st.T = f * fmaf(dr, st.S, st.T);
@@ -208,7 +250,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
             st.T = fmaf(e, t, st.T);
         }
         st.S += mu;
-        const float tot = wave_sum(mu);
+        const float tot = wave_sum_valu(mu);
         if (lane == 0) seg[w / kSegVecs] = make_float2(tot, st.ref);
     }
 }

@@ -56,12 +56,16 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     const float incl = wave_incl_scan(run, lane);
     const float up = __shfl_up(incl, 1);
     const float excl = lane ? up : 0.f;
-    const float total = __shfl(incl, 63);
+    // lanes past the last segment add only zeros, but the scan rounds their sums
+    // in another order: the total is the last owning lane's, and only owning
+    // lanes may cross
+    const bool owns = s0 < s1;
+    const float total = __shfl(incl, (a.nseg - 1) / per);
     const float target = u * total;
-    const uint64_t hit = __ballot(incl > target);
+    const uint64_t hit = __ballot(owns && incl > target);
     // no lane crosses only when rounding put the target at the very end: take the
     // last lane with mass (the maximal element has mass 1, so there is one)
-    const uint64_t has = __ballot(run > 0.f);
+    const uint64_t has = __ballot(owns && run > 0.f);
     const int L = hit ? __builtin_ctzll(hit) : has ? 63 - __builtin_clzll(has) : 0;
     int segsel = -1;
     float before = 0.f;

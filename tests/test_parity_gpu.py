@@ -477,6 +477,22 @@ def test_t1_adversarial_rows_and_edge_uniforms():
     assert gpu["tgt_candidate"][0, 0] == 0 and gpu["tgt_candidate"][0, 1] == 0
 
 
+@pytest.mark.parametrize("V,dtype", [(100, "bf16"), (16391, "bf16"), (4097, "f32"), (151936, "bf16")])
+def test_t1_uniforms_next_to_one(V, dtype):
+    # u just below 1 puts the target in the last segments, where the wave scan's
+    # lanes past the last segment round their (zero-padded) sums differently
+    wl = workloads.make_chain(B=6, K=3, V=V, d=64, h=32, dtype=dtype, seed=V % 101, bias=True,
+                              peaked=0.3)
+    u = torch.full((wl.B, wl.K + 1), 0.99999994, dtype=torch.float32)
+    u[:, 1] = 0.9999
+    u[:, 2] = 0.99999
+    gpu = _gpu_block(wl, 0.5, u=u)
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(wl.target), u.double().numpy(), stats)
+    stats.update(parity.check_block(gpu, _ref_block(wl, 0.5, u, cand)))
+    _report(f"T=1 u next to 1, V={V} {dtype}", stats, gpu)
+
+
 def test_t1_grid_counts_follow_softmax():
     # every target row is the same logit row; inverting the grid u_k = (k + 1/2)/n
     # must hit index v within a rounding step of n * p_v times
