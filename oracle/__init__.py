@@ -43,11 +43,12 @@ __all__ = [
     "F32", "BF16", "AMBIGUITY_BAND", "build", "row_stats", "element", "head_logits",
     "policy_accept", "chain_length", "chain_tokens", "tree_select", "verify_block",
     "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats", "sample_rows",
-    "cdf_at", "candidates",
+    "cdf_at", "candidates", "policy_sample", "action_logprob", "rl_round", "RL_ALPHA", "RL_BETA",
 ]
 
 F32, BF16 = 0, 1
 AMBIGUITY_BAND = 1e-3
+RL_ALPHA, RL_BETA = 1.0, 0.25       # failure-reward weights the paper trains with (Appendix C.2)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cospec_oracle.c")
@@ -229,6 +230,75 @@ def policy_accept(z: np.ndarray, lam: float):
     return accept, pi, ambiguous
 
 
+def policy_sample(z: np.ndarray, u):
+    """Sampled arbitration (Section 3.2: at training time mismatch actions are drawn
+    from pi_theta): a = 1[u < pi] for a caller-supplied uniform u, with pi = sigma(z)
+    taken in fp32 as in policy_accept; decisions with |pi - u| <= 1e-3 (fp64) are
+    flagged ambiguous."""
+    z = np.asarray(z, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    with np.errstate(over="ignore"):
+        z32 = z.astype(np.float32)
+        pi32 = np.float32(1.0) / (np.float32(1.0) + np.exp(-z32))
+        pi = 1.0 / (1.0 + np.exp(-z))
+    u32 = u.astype(np.float32)
+    accept = u32 < pi32
+    ambiguous = np.abs(pi - u32.astype(np.float64)) <= AMBIGUITY_BAND
+    return accept, pi, ambiguous
+
+
+def action_logprob(z: np.ndarray, accept) -> np.ndarray:
+    """log pi_theta(a | q) of the action taken on a mismatch decision (the rollout-time
+    probability in the PPO ratio of Section 3.2): log sigma(z) when a = 1 and
+    log(1 - sigma(z)) = log sigma(-z) when a = 0, in fp64."""
+    z = np.asarray(z, dtype=np.float64)
+    x = np.where(np.asarray(accept, bool), z, -z)
+    # log sigma(x) = -log(1 + e^-x), written without overflow for either sign of x
+    return np.where(x >= 0, -np.log1p(np.exp(-np.abs(x))), x - np.log1p(np.exp(-np.abs(x))))
+
+
+def rl_round(delta, accept, logp_tgt, correct: bool, alpha: float = RL_ALPHA,
+             beta: float = RL_BETA) -> dict:
+    """Per-round statistics of the reinforcement-learning stage (Section 3.2) for one
+    chain round with decisions i = 1..K (index i-1 of each array).
+
+      s      the round length (Eq. cospec_length);
+      I_r    effective actions {i : Delta_i = 0 and i <= min(s, K)};
+      i*     the first mismatch min{i : Delta_i = 0} (0 here when there is none);
+      rho    (s - i*) / ((K+1) - i*), NaN without a mismatch;
+      i_rej  the first rejected mismatch, K+1 when none is rejected;
+      S_acc  {i in I_r : a_i = 1, i < i_rej};  S_rej = {i_rej} if i_rej <= K;
+      g      correct rollout: rho on every effective decision; failed rollout
+             (Eq. failure_penalty): -alpha |l_i| on S_acc, -beta on S_rej.
+             g is reported as 0 outside I_r, where the paper defines no term;
+      J      the round's share of the rollout return, the sum of g over I_r.
+    """
+    K = len(delta)
+    s = chain_length(delta, accept)
+    mism = [i for i in range(1, K + 1) if not delta[i - 1]]
+    i_star = mism[0] if mism else 0
+    rho = (s - i_star) / ((K + 1) - i_star) if mism else math.nan
+    rejected = [i for i in mism if not accept[i - 1]]
+    i_rej = rejected[0] if rejected else K + 1
+    eff = [False] * K
+    s_acc = [False] * K
+    s_rej = [False] * K
+    g = [0.0] * K
+    for i in mism:
+        if i <= min(s, K):
+            eff[i - 1] = True
+            s_acc[i - 1] = bool(accept[i - 1]) and i < i_rej
+            s_rej[i - 1] = i == i_rej and i_rej <= K
+            if correct:
+                g[i - 1] = rho
+            else:
+                g[i - 1] = (-alpha * abs(float(logp_tgt[i - 1])) * s_acc[i - 1]
+                            - beta * s_rej[i - 1])
+    J = float(sum(g[i] for i in range(K) if eff[i]))
+    return dict(s=s, i_star=i_star, rho=rho, i_rej=i_rej, effective=np.array(eff),
+                s_acc=np.array(s_acc), s_rej=np.array(s_rej), g=np.array(g), J=J)
+
+
 def chain_length(delta, accept) -> int:
     """Eq. cospec_length: s = min{i : Delta_i = 0 and a_i = 0} (1-based), else K+1."""
     K = len(delta)
@@ -285,7 +355,8 @@ def _head_arrays(head):
 
 
 def verify_block(target, draft, draft_tokens, hidden, head, lam: float, sample_u=None,
-                 cand_override=None) -> dict:
+                 cand_override=None, policy_u=None, correct=None, alpha: float = RL_ALPHA,
+                 beta: float = RL_BETA) -> dict:
     """Oracle of one chain verify step.
 
     target [B, K+1, V], draft [B, K, V] (float32 or bf16 bits), draft_tokens int
@@ -294,7 +365,10 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float, sample_u
     i-1 (Section 3.1, Delta_i): its argmax, or with sample_u [B, K+1] its
     temperature-1 sample (see candidates()).  Mismatches are scored with the head
     (Section 3.3) and the round stops at the first rejected mismatch
-    (Eq. cospec_length), emitting the candidate of row s-1 last.
+    (Eq. cospec_length), emitting the candidate of row s-1 last.  With policy_u
+    [B, K] mismatch actions are sampled (policy_sample) instead of thresholded.
+    With correct [B] (the rollouts' Corr flags) the per-round RL statistics of
+    rl_round are added, from the nominal actions.
     """
     B, K1, V = target.shape
     K = K1 - 1
@@ -315,20 +389,28 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float, sample_u
     if len(mism):
         rows = mism[:, 0] * K + mism[:, 1]
         z[mism[:, 0], mism[:, 1]] = head_logits(hidden.reshape(B * K, -1), rows, w1, b1, w2, b2)
-    acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    if policy_u is None:
+        acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    else:
+        acc_m, pi_m, amb_m = policy_sample(np.where(delta, 0.0, z), policy_u)
     accept = np.where(delta, True, acc_m)
     pi = np.where(delta, 1.0, pi_m)
     ambiguous = np.where(delta, False, amb_m)
     z_tilde = np.where(delta, np.inf, z)
+    logp_action = np.where(delta, 0.0, action_logprob(np.where(delta, 0.0, z), accept))
     accept_len = np.empty(B, np.int64)
     tokens = np.empty((B, K + 1), np.int64)
     outcomes = []
+    rl = []
     for b in range(B):
         s = chain_length(delta[b], accept[b])
         accept_len[b] = s
         tokens[b] = chain_tokens(s, toks[b], cand[b])
         outcomes.append(chain_outcomes(delta[b], accept[b], ambiguous[b], toks[b], cand[b]))
-    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent, tgt_cand=cand,
+        if correct is not None:
+            rl.append(rl_round(delta[b], accept[b], logp_tgt[b], bool(correct[b]), alpha, beta))
+    return dict(logp_action=logp_action, rl=rl if correct is not None else None,
+                tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent, tgt_cand=cand,
                 drf_max=ds.max, drf_arg=ds.arg, drf_lse=ds.lse, drf_ent=ds.ent,
                 delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z, z_tilde=z_tilde,
                 pi=pi, accept=accept, ambiguous=ambiguous, accept_len=accept_len,
@@ -363,7 +445,7 @@ def _internal(parent) -> np.ndarray:
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float, sample_u=None,
-                cand_override=None) -> dict:
+                cand_override=None, policy_u=None) -> dict:
     """Oracle of one tree verify step (tree reading of Section 3.1/3.3).
 
     target, draft [B, N, V]; parent int [B, N] (parent[0] = -1, parent[n] < n);
@@ -407,11 +489,15 @@ def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float, sa
     mb, mn = np.nonzero(~delta)
     if len(mb):
         z[mb, mn] = head_logits(hidden.reshape(B * N, -1), mb * N + mn, w1, b1, w2, b2)
-    acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    if policy_u is None:
+        acc_m, pi_m, amb_m = policy_accept(np.where(delta, 0.0, z), lam)
+    else:
+        acc_m, pi_m, amb_m = policy_sample(np.where(delta, 0.0, z), policy_u)
     accept = np.where(delta, True, acc_m)
     pi = np.where(delta, 1.0, pi_m)
     ambiguous = np.where(delta, False, amb_m)
     z_tilde = np.where(delta, np.inf, z)
+    logp_action = np.where(delta, 0.0, action_logprob(np.where(delta, 0.0, z), accept))
     accept_len = np.empty(B, np.int64)
     tokens = np.empty((B, N), np.int64)
     path = np.empty((B, N), np.int64)
@@ -423,8 +509,8 @@ def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float, sa
         tokens[b], path[b] = _tree_emit(best, pth, toks[b], cand[b], N)
         outcomes.append(tree_outcomes(par[b], delta[b], accept[b], ambiguous[b], toks[b],
                                       cand[b]))
-    return dict(tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse, tgt_ent=ts.ent, tgt_cand=cand,
-                drf_max=drf_max, drf_arg=drf_arg, drf_lse=drf_lse, drf_ent=drf_ent,
+    return dict(logp_action=logp_action, tgt_max=ts.max, tgt_arg=ts.arg, tgt_lse=ts.lse,
+                tgt_ent=ts.ent, tgt_cand=cand, drf_max=drf_max, drf_arg=drf_arg, drf_lse=drf_lse, drf_ent=drf_ent,
                 internal=internal, delta=delta, logp_tgt=logp_tgt, logp_drf=logp_drf, z=z,
                 z_tilde=z_tilde, pi=pi, accept=accept, ambiguous=ambiguous,
                 accept_len=accept_len, tokens=tokens, path=path, outcomes=outcomes)

@@ -538,3 +538,90 @@ def test_sampled_candidates_on_peaked_rows_equal_greedy():
     r0 = oracle.verify_block(bits, d, toks, hid, head, 0.5)
     np.testing.assert_array_equal(r1["tgt_cand"], r0["tgt_arg"])
     np.testing.assert_array_equal(r1["tokens"], r0["tokens"])
+
+
+# ---------------------------------------------------------------- sampled arbitration and RL statistics
+
+@pytest.mark.parametrize("r", _load("rl_rounds.json")["rounds"], ids=lambda r: r["name"])
+def test_rl_round_golden(r):
+    for correct, gk, jk in ((True, "g_correct", "J_correct"), (False, "g_failed", "J_failed")):
+        out = oracle.rl_round(r["delta"], r["accept"], r["logp"], correct, r["alpha"], r["beta"])
+        assert out["s"] == r["s"] and out["i_star"] == r["i_star"] and out["i_rej"] == r["i_rej"]
+        if r["rho"] is None:
+            assert math.isnan(out["rho"])
+        else:
+            assert out["rho"] == pytest.approx(r["rho"], abs=1e-15)
+        np.testing.assert_array_equal(out["effective"], np.array(r["effective"], bool))
+        np.testing.assert_array_equal(out["s_acc"], np.array(r["s_acc"], bool))
+        np.testing.assert_array_equal(out["s_rej"], np.array(r["s_rej"], bool))
+        np.testing.assert_allclose(out["g"], r[gk], rtol=0, atol=1e-15)
+        assert out["J"] == pytest.approx(r[jk], abs=1e-15)
+
+
+@pytest.mark.parametrize("K", [1, 2, 4, 6])
+def test_rl_round_invariants_brute_force(K):
+    logp = -np.linspace(0.1, 3.0, K)
+    for delta in itertools.product([0, 1], repeat=K):
+        for acc in itertools.product([0, 1], repeat=K):
+            a = [1 if d else x for d, x in zip(delta, acc)]         # matches are forced accepts
+            ok = oracle.rl_round(delta, a, logp, True)
+            bad = oracle.rl_round(delta, a, logp, False)
+            s = oracle.chain_length(delta, a)
+            mism = [i + 1 for i in range(K) if not delta[i]]
+            eff = ok["effective"]
+            assert ok["s"] == s == ok["i_rej"] or (ok["i_rej"] == K + 1 and s == K + 1)
+            assert all(not delta[i] for i in range(K) if eff[i])      # I_r holds mismatches only
+            assert all(i + 1 <= min(s, K) for i in range(K) if eff[i])
+            assert not (bad["s_acc"] & bad["s_rej"]).any()
+            assert ((bad["s_acc"] | bad["s_rej"]) <= eff).all()
+            assert bad["s_rej"].sum() <= 1 and (bad["s_rej"].sum() == 0) == (s == K + 1)
+            assert all(g <= 0 for g in bad["g"])
+            if mism:
+                assert 0.0 <= ok["rho"] <= 1.0
+                assert (ok["rho"] == 1.0) == (s == K + 1)
+                assert ok["J"] == pytest.approx(eff.sum() * ok["rho"], abs=1e-12)
+                if not any(a[i - 1] for i in mism):                    # always defer: rho = 0
+                    assert ok["rho"] == 0.0 and ok["J"] == 0.0
+                    assert bad["J"] == -oracle.RL_BETA
+            else:
+                assert math.isnan(ok["rho"]) and not eff.any() and ok["J"] == 0.0 == bad["J"]
+
+
+def test_policy_sample_strict_and_grid():
+    a, pi, amb = oracle.policy_sample(np.zeros(3), [0.5, 0.4999, 0.50001])
+    assert list(a) == [False, True, False] and amb.all()          # u < pi, pi(0) = 1/2 exactly
+    a, _, _ = oracle.policy_sample(np.array([80.0, -80.0]), [1 - 1e-7, 1e-7])
+    assert list(a) == [True, False]
+    z = 0.37
+    n = 20000
+    a, pi, _ = oracle.policy_sample(np.full(n, z), (np.arange(n) + 0.5) / n)
+    assert abs(a.mean() - scipy.special.expit(z)) <= 1.0 / n + 1e-7
+
+
+def test_action_logprob_closed_form():
+    z = np.array([-40.0, -3.0, 0.0, 0.5, 7.0, 40.0])
+    np.testing.assert_allclose(oracle.action_logprob(z, np.ones(6, bool)), scipy.special.log_expit(z),
+                               rtol=1e-13, atol=1e-300)
+    np.testing.assert_allclose(oracle.action_logprob(z, np.zeros(6, bool)), scipy.special.log_expit(-z),
+                               rtol=1e-13, atol=1e-300)
+    assert oracle.action_logprob(np.array([0.0]), [True])[0] == pytest.approx(math.log(0.5), abs=1e-16)
+
+
+def test_verify_block_sampled_policy_and_rl():
+    wl = _small_chain(B=10, K=6, V=700, noise=1.2)
+    t, d, toks, hid, head = _np_chain(wl)
+    u = np.random.default_rng(5).random((wl.B, wl.K))
+    corr = np.arange(wl.B) % 2
+    r = oracle.verify_block(t, d, toks, hid, head, 0.5, policy_u=u, correct=corr)
+    for b in range(wl.B):
+        for i in range(wl.K):
+            if not r["delta"][b, i]:
+                assert r["accept"][b, i] == (np.float32(u[b, i]) < np.float32(1) / (np.float32(1) + np.exp(
+                    -np.float32(r["z"][b, i]))))
+        st = r["rl"][b]
+        assert st["s"] == r["accept_len"][b]
+        ref = oracle.rl_round(r["delta"][b], r["accept"][b], r["logp_tgt"][b], bool(corr[b]))
+        np.testing.assert_array_equal(st["g"], ref["g"])
+    # sampled actions differ from the lambda = 0.5 threshold somewhere
+    r2 = oracle.verify_block(t, d, toks, hid, head, 0.5)
+    assert (r["accept"] != r2["accept"]).any()
