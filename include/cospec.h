@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define COSPEC_ABI_VERSION 3
+#define COSPEC_ABI_VERSION 4
 #define COSPEC_MAX_K 64      /* chain: draft tokens per block              */
 #define COSPEC_MAX_N 256     /* tree: nodes per tree, root included        */
 #define COSPEC_MAX_SPLITS 64 /* workgroups per logit row (tuning override) */
@@ -111,7 +111,40 @@ typedef struct {
     uint8_t *accept;       /* per decision: a_i (1 on matches)                 */
     int32_t *tgt_candidate; /* per target row: the verification candidate used
                               (the argmax, or the temperature-1 sample)        */
+    float *logp_action;    /* per decision: log pi(a_i) of the action taken,
+                              log sigma(z) if accepted, log sigma(-z) if not
+                              (the rollout-time probability of Section 3.2);
+                              0 on matches, NaN where the head did not run or
+                              the draft token is invalid                      */
 } cospec_features;
+
+/*
+ * Per-round statistics of the reinforcement-learning stage (Section 3.2), for
+ * chains only.  With decisions i = 1..K, s the round length and Delta, a the
+ * mismatch flags and actions:
+ *   effective actions  I = {i : Delta_i = 0 and i <= min(s, K)}
+ *   first mismatch     i* = min{i : Delta_i = 0}
+ *   rho                (s - i*) / ((K+1) - i*)
+ *   first rejection    i_rej = min{i : Delta_i = 0 and a_i = 0}, or K+1
+ *   S_acc              {i in I : a_i = 1, i < i_rej};  S_rej = {i_rej} if <= K
+ *   reward g_i         correct rollout: rho on I; failed rollout
+ *                      (Eq. failure_penalty): -alpha |l_i| on S_acc, -beta on
+ *                      S_rej, with l_i = log p_T(draft token i)
+ *   round return       sum of g over I (the round's share of J)
+ * An invalid draft token counts as a rejected mismatch with l_i = NaN.  Every
+ * output is optional; `correct` is required when reward or round_return is set.
+ */
+typedef struct {
+    const uint8_t *correct;   /* [B] in: Corr of each sequence's rollout (0 or 1)     */
+    float alpha, beta;        /* failure-reward weights (the paper uses 1.0, 0.25)    */
+    uint8_t *effective;       /* [B][K] out: 1 if decision i is in I                   */
+    uint8_t *in_s_acc;        /* [B][K] out: 1 if decision i is in S_acc               */
+    int32_t *first_mismatch;  /* [B] out: i*, or 0 when the round has no mismatch      */
+    int32_t *first_reject;    /* [B] out: i_rej (K+1 when no mismatch is rejected)     */
+    float *rho;               /* [B] out: rho, NaN when the round has no mismatch      */
+    float *reward;            /* [B][K] out: g_i on I, 0 elsewhere                     */
+    float *round_return;      /* [B] out: sum of g over I                              */
+} cospec_rl;
 
 /*
  * Optional hooks; a NULL options pointer, or zero/NULL members, mean defaults.
@@ -148,6 +181,14 @@ typedef struct {
      * may select either neighbour.
      */
     const float *sample_uniform;
+    /*
+     * Sampled arbitration (Section 3.2: rollouts draw mismatch actions from the
+     * policy).  NULL: a_i = 1[sigma(z_i) > lambda] (Eq. infer_thre).  Otherwise
+     * one uniform per decision ([B][K] chain, [B][N] tree) and a mismatch is
+     * accepted when policy_uniform < sigma(z_i) (fp32); lambda is then unused.
+     */
+    const float *policy_uniform;
+    const cospec_rl *rl;      /* chain only: per-round RL statistics, or NULL      */
 } cospec_options;
 
 /* COSPEC_ABI_VERSION of the built library. */

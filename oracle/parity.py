@@ -81,6 +81,12 @@ def _decisions(gpu, ref, dmask, stats):
     firm = dmask & ~ref["ambiguous"]
     _exact("accept", acc, ref["accept"], firm)
     stats["ambiguous_decisions"] = int((dmask & ref["ambiguous"]).sum())
+    if "logp_action" in gpu and "logp_action" in ref:
+        la = _np(gpu["logp_action"])
+        if not np.all(la[match] == 0.0):
+            raise ParityError("logp_action must be 0 on matched decisions")
+        scored = mism & firm & np.isfinite(ref["logp_action"]) & np.isfinite(_np(gpu["z_tilde"]))
+        _close("logp_action", la, ref["logp_action"], "logp", stats, scored)
 
 
 def _outcomes(got_len, got_tok, got_path, ref, stats):
@@ -170,4 +176,32 @@ def check_outputs_only(gpu: dict, ref: dict, tree: bool = False) -> dict:
     stats = {}
     _outcomes(_np(gpu["accept_len"]), _np(gpu["tokens"]), _np(gpu["path"]) if tree else None,
               ref, stats)
+    return stats
+
+
+def check_rl(gpu: dict, ref: dict, correct, alpha: float, beta: float) -> dict:
+    """Per-round RL statistics of a chain step (the rl_* outputs) against
+    oracle.rl_round, evaluated on the GPU's own actions (which check_block has
+    already matched to the oracle's outside the ambiguity band) and the oracle's
+    log p_T."""
+    from . import rl_round
+    stats = {}
+    acc = _np(gpu["accept"]).astype(bool)
+    B, K = acc.shape
+    eff, sacc, g = np.zeros((B, K), bool), np.zeros((B, K), bool), np.zeros((B, K))
+    istar, irej, rho, J = (np.zeros(B, np.int64), np.zeros(B, np.int64), np.zeros(B), np.zeros(B))
+    for b in range(B):
+        r = rl_round(ref["delta"][b], acc[b], ref["logp_tgt"][b], bool(correct[b]), alpha, beta)
+        eff[b], sacc[b], g[b] = r["effective"], r["s_acc"], r["g"]
+        istar[b], irej[b], rho[b], J[b] = r["i_star"], r["i_rej"], r["rho"], r["J"]
+    _exact("rl_effective", gpu["rl_effective"], eff)
+    _exact("rl_in_s_acc", gpu["rl_in_s_acc"], sacc)
+    _exact("rl_first_mismatch", gpu["rl_first_mismatch"], istar)
+    _exact("rl_first_reject", gpu["rl_first_reject"], irej)
+    has = istar > 0
+    if not np.all(np.isnan(_np(gpu["rl_rho"])[~has])):
+        raise ParityError("rho must be NaN for rounds without a mismatch")
+    _close("rl_rho", gpu["rl_rho"], rho, "logp", stats, has)
+    _close("rl_reward", gpu["rl_reward"], g, "logp", stats)
+    _close("rl_return", gpu["rl_round_return"], J, "logp", stats)
     return stats

@@ -35,11 +35,19 @@ class _Head(ctypes.Structure):
 
 _FEATURE_FIELDS = ["tgt_argmax", "tgt_max", "tgt_lse", "tgt_entropy", "drf_argmax", "drf_max",
                    "drf_lse", "drf_entropy", "logp_tgt", "logp_drf", "delta", "z_tilde", "policy",
-                   "accept", "tgt_candidate"]
+                   "accept", "tgt_candidate", "logp_action"]
 
 
 class _Features(ctypes.Structure):
     _fields_ = [(f, ctypes.c_void_p) for f in _FEATURE_FIELDS]
+
+
+class _RL(ctypes.Structure):
+    _fields_ = [("correct", ctypes.c_void_p), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
+                ("effective", ctypes.c_void_p), ("in_s_acc", ctypes.c_void_p),
+                ("first_mismatch", ctypes.c_void_p), ("first_reject", ctypes.c_void_p),
+                ("rho", ctypes.c_void_p), ("reward", ctypes.c_void_p),
+                ("round_return", ctypes.c_void_p)]
 
 
 class _Options(ctypes.Structure):
@@ -47,7 +55,8 @@ class _Options(ctypes.Structure):
                 ("reduce2_begin", ctypes.c_void_p), ("reduce2_end", ctypes.c_void_p),
                 ("splits", ctypes.c_int32), ("aux_stream", ctypes.c_void_p),
                 ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p),
-                ("sample_uniform", ctypes.c_void_p)]
+                ("sample_uniform", ctypes.c_void_p), ("policy_uniform", ctypes.c_void_p),
+                ("rl", ctypes.POINTER(_RL))]
 
 
 def _event_handle(ev) -> int:
@@ -139,7 +148,7 @@ class Prepared:
     `launch()` enqueues the step with no allocation."""
 
     def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, splits,
-                 overlap, uniform=None):
+                 overlap, uniform=None, policy_u=None, rl=None):
         self._fn = fn
         self._args = args_before_feats
         self.outputs = outputs
@@ -148,6 +157,8 @@ class Prepared:
         self.workspace = workspace
         self.splits = int(splits)
         self.uniform = uniform
+        self.policy_u = policy_u
+        self.rl = rl                    # (struct, output tensors, correct tensor) or None
         self.aux = None
         if overlap:
             dev = workspace.device
@@ -155,12 +166,15 @@ class Prepared:
         self._keep = []
 
     def _options(self, timing):
-        if timing is None and not self.splits and self.aux is None and self.uniform is None:
+        if (timing is None and not self.splits and self.aux is None and self.uniform is None
+                and self.policy_u is None and self.rl is None):
             return None
         ev = [None] * 4 if timing is None else [None if e is None else _event_handle(e) for e in timing]
         aux = (None, None, None) if self.aux is None else (
             self.aux[0].cuda_stream, _event_handle(self.aux[1]), _event_handle(self.aux[2]))
-        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux, _ptr(self.uniform))
+        rl = None if self.rl is None else ctypes.pointer(self.rl[0])
+        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux, _ptr(self.uniform),
+                        _ptr(self.policy_u), rl)
 
     def launch(self, timing=None):
         """Enqueue the step on torch's current stream.  `timing` = four torch events
@@ -174,6 +188,8 @@ class Prepared:
     def result(self) -> dict:
         out = dict(self.outputs)
         out.update(self.features or {})
+        if self.rl is not None:
+            out.update({"rl_" + k: v for k, v in self.rl[1].items()})
         return out
 
 
@@ -185,7 +201,8 @@ def _features(alloc: bool, dev, B, RT, RD, D):
                   tgt_entropy=((B, RT), f32), drf_argmax=((B, RD), i32), drf_max=((B, RD), f32),
                   drf_lse=((B, RD), f32), drf_entropy=((B, RD), f32), logp_tgt=((B, D), f32),
                   logp_drf=((B, D), f32), delta=((B, D), u8), z_tilde=((B, D), f32),
-                  policy=((B, D), f32), accept=((B, D), u8), tgt_candidate=((B, RT), i32))
+                  policy=((B, D), f32), accept=((B, D), u8), tgt_candidate=((B, RT), i32),
+                  logp_action=((B, D), f32))
     feats = {k: torch.empty(s, dtype=t, device=dev) for k, (s, t) in shapes.items()}
     st = _Features(*[_ptr(feats[f]) for f in _FEATURE_FIELDS])
     return feats, st
@@ -199,11 +216,43 @@ def _uniforms(u: Optional[torch.Tensor], B: int, RT: int):
     return u
 
 
+def _policy_uniforms(u: Optional[torch.Tensor], B: int, D: int):
+    if u is None:
+        return None
+    if tuple(u.shape) != (B, D) or u.dtype != torch.float32 or not u.is_contiguous() or not u.is_cuda:
+        raise ValueError("policy_u must be a contiguous float32 device tensor [B, decisions]")
+    return u
+
+
+def _rl(correct: Optional[torch.Tensor], alpha: float, beta: float, B: int, K: int, dev):
+    if correct is None:
+        return None
+    if tuple(correct.shape) != (B,) or correct.dtype != torch.uint8 or not correct.is_cuda:
+        raise ValueError("correct must be a uint8 device tensor [B]")
+    correct = correct.contiguous()
+    outs = dict(effective=torch.empty((B, K), dtype=torch.uint8, device=dev),
+                in_s_acc=torch.empty((B, K), dtype=torch.uint8, device=dev),
+                first_mismatch=torch.empty(B, dtype=torch.int32, device=dev),
+                first_reject=torch.empty(B, dtype=torch.int32, device=dev),
+                rho=torch.empty(B, dtype=torch.float32, device=dev),
+                reward=torch.empty((B, K), dtype=torch.float32, device=dev),
+                round_return=torch.empty(B, dtype=torch.float32, device=dev))
+    st = _RL(_ptr(correct), float(alpha), float(beta), *[_ptr(outs[k]) for k in (
+        "effective", "in_s_acc", "first_mismatch", "first_reject", "rho", "reward", "round_return")])
+    return st, outs, correct
+
+
 def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
                   splits: int = 0, overlap: bool = False,
-                  sample_u: Optional[torch.Tensor] = None) -> Prepared:
+                  sample_u: Optional[torch.Tensor] = None,
+                  policy_u: Optional[torch.Tensor] = None,
+                  correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
+                  beta: float = 0.25) -> Prepared:
     """sample_u: one uniform per target row [B, K+1] for temperature-1 candidates
-    (cospec_options.sample_uniform); None for the greedy argmax."""
+    (cospec_options.sample_uniform); None for the greedy argmax.  policy_u: one
+    uniform per decision [B, K] for sampled arbitration.  correct: uint8 [B]
+    rollout correctness; turns on the per-round RL statistics (returned with an
+    "rl_" prefix) with failure-reward weights alpha and beta."""
     B, R, V = target.shape
     K = R - 1
     ld = _row_stride(target)
@@ -228,15 +277,18 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
             ctypes.byref(hs), float(lam), B, K, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]))
     p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits, overlap,
-                 _uniforms(sample_u, B, K + 1))
+                 _uniforms(sample_u, B, K + 1), _policy_uniforms(policy_u, B, K),
+                 _rl(correct, alpha, beta, B, K, dev))
     p._keep = [hs, target, draft, draft_tokens, hidden, head]
     return p
 
 
 def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
                  features: bool = True, splits: int = 0, overlap: bool = False,
-                 sample_u: Optional[torch.Tensor] = None) -> Prepared:
-    """sample_u: one uniform per target row [B, N] for temperature-1 candidates."""
+                 sample_u: Optional[torch.Tensor] = None,
+                 policy_u: Optional[torch.Tensor] = None) -> Prepared:
+    """sample_u: one uniform per target row [B, N] for temperature-1 candidates;
+    policy_u: one uniform per node [B, N] for sampled arbitration."""
     B, N, V = target.shape
     ld = _row_stride(target)
     if _row_stride(draft) != ld or tuple(draft.shape) != (B, N, V):
@@ -261,27 +313,32 @@ def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
             _ptr(hidden), ctypes.byref(hs), float(lam), B, N, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]), _ptr(outputs["path"]))
     p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits, overlap,
-                 _uniforms(sample_u, B, N))
+                 _uniforms(sample_u, B, N), _policy_uniforms(policy_u, B, N))
     p._keep = [hs, target, draft, parent, node_tokens, hidden, head]
     return p
 
 
 def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
                  splits: int = 0, overlap: bool = False,
-                 sample_u: Optional[torch.Tensor] = None) -> dict:
-    """cospec_verify_block on device tensors; returns accept_len, tokens (+ features)."""
+                 sample_u: Optional[torch.Tensor] = None,
+                 policy_u: Optional[torch.Tensor] = None,
+                 correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
+                 beta: float = 0.25) -> dict:
+    """cospec_verify_block on device tensors; returns accept_len, tokens (+ features,
+    + rl_* statistics when `correct` is given)."""
     p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits, overlap,
-                      sample_u)
+                      sample_u, policy_u, correct, alpha, beta)
     p.launch()
     return p.result()
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
                 features: bool = True, splits: int = 0, overlap: bool = False,
-                sample_u: Optional[torch.Tensor] = None) -> dict:
+                sample_u: Optional[torch.Tensor] = None,
+                policy_u: Optional[torch.Tensor] = None) -> dict:
     """cospec_verify_tree on device tensors; returns accept_len, tokens, path (+ features)."""
     p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits,
-                     overlap, sample_u)
+                     overlap, sample_u, policy_u)
     p.launch()
     return p.result()
 

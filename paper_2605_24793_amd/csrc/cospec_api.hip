@@ -17,8 +17,9 @@
 //                       score is requested)
 //   4. k_vocab_reduce   with the aux stream only: the draft rows (tree: nodes with
 //                       a child)
-//   5. k_chain_finish / k_tree_finish   draft statistics, log p_D, verdicts,
-//                       first stop, emission
+//   5. k_chain_finish / k_tree_finish   draft statistics, log p_D, verdicts
+//                       (threshold or sampled), first stop, emission, and for
+//                       chains the optional per-round RL statistics
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -65,7 +66,7 @@ inline size_t head_bytes(int64_t m_cap, const cospec_head *hd) {
 
 // Workspace carving shared by the size query and the call.
 struct Layout {
-    size_t partials, seg, tgt_arg, state, listpos, list, count, upart, z, total;
+    size_t partials, seg, tgt_arg, state, listpos, list, count, logp, upart, z, total;
     int64_t partial_slots;
 };
 
@@ -94,6 +95,7 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     L.listpos = off;  off += round_up(static_cast<size_t>(B * D) * 4);
     L.list = off;     off += round_up(static_cast<size_t>(B * D) * 4);
     L.count = off;    off += kAlign;
+    L.logp = off;     off += round_up(static_cast<size_t>(B * D) * 4);
     const int64_t m_cap = B * D;
     L.upart = off;    off += round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
                                       static_cast<size_t>(hd->h) * 4);
@@ -115,7 +117,7 @@ bool feats_aligned(const cospec_features *f) {
     if (!f) return true;
     const void *p4[] = {f->tgt_argmax, f->tgt_max, f->tgt_lse, f->tgt_entropy, f->drf_argmax, f->drf_max,
                         f->drf_lse, f->drf_entropy, f->logp_tgt, f->logp_drf, f->z_tilde, f->policy,
-                        f->tgt_candidate};
+                        f->tgt_candidate, f->logp_action};
     for (const void *p : p4)
         if (p && !aligned(p, 4)) return false;
     return true;
@@ -151,6 +153,16 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     const Layout L = layout(rows, c.B, c.RT, c.D, c.head, c.V);
     const float *uniform = c.opts ? c.opts->sample_uniform : nullptr;
     if (uniform && !aligned(uniform, 4)) return COSPEC_ERR_INVALID_ARG;
+    const float *policy_u = c.opts ? c.opts->policy_uniform : nullptr;
+    if (policy_u && !aligned(policy_u, 4)) return COSPEC_ERR_INVALID_ARG;
+    const cospec_rl *rl = c.opts ? c.opts->rl : nullptr;
+    if (rl) {
+        if (c.is_tree) return COSPEC_ERR_INVALID_ARG;          // defined for chains only
+        if ((rl->reward || rl->round_return) && !rl->correct) return COSPEC_ERR_INVALID_ARG;
+        const void *p4[] = {rl->first_mismatch, rl->first_reject, rl->rho, rl->reward, rl->round_return};
+        for (const void *p : p4)
+            if (p && !aligned(p, 4)) return COSPEC_ERR_INVALID_ARG;
+    }
     if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
     if (!c.ws || !aligned(c.ws, kAlign) || c.ws_bytes < L.total) return COSPEC_ERR_WORKSPACE;
 
@@ -162,14 +174,15 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     int32_t *listpos = reinterpret_cast<int32_t *>(ws + L.listpos);
     int32_t *list = reinterpret_cast<int32_t *>(ws + L.list);
     int32_t *count = reinterpret_cast<int32_t *>(ws + L.count);
+    float *ws_logp = reinterpret_cast<float *>(ws + L.logp);
     float *upart = reinterpret_cast<float *>(ws + L.upart);
     float *zlog = reinterpret_cast<float *>(ws + L.z);
 
     const cospec_features F = c.feats ? *c.feats : cospec_features{};
     const bool decisions = c.B > 0 && (c.is_tree ? c.D > 1 : c.D > 0);
     const bool lambda_decides = !(c.lambda >= 0.0f && c.lambda < 1.0f);
-    const bool want_scores = F.z_tilde || F.policy;
-    const bool head = decisions && (!lambda_decides || want_scores);
+    const bool want_scores = F.z_tilde || F.policy || F.logp_action;
+    const bool head = decisions && (!lambda_decides || want_scores || policy_u);
 
     const bool aux = c.opts && c.opts->aux_stream;
     if (aux && (!c.opts->aux_ready || !c.opts->aux_done || c.opts->aux_stream == c.stream))
@@ -240,6 +253,7 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     da.tgt_cand = F.tgt_candidate;
     da.logp_tgt = F.logp_tgt; da.delta = F.delta;
     da.ws_tgt_arg = tgt_arg;
+    da.ws_logp_tgt = ws_logp;
     da.ws_state = state;
     da.ws_listpos = listpos;
     da.ws_list = list;
@@ -307,6 +321,16 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     fa.drf_argmax = F.drf_argmax; fa.drf_max = F.drf_max; fa.drf_lse = F.drf_lse; fa.drf_ent = F.drf_entropy;
     fa.logp_drf = F.logp_drf;
     fa.z_tilde = F.z_tilde; fa.policy = F.policy; fa.accept = F.accept;
+    fa.logp_action = F.logp_action;
+    fa.policy_u = policy_u;
+    fa.ws_logp_tgt = ws_logp;
+    if (rl) {
+        fa.rl_on = 1;
+        fa.rl_correct = rl->correct; fa.rl_alpha = rl->alpha; fa.rl_beta = rl->beta;
+        fa.rl_effective = rl->effective; fa.rl_s_acc = rl->in_s_acc;
+        fa.rl_first_mismatch = rl->first_mismatch; fa.rl_first_reject = rl->first_reject;
+        fa.rl_rho = rl->rho; fa.rl_reward = rl->reward; fa.rl_return = rl->round_return;
+    }
     if (launch_finish(dt, fa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     return COSPEC_OK;
 }

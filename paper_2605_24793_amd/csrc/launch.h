@@ -72,6 +72,7 @@ struct DecideArgs {
     int32_t sampled;           // ws_tgt_arg already holds the candidates (k_sample)
     int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent; int32_t *tgt_cand;
     float *logp_tgt; uint8_t *delta;
+    float *ws_logp_tgt;        // [B*D] log p_T(draft token), kept for the finish kernel
     int32_t *ws_tgt_arg;       // [B*RT] verification candidate per target row
     uint8_t *ws_state;         // [B*D]
     int32_t *ws_listpos;       // [B*D] position in the compacted list or -1
@@ -112,6 +113,14 @@ struct FinishArgs {
     const float *z;            // head logits by compacted position
     int32_t head_ran;
     float lambda;
+    const float *policy_u;     // [B*D] uniforms of sampled arbitration, or null (threshold)
+    const float *ws_logp_tgt;  // [B*D]
+    // chain RL statistics (all optional)
+    int32_t rl_on;
+    const uint8_t *rl_correct; float rl_alpha, rl_beta;
+    uint8_t *rl_effective; uint8_t *rl_s_acc; int32_t *rl_first_mismatch; int32_t *rl_first_reject;
+    float *rl_rho; float *rl_reward; float *rl_return;
+    float *logp_action;
     const int32_t *ws_tgt_arg;
     int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
     int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent; float *logp_drf;

@@ -452,6 +452,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
         a.ws_state[di] = state;
         if (a.delta) a.delta[di] = state == kStateMatch;
         if (a.logp_tgt) a.logp_tgt[di] = lpt;
+        a.ws_logp_tgt[di] = lpt;
     }
 }
 

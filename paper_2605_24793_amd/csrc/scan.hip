@@ -8,7 +8,8 @@
 //
 // Chain (Section 3.3, Eq. cospec_length): one wave per sequence, lane i-1 owns
 // decision i and draft row i-1.  A matched decision passes (z_tilde = +inf,
-// Eq. policy-prob); a mismatch passes when sigma(z) > lambda (Eq. infer_thre).
+// Eq. policy-prob); a mismatch passes when sigma(z) > lambda (Eq. infer_thre),
+// or, with sampled arbitration, when its uniform is below sigma(z).
 // The first failing decision is the lowest set bit of a wave ballot, s = its
 // position (1-based) or K+1; the round emits draft tokens 1..s-1 and the target
 // token of row s-1.
@@ -31,22 +32,30 @@ namespace {
 struct Verdict {
     bool pass;
     float z_tilde, policy;
+    float logp_action;   // log pi(a) of the action taken
 };
 
-// Verdict of one decision slot from its decide state and the head's logits.
-__device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int head_ran, float lambda) {
+// log sigma(x) without overflow for either sign of x.
+__device__ inline float log_sigmoid(float x) { return fminf(x, 0.f) - log1pf(expf(-fabsf(x))); }
+
+// Verdict of one decision slot from its decide state and the head's logits: the
+// threshold (Eq. infer_thre), or with uniforms a sampled action (u < pi).
+__device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int head_ran, float lambda,
+                                  const float *pu, int64_t di) {
     Verdict v;
     if (state == kStateMatch) {
-        v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f;
+        v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f; v.logp_action = 0.0f;
     } else if (state != kStateMismatch) {          // invalid token or parent: always rejected
-        v.pass = false; v.z_tilde = NAN; v.policy = NAN;
+        v.pass = false; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
     } else if (!head_ran || pos < 0) {
         // head skipped: lambda >= 1 or lambda < 0 decides every mismatch by itself
-        v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN;
+        v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
     } else {
         const float z = zs[pos];
         const float pi = 1.0f / (1.0f + expf(-z));
-        v.pass = pi > lambda; v.z_tilde = z; v.policy = pi;
+        v.pass = pu ? pu[di] < pi : pi > lambda;
+        v.z_tilde = z; v.policy = pi;
+        v.logp_action = log_sigmoid(v.pass ? z : -z);
     }
     return v;
 }
@@ -65,20 +74,24 @@ __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= a.B) return;                                  // whole wave leaves together
     const int K = a.D;
-    bool fail = false;
+    const int64_t di = static_cast<int64_t>(b) * K + lane;  // decision lane+1, draft row lane
+    bool fail = false, mism = false;
+    float lpt = NAN;
     if (lane < K) {
-        const int64_t di = static_cast<int64_t>(b) * K + lane;        // decision lane+1, draft row lane
         const uint8_t st = a.ws_state[di];
         const bool valid = st != kStateReject;
+        mism = st != kStateMatch;
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, a.tokens[di]) : 0.f;
         const RowStat rs = merge_row(a.partials + (a.drf_row0 + di) * a.splits, a.splits);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
-        const Verdict v = verdict(st, a.ws_listpos[di], a.z, a.head_ran, a.lambda);
+        const Verdict v = verdict(st, a.ws_listpos[di], a.z, a.head_ran, a.lambda, a.policy_u, di);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
         if (a.policy) a.policy[di] = v.policy;
         if (a.accept) a.accept[di] = v.pass;
+        if (a.logp_action) a.logp_action[di] = v.logp_action;
+        lpt = a.ws_logp_tgt[di];
     }
     const uint64_t rej = __ballot(fail);
     const int s = rej ? __builtin_ctzll(rej) + 1 : K + 1;
@@ -88,6 +101,31 @@ __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
         if (j < s - 1) tok = a.tokens[static_cast<int64_t>(b) * K + j];
         else if (j == s - 1) tok = a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + j];
         a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = tok;
+    }
+    if (!a.rl_on) return;
+    // Section 3.2: effective actions up to the stop, rho, S_acc / S_rej and the
+    // shaped reward; the first rejected mismatch is the stop itself (or K+1)
+    const uint64_t mm = __ballot(mism);
+    const int i_star = mm ? __builtin_ctzll(mm) + 1 : 0;
+    const int i = lane + 1;
+    const bool eff = mism && i <= min(s, K);
+    const bool acc = eff && !fail && i < s;
+    const bool rjt = eff && i == s && s <= K;
+    const float rho = mm ? static_cast<float>(s - i_star) / static_cast<float>(K + 1 - i_star) : NAN;
+    const bool correct = a.rl_correct && a.rl_correct[b];
+    float g = 0.f;
+    if (eff) g = correct ? rho : -(acc ? a.rl_alpha * fabsf(lpt) : 0.f) - (rjt ? a.rl_beta : 0.f);
+    if (lane < K) {
+        if (a.rl_effective) a.rl_effective[di] = eff;
+        if (a.rl_s_acc) a.rl_s_acc[di] = acc;
+        if (a.rl_reward) a.rl_reward[di] = g;
+    }
+    const float J = wave_sum(g);
+    if (lane == 0) {
+        if (a.rl_first_mismatch) a.rl_first_mismatch[b] = i_star;
+        if (a.rl_first_reject) a.rl_first_reject[b] = s;
+        if (a.rl_rho) a.rl_rho[b] = rho;
+        if (a.rl_return) a.rl_return[b] = J;
     }
 }
 
@@ -137,7 +175,8 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
 
     int anc = -1, dep = 0, ok = 1;
     if (n < N) {
-        const Verdict v = verdict(st, a.ws_listpos[base + n], a.z, a.head_ran, a.lambda);
+        const Verdict v = verdict(st, a.ws_listpos[base + n], a.z, a.head_ran, a.lambda, a.policy_u,
+                                  base + n);
         if (n > 0) {
             anc = par;
             dep = 1;
@@ -150,6 +189,7 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
         if (a.z_tilde) a.z_tilde[base + n] = v.z_tilde;
         if (a.policy) a.policy[base + n] = v.policy;
         if (a.accept) a.accept[base + n] = n == 0 ? 1 : v.pass;
+        if (a.logp_action) a.logp_action[base + n] = n == 0 ? 0.0f : v.logp_action;
     }
     // pointer jumping: anc = ancestor 2^k steps up (or -1), dep = distance to it,
     // ok = every decision from this node up to (not including) anc passes

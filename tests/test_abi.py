@@ -129,13 +129,27 @@ def test_verify_block_sample_uniform_alignment():
     assert _block(L, feats=ctypes.byref(f)) == INVALID
 
 
+def test_rl_and_policy_uniform_arguments():
+    L = cs.lib()
+    assert _block(L, opts=ctypes.byref(binding._Options(policy_uniform=FAKE + 1))) == INVALID
+    rl = binding._RL(reward=FAKE)                                   # reward needs correct flags
+    assert _block(L, opts=ctypes.byref(binding._Options(rl=ctypes.pointer(rl)))) == INVALID
+    rl = binding._RL(correct=FAKE, rho=FAKE + 2)                    # misaligned output
+    assert _block(L, opts=ctypes.byref(binding._Options(rl=ctypes.pointer(rl)))) == INVALID
+    rl = binding._RL(correct=FAKE, reward=FAKE, alpha=1.0, beta=0.25)
+    assert _block(L, B=0, opts=ctypes.byref(binding._Options(rl=ctypes.pointer(rl)))) == OK
+    assert _tree(L, opts=ctypes.byref(binding._Options(rl=ctypes.pointer(rl)))) == INVALID
+
+
 def _tree(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
-             lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30)
+             lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30,
+             opts=None)
     a.update(kw)
     return L.cospec_verify_tree(a["tgt"], a["drf"], a["dt"], a["ld"], a["par"], a["toks"], a["hid"],
                                 ctypes.byref(a["head"]), a["lam"], a["B"], a["N"], a["V"],
-                                a["alen"], a["otok"], a["path"], None, None, a["ws"], a["wsb"], None)
+                                a["alen"], a["otok"], a["path"], None, a["opts"], a["ws"], a["wsb"],
+                                None)
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -518,3 +518,82 @@ def test_t1_greedy_path_unchanged_and_deterministic():
     for k in a:
         assert torch.equal(a[k], b[k]) or (a[k].dtype.is_floating_point and
                                            torch.equal(torch.nan_to_num(a[k]), torch.nan_to_num(b[k]))), k
+
+
+# ------------------------------------------------------------------ sampled arbitration and RL statistics
+
+def _policy_block(wl, lam, pu, correct=None, alpha=1.0, beta=0.25, **kw):
+    out = cs.verify_block(_padded(wl.target, 0), _padded(wl.draft, 0), wl.draft_tokens.to(DEV),
+                          wl.hidden.to(DEV), _head_dev(wl.head), lam, policy_u=pu.to(DEV),
+                          correct=None if correct is None else correct.to(DEV), alpha=alpha, beta=beta,
+                          **kw)
+    torch.cuda.synchronize()
+    return {k: v.cpu() for k, v in out.items()}
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_sampled_arbitration_and_rl_statistics(cfg):
+    wl = workloads.make_config(cfg)
+    pu = _uniforms((wl.B, wl.K), 200 + cfg)
+    correct = (torch.arange(wl.B) % 3 != 0).to(torch.uint8)
+    gpu = _policy_block(wl, 0.5, pu, correct)
+    ref = oracle.verify_block(_conv(wl.target), _conv(wl.draft), wl.draft_tokens.numpy(),
+                              _conv(wl.hidden), _head_np(wl.head), 0.5, policy_u=pu.double().numpy())
+    stats = parity.check_block(gpu, ref)
+    stats.update(parity.check_rl(gpu, ref, correct.numpy(), 1.0, 0.25))
+    _report(f"sampled arbitration + RL, config {cfg}", stats, gpu)
+    thr = _gpu_block(wl, 0.5)
+    assert not torch.equal(thr["accept"], gpu["accept"])          # the uniforms, not lambda, decide
+
+
+@pytest.mark.parametrize("lam", [0.5, 1.0, -1.0])
+def test_rl_statistics_under_threshold_policy(lam):
+    wl = workloads.make_chain(B=40, K=9, V=5003, d=64, h=32, seed=31, bias=True, noise=0.9)
+    correct = (torch.arange(wl.B) % 2).to(torch.uint8)
+    out = cs.verify_block(_padded(wl.target, 1), _padded(wl.draft, 1), wl.draft_tokens.to(DEV),
+                          wl.hidden.to(DEV), _head_dev(wl.head), lam, correct=correct.to(DEV),
+                          alpha=2.0, beta=0.5)
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in out.items()}
+    ref = _ref_block(wl, lam)
+    stats = parity.check_block(gpu, ref)
+    stats.update(parity.check_rl(gpu, ref, correct.numpy(), 2.0, 0.5))
+    _report(f"RL statistics, lambda {lam}", stats, gpu)
+    if lam >= 1.0:                       # always defer: rho = 0 on every round with a mismatch
+        has = gpu["rl_first_mismatch"] > 0
+        assert (gpu["rl_rho"][has] == 0).all()
+
+
+def test_rl_statistics_with_invalid_tokens_and_k_zero():
+    wl = workloads.make_chain(B=6, K=5, V=1000, d=64, h=32, seed=3, bias=True)
+    wl.draft_tokens[1, 2] = -7
+    wl.draft_tokens[4, 0] = 5000
+    correct = torch.tensor([0, 0, 1, 0, 0, 1], dtype=torch.uint8)
+    out = cs.verify_block(wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV),
+                          wl.hidden.to(DEV), _head_dev(wl.head), 0.3, correct=correct.to(DEV))
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in out.items()}
+    # an invalid token is a rejected mismatch: the stop, in S_rej, reward -beta
+    assert gpu["accept_len"][1] <= 3 and gpu["accept_len"][4] == 1
+    assert gpu["rl_first_reject"][4] == 1 and gpu["rl_reward"][4, 0] == pytest.approx(-0.25)
+    w0 = workloads.make_chain(B=3, K=0, V=256, d=64, h=32, seed=4, dtype="f32")
+    out = cs.verify_block(w0.target.to(DEV), w0.draft.to(DEV), w0.draft_tokens.to(DEV), w0.hidden.to(DEV),
+                          _head_dev(w0.head), 0.5, correct=torch.ones(3, dtype=torch.uint8, device=DEV))
+    torch.cuda.synchronize()
+    assert (out["rl_first_mismatch"].cpu() == 0).all() and (out["rl_first_reject"].cpu() == 1).all()
+    assert torch.isnan(out["rl_rho"].cpu()).all() and (out["rl_round_return"].cpu() == 0).all()
+
+
+def test_sampled_arbitration_on_trees():
+    tr = workloads.make_random_tree(B=5, N=60, V=3001, d=64, h=48, shape="random", seed=8, bias=True,
+                                    noise=0.5)
+    pu = _uniforms((tr.B, tr.N), 300)
+    out = cs.verify_tree(_padded(tr.target, 1), _padded(tr.draft, 1), tr.parent.to(DEV),
+                         tr.node_tokens.to(DEV), tr.hidden.to(DEV), _head_dev(tr.head), 0.5,
+                         policy_u=pu.to(DEV))
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in out.items()}
+    ref = oracle.verify_tree(_conv(tr.target), _conv(tr.draft), tr.parent.numpy(), tr.node_tokens.numpy(),
+                             _conv(tr.hidden), _head_np(tr.head), 0.5, policy_u=pu.double().numpy())
+    stats = parity.check_tree(gpu, ref)
+    _report("sampled arbitration, random trees", stats, gpu)
