@@ -189,6 +189,16 @@ typedef struct {
      */
     const float *policy_uniform;
     const cospec_rl *rl;      /* chain only: per-round RL statistics, or NULL      */
+    /*
+     * Packed arbitrator hidden states (for example one row per token of every
+     * sequence's input q, Section 3.3).  NULL: `hidden` is [B][K][d] (chain) or
+     * [B][N][d] (tree).  Otherwise `hidden` is [hidden_rows][d] and decision
+     * slot j of sequence b (chain: decision j+1; tree: node j) reads row
+     * hidden_row0[b] + j.  A mismatch whose row falls outside [0, hidden_rows)
+     * gets z = NaN and is rejected.
+     */
+    const int64_t *hidden_row0;
+    int64_t hidden_rows;
 } cospec_options;
 
 /* COSPEC_ABI_VERSION of the built library. */
@@ -231,6 +241,44 @@ cospec_status cospec_verify_block(const void *target_logits, const void *draft_l
                                   int32_t V, int32_t *accept_len, int32_t *out_tokens,
                                   const cospec_features *feats, const cospec_options *opts,
                                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The same chain step in two phases, for an arbitrator whose input needs the
+ * target's candidates: its input q (Section 3.3) holds the draft tokens next to
+ * the target's candidates ytilde_1..K, so its hidden states can only be
+ * computed once the target rows are reduced.
+ *
+ *  phase 1, cospec_verify_block_reduce: the vocabulary reductions, the
+ *    candidates, Delta and the mismatch list.  Writes `candidates` ([B][K+1]
+ *    int32: the argmax, or the temperature-1 sample, of every target row) and
+ *    the features computed there (per target row, delta, logp_tgt).
+ *  the caller builds q from the candidates and runs its arbitrator;
+ *  phase 2, cospec_verify_block_arbitrate: the head on the mismatch rows, the
+ *    verdicts, the first stop, the emission and the remaining features (per
+ *    draft row, logp_drf, z_tilde, policy, accept, logp_action, RL statistics).
+ *
+ * Both phases take the arguments of cospec_verify_block (phase 1 without
+ * hidden, lambda and the outputs) with the same values and workspace; the
+ * workspace must not be touched between them and phase 2 must be enqueued on a
+ * stream ordered after phase 1.  Of the options, phase 1 reads splits (which
+ * phase 2 must repeat) and sample_uniform; phase 2 reads policy_uniform, rl and
+ * the hidden-row map; aux_stream is not supported.  The two phases together
+ * give exactly the results of one cospec_verify_block call.
+ */
+cospec_status cospec_verify_block_reduce(const void *target_logits, const void *draft_logits,
+                                         cospec_dtype logit_dtype, int64_t ld,
+                                         const int32_t *draft_tokens, const cospec_head *head,
+                                         int32_t B, int32_t K, int32_t V, int32_t *candidates,
+                                         const cospec_features *feats, const cospec_options *opts,
+                                         void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+cospec_status cospec_verify_block_arbitrate(const void *target_logits, const void *draft_logits,
+                                            cospec_dtype logit_dtype, int64_t ld,
+                                            const int32_t *draft_tokens, const void *hidden,
+                                            const cospec_head *head, float lambda, int32_t B, int32_t K,
+                                            int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                            const cospec_features *feats, const cospec_options *opts,
+                                            void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Workspace bytes cospec_verify_tree needs (0 for invalid sizes). */
 size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const cospec_head *head);

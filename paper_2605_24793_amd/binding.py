@@ -16,7 +16,8 @@ import torch
 from . import _build
 
 __all__ = ["lib", "verify_block", "verify_tree", "arbitrate", "CospecError", "Prepared",
-           "prepare_block", "prepare_tree", "status_string", "MAX_K", "MAX_N", "MAX_SPLITS"]
+           "prepare_block", "prepare_tree", "SplitBlock", "status_string", "MAX_K", "MAX_N",
+           "MAX_SPLITS"]
 
 MAX_K, MAX_N, MAX_SPLITS = 64, 256, 64
 _F32, _BF16 = 0, 1
@@ -56,7 +57,8 @@ class _Options(ctypes.Structure):
                 ("splits", ctypes.c_int32), ("aux_stream", ctypes.c_void_p),
                 ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p),
                 ("sample_uniform", ctypes.c_void_p), ("policy_uniform", ctypes.c_void_p),
-                ("rl", ctypes.POINTER(_RL))]
+                ("rl", ctypes.POINTER(_RL)), ("hidden_row0", ctypes.c_void_p),
+                ("hidden_rows", ctypes.c_int64)]
 
 
 def _event_handle(ev) -> int:
@@ -93,6 +95,12 @@ def lib():
         L.cospec_verify_tree.argtypes = [P, P, I32, I64, P, P, P, HP, ctypes.c_float, I32, I32,
                                          I32, P, P, P, ctypes.POINTER(_Features),
                                          ctypes.POINTER(_Options), P, SZ, P]
+        L.cospec_verify_block_reduce.restype = I32
+        L.cospec_verify_block_reduce.argtypes = [P, P, I32, I64, P, HP, I32, I32, I32, P,
+                                                 ctypes.POINTER(_Features), ctypes.POINTER(_Options),
+                                                 P, SZ, P]
+        L.cospec_verify_block_arbitrate.restype = I32
+        L.cospec_verify_block_arbitrate.argtypes = L.cospec_verify_block.argtypes
         L.cospec_arbitrate.restype = I32
         L.cospec_arbitrate.argtypes = [P, I64, P, I64, HP, ctypes.c_float, P, P, P, SZ, P]
         _lib = L
@@ -362,3 +370,81 @@ def arbitrate(hidden, head, lam: float, row_index: Optional[torch.Tensor] = None
                               float(lam), _ptr(z), _ptr(acc), _ptr(ws), ws.numel(), _stream())
     _check(code, "cospec_arbitrate")
     return dict(z=z, accept=acc)
+
+
+class SplitBlock:
+    """The chain step in two phases around the caller's arbitrator
+    (cospec_verify_block_reduce, then cospec_verify_block_arbitrate).  Creating it
+    enqueues phase 1; `candidates` ([B, K+1] int32) then holds the target's
+    candidates the arbitrator's input needs; `arbitrate()` enqueues phase 2 on the
+    hidden states and returns the results of the whole step."""
+
+    def __init__(self, target, draft, draft_tokens, head, features: bool = True, splits: int = 0,
+                 sample_u: Optional[torch.Tensor] = None):
+        B, R, V = target.shape
+        K = R - 1
+        ld = _row_stride(target)
+        if K > 0 and (_row_stride(draft) != ld or tuple(draft.shape) != (B, K, V)
+                      or tuple(draft_tokens.shape) != (B, K) or draft_tokens.dtype != torch.int32
+                      or not draft_tokens.is_contiguous()):
+            raise ValueError("shape/dtype mismatch between target, draft and draft_tokens")
+        dev = target.device
+        self._hs = _head_struct(head)
+        L = lib()
+        ws_bytes = L.cospec_verify_block_workspace_size(B, K, V, ctypes.byref(self._hs))
+        if ws_bytes == 0 and B > 0:
+            raise CospecError("invalid sizes for cospec_verify_block_reduce")
+        self.workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self.candidates = torch.empty((B, K + 1), dtype=torch.int32, device=dev)
+        self.features, self._fst = _features(features, dev, B, K + 1, K, K)
+        self.splits = int(splits)
+        self._u = _uniforms(sample_u, B, K + 1)
+        self._common = (_ptr(target), _ptr(draft) if K > 0 else None, _dtype_code(target), ld,
+                        _ptr(draft_tokens) if K > 0 else None)
+        self._sizes = (B, K, V)
+        self._keep = [target, draft, draft_tokens, head]
+        opts = _Options(splits=self.splits, sample_uniform=_ptr(self._u))
+        code = L.cospec_verify_block_reduce(*self._common, ctypes.byref(self._hs), B, K, V,
+                                            _ptr(self.candidates),
+                                            ctypes.byref(self._fst) if self._fst is not None else None,
+                                            ctypes.byref(opts), _ptr(self.workspace),
+                                            self.workspace.numel(), _stream())
+        _check(code, "cospec_verify_block_reduce")
+
+    def arbitrate(self, hidden, lam: float, policy_u: Optional[torch.Tensor] = None,
+                  correct: Optional[torch.Tensor] = None, alpha: float = 1.0, beta: float = 0.25,
+                  hidden_row0: Optional[torch.Tensor] = None) -> dict:
+        """Phase 2.  hidden: [B, K, d], or with hidden_row0 (int64 [B]) a packed
+        [rows, d] array where decision i of sequence b reads row hidden_row0[b] + i - 1."""
+        B, K, V = self._sizes
+        dev = self.workspace.device
+        if not hidden.is_contiguous():
+            raise ValueError("hidden must be contiguous")
+        if hidden_row0 is not None:
+            if tuple(hidden_row0.shape) != (B,) or hidden_row0.dtype != torch.int64 or not hidden_row0.is_cuda:
+                raise ValueError("hidden_row0 must be an int64 device tensor [B]")
+            hidden_row0 = hidden_row0.contiguous()
+            n_hidden = hidden.reshape(-1, hidden.shape[-1]).shape[0]
+        elif K > 0 and tuple(hidden.shape[:2]) != (B, K):
+            raise ValueError("hidden must be [B, K, d] without hidden_row0")
+        outputs = dict(accept_len=torch.empty(B, dtype=torch.int32, device=dev),
+                       tokens=torch.empty((B, K + 1), dtype=torch.int32, device=dev))
+        pu = _policy_uniforms(policy_u, B, K)
+        rl = _rl(correct, alpha, beta, B, K, dev)
+        opts = _Options(splits=self.splits, policy_uniform=_ptr(pu),
+                        rl=None if rl is None else ctypes.pointer(rl[0]),
+                        hidden_row0=_ptr(hidden_row0),
+                        hidden_rows=n_hidden if hidden_row0 is not None else 0)
+        code = lib().cospec_verify_block_arbitrate(
+            *self._common, _ptr(hidden) if K > 0 else None, ctypes.byref(self._hs), float(lam), B, K, V,
+            _ptr(outputs["accept_len"]), _ptr(outputs["tokens"]),
+            ctypes.byref(self._fst) if self._fst is not None else None, ctypes.byref(opts),
+            _ptr(self.workspace), self.workspace.numel(), _stream())
+        _check(code, "cospec_verify_block_arbitrate")
+        out = dict(outputs)
+        out.update(self.features or {})
+        out["tgt_candidate"] = self.candidates
+        if rl is not None:
+            out.update({"rl_" + k: v for k, v in rl[1].items()})
+        self._keep += [hidden, pu, rl, hidden_row0]
+        return out

@@ -141,7 +141,12 @@ struct Common {
     hipStream_t stream;
 };
 
-cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int32_t *out_path) {
+// Which part of the step a call enqueues: the whole step, or one of the two
+// phases of the split form (reductions + decide, then head + finish).
+enum Phase { kWhole, kReducePhase, kArbitratePhase };
+
+cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *out_tokens,
+                  int32_t *out_path) {
     const int eb = elem_bytes(c.dt);
     const int64_t rows = static_cast<int64_t>(c.B) * (c.RT + c.RD);
     const int64_t nvec = static_cast<int64_t>(c.V) * eb / 16;
@@ -185,8 +190,12 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     const bool head = decisions && (!lambda_decides || want_scores || policy_u);
 
     const bool aux = c.opts && c.opts->aux_stream;
-    if (aux && (!c.opts->aux_ready || !c.opts->aux_done || c.opts->aux_stream == c.stream))
+    if (aux && (phase != kWhole || !c.opts->aux_ready || !c.opts->aux_done || c.opts->aux_stream == c.stream))
         return COSPEC_ERR_INVALID_ARG;
+    const int64_t *hidden_row0 = c.opts ? c.opts->hidden_row0 : nullptr;
+    const int64_t hidden_rows = hidden_row0 ? c.opts->hidden_rows : static_cast<int64_t>(c.B) * c.D;
+    if (hidden_row0 && (!aligned(hidden_row0, 8) || hidden_rows < 0)) return COSPEC_ERR_INVALID_ARG;
+    const bool do_reduce = phase != kArbitratePhase, do_arbitrate = phase != kReducePhase;
 
     ReduceArgs ra{};
     ra.tgt = static_cast<const char *>(c.tgt);
@@ -210,6 +219,7 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     // 1. target rows; the draft rows too in the same launch unless the head overlaps
     //    their reduction on the aux stream (one launch is cheaper than two)
     const bool split_reduce = aux && head;
+    if (do_reduce) {
     ReduceArgs rt = ra;
     rt.row_offset = 0;
     rt.n_rows = split_reduce ? ra.n_tgt_rows : static_cast<int32_t>(c.B * (c.RT + c.RD));
@@ -247,7 +257,7 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     da.tokens = c.tokens;
     da.partials = partials;
     da.splits = splits;
-    da.score_mismatch = head;
+    da.score_mismatch = phase == kReducePhase ? decisions : head;   // phase 2 may need the list
     da.sampled = uniform != nullptr;
     da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
     da.tgt_cand = F.tgt_candidate;
@@ -259,13 +269,17 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     da.ws_list = list;
     da.ws_count = count;
     if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+    }
+    if (!do_arbitrate) return COSPEC_OK;
 
     // 3. head, on the aux stream when given
     const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
     if (head) {
         HeadArgs ha{};
         ha.hidden = c.hidden;
-        ha.n_rows = m_cap;
+        ha.n_rows = hidden_rows;
+        ha.row0 = hidden_row0;
+        ha.slots = static_cast<int32_t>(c.D);
         ha.list = list;
         ha.count_dev = count;
         ha.count_host = 0;
@@ -289,7 +303,7 @@ cospec_status run(const Common &c, int32_t *accept_len, int32_t *out_tokens, int
     // 4. draft rows (features only), when they were not reduced with the target rows
     ReduceArgs rd = ra;
     rd.row_offset = ra.n_tgt_rows;
-    rd.n_rows = split_reduce ? static_cast<int32_t>(c.B * c.RD) : 0;
+    rd.n_rows = split_reduce ? static_cast<int32_t>(c.B * c.RD) : 0;   // only in a whole step
     rd.reset_counter = nullptr;
     if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
@@ -368,12 +382,12 @@ size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const 
     return layout(static_cast<int64_t>(B) * 2 * N, B, N, N, head, V).total;
 }
 
-cospec_status cospec_verify_block(const void *target_logits, const void *draft_logits,
-                                  cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
-                                  const void *hidden, const cospec_head *head, float lambda, int32_t B,
-                                  int32_t K, int32_t V, int32_t *accept_len, int32_t *out_tokens,
-                                  const cospec_features *feats, const cospec_options *opts, void *workspace,
-                                  size_t workspace_bytes, hipStream_t stream) {
+// Host-side checks of a chain call; fills `c` on success.
+cospec_status block_common(const void *target_logits, const void *draft_logits, cospec_dtype logit_dtype,
+                           int64_t ld, const int32_t *draft_tokens, const void *hidden, bool need_hidden,
+                           const cospec_head *head, float lambda, int32_t B, int32_t K, int32_t V,
+                           const cospec_features *feats, const cospec_options *opts, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream, Common &c) {
     if (!dtype_ok(logit_dtype) || B < 0 || K < 0 || V < 1 || isnan(lambda)) return COSPEC_ERR_INVALID_ARG;
     if (K > COSPEC_MAX_K) return COSPEC_ERR_UNSUPPORTED;
     cospec_status st = check_head(head);
@@ -382,19 +396,65 @@ cospec_status cospec_verify_block(const void *target_logits, const void *draft_l
     if ((st = check_logits(target_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
     if (K > 0) {
         if ((st = check_logits(draft_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
-        if (!draft_tokens || !aligned(draft_tokens, 4) || !hidden || !aligned(hidden, 16))
-            return COSPEC_ERR_INVALID_ARG;
+        if (!draft_tokens || !aligned(draft_tokens, 4)) return COSPEC_ERR_INVALID_ARG;
+        if (need_hidden && (!hidden || !aligned(hidden, 16))) return COSPEC_ERR_INVALID_ARG;
     }
-    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4) || !feats_aligned(feats))
-        return COSPEC_ERR_INVALID_ARG;
+    if (!feats_aligned(feats)) return COSPEC_ERR_INVALID_ARG;
     if (static_cast<int64_t>(B) * (2 * K + 1) > INT32_MAX / 2) return COSPEC_ERR_UNSUPPORTED;
-    Common c{};
     c.tgt = target_logits; c.drf = draft_logits; c.dt = logit_dtype; c.ld = ld;
     c.hidden = hidden; c.head = head; c.lambda = lambda; c.B = B; c.V = V;
     c.RT = K + 1; c.RD = K; c.D = K; c.is_tree = 0;
     c.parent = nullptr; c.tokens = draft_tokens;
     c.feats = feats; c.opts = opts; c.ws = workspace; c.ws_bytes = workspace_bytes; c.stream = stream;
-    return run(c, accept_len, out_tokens, nullptr);
+    return COSPEC_OK;
+}
+
+cospec_status cospec_verify_block(const void *target_logits, const void *draft_logits,
+                                  cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
+                                  const void *hidden, const cospec_head *head, float lambda, int32_t B,
+                                  int32_t K, int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                  const cospec_features *feats, const cospec_options *opts, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+    Common c{};
+    cospec_status st = block_common(target_logits, draft_logits, logit_dtype, ld, draft_tokens, hidden, true,
+                                    head, lambda, B, K, V, feats, opts, workspace, workspace_bytes, stream, c);
+    if (st != COSPEC_OK || B == 0) return st;
+    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4))
+        return COSPEC_ERR_INVALID_ARG;
+    return run(c, kWhole, accept_len, out_tokens, nullptr);
+}
+
+cospec_status cospec_verify_block_reduce(const void *target_logits, const void *draft_logits,
+                                         cospec_dtype logit_dtype, int64_t ld,
+                                         const int32_t *draft_tokens, const cospec_head *head,
+                                         int32_t B, int32_t K, int32_t V, int32_t *candidates,
+                                         const cospec_features *feats, const cospec_options *opts,
+                                         void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    Common c{};
+    cospec_status st = block_common(target_logits, draft_logits, logit_dtype, ld, draft_tokens, nullptr, false,
+                                    head, 0.5f, B, K, V, feats, opts, workspace, workspace_bytes, stream, c);
+    if (st != COSPEC_OK || B == 0) return st;
+    if (!candidates || !aligned(candidates, 4)) return COSPEC_ERR_INVALID_ARG;
+    cospec_features f = feats ? *feats : cospec_features{};
+    f.tgt_candidate = candidates;
+    c.feats = &f;
+    return run(c, kReducePhase, nullptr, nullptr, nullptr);
+}
+
+cospec_status cospec_verify_block_arbitrate(const void *target_logits, const void *draft_logits,
+                                            cospec_dtype logit_dtype, int64_t ld,
+                                            const int32_t *draft_tokens, const void *hidden,
+                                            const cospec_head *head, float lambda, int32_t B, int32_t K,
+                                            int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                            const cospec_features *feats, const cospec_options *opts,
+                                            void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    Common c{};
+    cospec_status st = block_common(target_logits, draft_logits, logit_dtype, ld, draft_tokens, hidden, true,
+                                    head, lambda, B, K, V, feats, opts, workspace, workspace_bytes, stream, c);
+    if (st != COSPEC_OK || B == 0) return st;
+    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4))
+        return COSPEC_ERR_INVALID_ARG;
+    return run(c, kArbitratePhase, accept_len, out_tokens, nullptr);
 }
 
 cospec_status cospec_verify_tree(const void *target_logits, const void *draft_logits,
@@ -423,7 +483,7 @@ cospec_status cospec_verify_tree(const void *target_logits, const void *draft_lo
     c.RT = N; c.RD = N; c.D = N; c.is_tree = 1;
     c.parent = parent; c.tokens = node_tokens;
     c.feats = feats; c.opts = opts; c.ws = workspace; c.ws_bytes = workspace_bytes; c.stream = stream;
-    return run(c, accept_len, out_tokens, out_path);
+    return run(c, kWhole, accept_len, out_tokens, out_path);
 }
 
 size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head) {

@@ -71,6 +71,13 @@ __device__ inline void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// Hidden row of list entry m (see HeadArgs::row0).
+__device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
+    int64_t id = a.list ? static_cast<int64_t>(a.list[m]) : m;
+    if (a.row0 && id >= 0) id = a.row0[id / a.slots] + id % a.slots;
+    return id;
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
@@ -110,8 +117,8 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
         lvec[i] = lslot ^ (row & 7);
         int64_t m = m_base + row;
         if (m >= M) m = M - 1;                     // garbage rows are computed, never stored
-        int64_t id = a.list ? static_cast<int64_t>(a.list[m]) : m;
-        if (id < 0 || id >= a.n_rows) id = 0;
+        int64_t id = hidden_row(a, m);
+        if (id < 0 || id >= a.n_rows) id = 0;     // its logit is set to NaN by the epilogue
         ga[i] = static_cast<const char *>(a.hidden) + id * static_cast<int64_t>(a.d) * EB;
         int n = n_base + row;
         if (n >= a.h) n = a.h - 1;
@@ -224,7 +231,10 @@ __global__ __launch_bounds__(256) void k_head_epilogue(HeadArgs a) {
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-    if (lane == 0) a.z[m] = acc + a.b2;
+    if (lane == 0) {
+        const int64_t id = hidden_row(a, m);
+        a.z[m] = id >= 0 && id < a.n_rows ? acc + a.b2 : NAN;
+    }
 }
 
 __global__ __launch_bounds__(256) void k_arb_finish(ArbFinishArgs a) {

@@ -84,6 +84,9 @@ struct HeadArgs {
     const void *hidden;        // [n_rows][d]
     int64_t n_rows;
     const int32_t *list;       // selected rows, or null = identity
+    const int64_t *row0;       // packed hidden states: entry e of the list reads row
+                               // row0[e / slots] + e % slots, or null (row e)
+    int32_t slots;
     const int32_t *count_dev;  // M on the device, or null
     int64_t count_host;        // M when count_dev is null
     int64_t m_cap;             // capacity of the list (rows of upart and z)

@@ -141,6 +141,27 @@ def test_rl_and_policy_uniform_arguments():
     assert _tree(L, opts=ctypes.byref(binding._Options(rl=ctypes.pointer(rl)))) == INVALID
 
 
+def test_split_phase_arguments():
+    L = cs.lib()
+    hd = _head()
+
+    def reduce(cand=FAKE, opts=None, toks=FAKE, B=4):
+        return L.cospec_verify_block_reduce(FAKE, FAKE, 1, 151936, toks, ctypes.byref(hd), B, 7, 151936,
+                                            cand, None, opts, FAKE, 1 << 30, None)
+    assert reduce(cand=None) == INVALID                        # candidates are required
+    assert reduce(cand=FAKE + 2) == INVALID
+    assert reduce(toks=None) == INVALID
+    assert reduce(B=0, cand=None) == OK
+    aux = binding._Options(aux_stream=FAKE, aux_ready=FAKE, aux_done=FAKE)
+    assert reduce(opts=ctypes.byref(aux)) == INVALID          # no second stream in the split form
+    # phase 2 checks like cospec_verify_block; a packed hidden map must be 8-byte aligned
+    a = L.cospec_verify_block_arbitrate
+    args = [FAKE, FAKE, 1, 151936, FAKE, FAKE, ctypes.byref(hd), 0.5, 4, 7, 151936, FAKE, FAKE, None]
+    assert a(*args, ctypes.byref(binding._Options(hidden_row0=FAKE + 4, hidden_rows=10)), FAKE, 1 << 30,
+             None) == INVALID
+    assert a(*args[:11], None, FAKE, None, None, FAKE, 1 << 30, None) == INVALID   # accept_len missing
+
+
 def _tree(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
              lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30,

@@ -597,3 +597,62 @@ def test_sampled_arbitration_on_trees():
                              _conv(tr.hidden), _head_np(tr.head), 0.5, policy_u=pu.double().numpy())
     stats = parity.check_tree(gpu, ref)
     _report("sampled arbitration, random trees", stats, gpu)
+
+
+# ------------------------------------------------------------------ split phases and packed hidden states
+
+def _same(a, b, keys):
+    for k in keys:
+        x, y = a[k].cpu(), b[k].cpu()
+        if x.dtype.is_floating_point:
+            assert torch.equal(torch.nan_to_num(x, nan=-7.0), torch.nan_to_num(y, nan=-7.0)), k
+        else:
+            assert torch.equal(x, y), k
+
+
+@pytest.mark.parametrize("t1", [False, True])
+def test_split_phases_equal_the_whole_step(t1):
+    wl = workloads.make_config(3, B=24)
+    u = _uniforms((wl.B, wl.K + 1), 61) if t1 else None
+    pu = _uniforms((wl.B, wl.K), 62)
+    corr = (torch.arange(wl.B) % 2).to(torch.uint8)
+    tgt, drf, tok = wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV)
+    head = _head_dev(wl.head)
+    whole = cs.verify_block(tgt, drf, tok, wl.hidden.to(DEV), head, 0.5, sample_u=None if u is None else u.to(DEV),
+                            policy_u=pu.to(DEV), correct=corr.to(DEV))
+    sb = cs.SplitBlock(tgt, drf, tok, head, sample_u=None if u is None else u.to(DEV))
+    torch.cuda.synchronize()
+    cand = sb.candidates.cpu()
+    assert torch.equal(cand, whole["tgt_candidate"].cpu())     # what the arbitrator's input needs
+    split = sb.arbitrate(wl.hidden.to(DEV), 0.5, policy_u=pu.to(DEV), correct=corr.to(DEV))
+    torch.cuda.synchronize()
+    _same(whole, split, [k for k in whole if k in split])
+
+
+def test_packed_hidden_rows():
+    wl = workloads.make_config(3, B=16)
+    B, K, d = wl.B, wl.K, wl.head.d
+    # each sequence's arbitrator input q = [context, SEP, draft 1..K, SEP, candidates, SEP]
+    # packed back to back; decision i reads the row of draft token i
+    g = torch.Generator().manual_seed(4)
+    ctx = torch.randint(3, 40, (B,), generator=g)
+    qlen = ctx + 2 * K + 3
+    start = torch.cumsum(qlen, 0) - qlen
+    packed = torch.randn(int(qlen.sum()), d, generator=g).to(wl.hidden.dtype)
+    row0 = start + ctx + 1
+    for b in range(B):
+        packed[row0[b]:row0[b] + K] = wl.hidden[b]
+    ref = _gpu_block(wl, 0.5)
+    sb = cs.SplitBlock(wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV), _head_dev(wl.head))
+    out = sb.arbitrate(packed.to(DEV), 0.5, hidden_row0=row0.to(DEV))
+    torch.cuda.synchronize()
+    _same(ref, out, ["accept_len", "tokens", "z_tilde", "accept", "policy"])
+    # a row outside the packed array: z = NaN and the mismatch is rejected
+    bad = row0.clone()
+    bad[3] = packed.shape[0] - 2                     # decisions 3.. of sequence 3 fall off the end
+    out = sb.arbitrate(packed.to(DEV), 0.5, hidden_row0=bad.to(DEV))
+    torch.cuda.synchronize()
+    zt, acc, delta = out["z_tilde"].cpu()[3], out["accept"].cpu()[3], out["delta"].cpu()[3]
+    for i in range(2, K):
+        if not delta[i]:
+            assert torch.isnan(zt[i]) and acc[i] == 0
