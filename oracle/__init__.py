@@ -44,11 +44,13 @@ __all__ = [
     "policy_accept", "chain_length", "chain_tokens", "tree_select", "verify_block",
     "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats", "sample_rows",
     "cdf_at", "candidates", "policy_sample", "action_logprob", "rl_round", "RL_ALPHA", "RL_BETA",
+    "residual_sample", "sps_block", "SPS_BAND",
 ]
 
 F32, BF16 = 0, 1
 AMBIGUITY_BAND = 1e-3
 RL_ALPHA, RL_BETA = 1.0, 0.25       # failure-reward weights the paper trains with (Appendix C.2)
+SPS_BAND = 1e-4                     # speculative-sampling tests closer than this to their uniform
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cospec_oracle.c")
@@ -79,6 +81,8 @@ def _load():
         lib.oracle_sample_rows.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
         lib.oracle_cdf_at.restype = I64
         lib.oracle_cdf_at.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P]
+        lib.oracle_residual_sample.restype = I64
+        lib.oracle_residual_sample.argtypes = [P, P, ctypes.c_int, I64, I64, I64, P, P, P, P, P, P]
         lib.oracle_head.restype = None
         lib.oracle_head.argtypes = [P, ctypes.c_int, I64, P, I64, P, P, P, ctypes.c_double, I64,
                                     I64, P]
@@ -172,6 +176,99 @@ def cdf_at(rows: np.ndarray, idx):
         if rc != 0:
             raise ValueError(f"non-finite logit in row {-rc - 1}")
     return lo.reshape(shape), hi.reshape(shape)
+
+
+def residual_sample(target_rows, draft_rows, u=None, query=None):
+    """Speculative sampling's resampling step for rows [n, V] (see
+    oracle_residual_sample): a sample of max(0, p_T - p_D) / Z by inversion of u,
+    or of p_T when draft_rows is None; with `query` the given candidates are
+    placed instead.  Returns (index, P(index-1), P(index)), P normalised by Z."""
+    t = np.ascontiguousarray(target_rows)
+    n, V = t.shape
+    d = None if draft_rows is None else np.ascontiguousarray(draft_rows)
+    if d is not None and (d.shape != t.shape or _code(d) != _code(t)):
+        raise TypeError("target and draft rows must share shape and dtype")
+    uu = np.ascontiguousarray(np.zeros(n) if u is None else np.asarray(u, np.float64).reshape(n))
+    qq = None if query is None else np.ascontiguousarray(np.asarray(query, np.int64).reshape(n))
+    idx = np.empty(n, np.int64) if query is None else qq.copy()
+    lo = np.empty(n, np.float64)
+    hi = np.empty(n, np.float64)
+    work = np.empty(2 * max(V, 1), np.float64)
+    if n:
+        rc = _load().oracle_residual_sample(_ptr(t), None if d is None else _ptr(d), _code(t), V, n, V,
+                                            _ptr(uu), None if qq is None else _ptr(qq), _ptr(work),
+                                            _ptr(idx), _ptr(lo), _ptr(hi))
+        if rc == -(n + 1):
+            raise IndexError("candidate index out of range")
+        if rc != 0:
+            raise ValueError(f"non-finite logit in row {-rc - 1}")
+    return idx, lo, hi
+
+
+def sps_block(target, draft, draft_tokens, u) -> dict:
+    """Standard speculative sampling over a chain block, the distribution-preserving
+    baseline the paper runs at T = 1 (Section 2, Appendix C.3).
+
+    target [B, K+1, V], draft [B, K, V], draft_tokens [B, K] (drawn from the draft),
+    u [B, K+1] uniforms.  Draft token i (rows i-1) is accepted when u[b, i-1] <
+    min(1, p_T(token) / p_D(token)); the round stops at the first rejection s and
+    emits draft tokens 1..s-1, then a sample of max(0, p_T - p_D) from rows s-1 by
+    inversion of u[b, K], or, with every token accepted (s = K+1), a sample of p_T
+    from target row K.  The test is taken in fp64; tests within SPS_BAND of their
+    uniform are flagged ambiguous, and `stops` lists every round length the
+    ambiguous tests allow.
+    """
+    B, K1, V = target.shape
+    K = K1 - 1
+    toks = np.asarray(draft_tokens, dtype=np.int64)
+    uu = np.asarray(u, dtype=np.float64)
+    if toks.size and (toks.min() < 0 or toks.max() >= V):
+        raise ValueError("draft token out of range")
+    ts = row_stats(target)
+    ds = row_stats(draft)
+    logp_t = _gather(target[:, :K, :], toks) - ts.lse[:, :K]
+    logp_d = _gather(draft, toks) - ds.lse
+    ratio = np.exp(logp_t - logp_d)
+    accept = uu[:, :K] < ratio
+    ambiguous = np.abs(uu[:, :K] - ratio) <= SPS_BAND
+    accept_len = np.empty(B, np.int64)
+    tokens = np.full((B, K + 1), -1, np.int64)
+    stops = []
+    for b in range(B):
+        s = K + 1
+        for i in range(1, K + 1):
+            if not accept[b, i - 1]:
+                s = i
+                break
+        accept_len[b] = s
+        tokens[b, : s - 1] = toks[b, : s - 1]
+        tokens[b, s - 1] = final_token(target[b], draft[b], s, uu[b, K])
+        possible, certain = set(), False
+        for i in range(1, K + 1):                  # the stop can be any ambiguous test before
+            if ambiguous[b, i - 1]:                # the first certain rejection
+                possible.add(i)
+            elif not accept[b, i - 1]:
+                possible.add(i)
+                certain = True
+                break
+        if not certain:
+            possible.add(K + 1)
+        stops.append(possible)
+    return dict(tgt_lse=ts.lse, drf_lse=ds.lse, logp_tgt=logp_t, logp_drf=logp_d, ratio=ratio,
+                accept=accept, ambiguous=ambiguous, accept_len=accept_len, tokens=tokens, stops=stops)
+
+
+def final_token(target_seq, draft_seq, s: int, u_last: float, query=None):
+    """The token a speculative-sampling round of length s emits last (see sps_block):
+    from the residual of rows s-1 when s <= K, from target row K when s = K+1.
+    With `query`, returns (P(query-1), P(query)) of that distribution instead."""
+    K = draft_seq.shape[0]
+    t = target_seq[s - 1: s]
+    d = draft_seq[s - 1: s] if s <= K else None
+    if query is None:
+        return int(residual_sample(t, d, [u_last])[0][0])
+    _, lo, hi = residual_sample(t, d, query=[query])
+    return float(lo[0]), float(hi[0])
 
 
 def candidates(target, stats: "RowStats", sample_u=None, override=None):

@@ -193,3 +193,69 @@ int64_t oracle_cdf_at(const void *rows, int dtype, int64_t ld, int64_t nrows, in
     }
     return 0;
 }
+
+/*
+ * Resampling step of standard speculative sampling (the distribution-preserving
+ * baseline the paper runs at T = 1, Section 2 and Appendix C.3).  With p = the
+ * softmax of a target row and q = the softmax of the draft row at the same
+ * position, the residual distribution is max(0, p - q) / Z, Z = sum_v max(0,
+ * p[v] - q[v]); with no draft row (drf == NULL) the distribution is p itself
+ * (the bonus token after K accepted draft tokens).  For row r:
+ *   query == NULL: inversion of u[r]: the smallest v whose cumulative weight
+ *                  exceeds u[r] * Z (the last v of positive weight if rounding
+ *                  leaves none); writes it to out_idx[r];
+ *   query != NULL: the candidate is query[r].
+ * out_lo[r], out_hi[r] = the normalised cumulative weight before and at the
+ * candidate.  `work` holds 2 V doubles.  Returns 0, -(r+1) for a non-finite
+ * entry in row r, or -(nrows+1) for a query outside [0, V).
+ */
+int64_t oracle_residual_sample(const void *tgt, const void *drf, int dtype, int64_t ld, int64_t nrows,
+                               int64_t V, const double *u, const int64_t *query, double *work,
+                               int64_t *out_idx, double *out_lo, double *out_hi)
+{
+    size_t esz = dtype == ORACLE_F32 ? 4 : 2;
+    double *p = work, *q = work + V;
+    for (int64_t r = 0; r < nrows; ++r) {
+        const void *trow = (const char *)tgt + (size_t)r * (size_t)ld * esz;
+        if (oracle_softmax_row(trow, dtype, V, p))
+            return -(r + 1);
+        if (drf) {
+            const void *drow = (const char *)drf + (size_t)r * (size_t)ld * esz;
+            if (oracle_softmax_row(drow, dtype, V, q))
+                return -(r + 1);
+            for (int64_t v = 0; v < V; ++v)
+                p[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;
+        }
+        double z = 0.0;
+        for (int64_t v = 0; v < V; ++v)
+            z += p[v];
+        int64_t pick;
+        if (query) {
+            if (query[r] < 0 || query[r] >= V)
+                return -(nrows + 1);
+            pick = query[r];
+        } else {
+            double target = u[r] * z, cum = 0.0;
+            int64_t last = 0;
+            pick = -1;
+            for (int64_t v = 0; v < V; ++v) {
+                if (p[v] > 0.0)
+                    last = v;
+                cum += p[v];
+                if (p[v] > 0.0 && cum > target) {
+                    pick = v;
+                    break;
+                }
+            }
+            if (pick < 0)
+                pick = last;
+            out_idx[r] = pick;
+        }
+        double before = 0.0;
+        for (int64_t v = 0; v < pick; ++v)
+            before += p[v];
+        out_lo[r] = before / z;
+        out_hi[r] = (before + p[pick]) / z;
+    }
+    return 0;
+}

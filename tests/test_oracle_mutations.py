@@ -34,7 +34,8 @@ MUTATIONS = [
      "tokens[b] = chain_tokens(s, toks[b], ts.arg[b])"),                        # emits the argmax at T = 1
     ("cospec_oracle.c", "p[v] = exp(oracle_elem(row, dtype, v) - lse);",
      "p[v] = exp(oracle_elem(row, dtype, v));"),                                # unnormalised probabilities
-    ("cospec_oracle.c", "pick = v;\n", "pick = v + 1 < V ? v + 1 : v;\n"),     # one past the crossing
+    ("cospec_oracle.c", "if (at > u[r]) {\n                pick = v;",
+     "if (at > u[r]) {\n                pick = v + 1 < V ? v + 1 : v;"),         # one past the crossing
     ("cospec_oracle.c", "at = before + work[v];", "at = work[v];"),              # not cumulative
     ("__init__.py", "if i <= min(s, K):", "if i < min(s, K):"),                  # drops the stopping decision
     ("__init__.py", "rho = (s - i_star) / ((K + 1) - i_star)", "rho = (s - i_star) / (K - i_star + 1e-9)"),
@@ -42,6 +43,9 @@ MUTATIONS = [
      "s_acc[i - 1] = i <= i_rej"),                                            # rejected one in S_acc
     ("__init__.py", "- beta * s_rej[i - 1])", "+ beta * s_rej[i - 1])"),        # rejection rewarded
     ("__init__.py", "accept = u32 < pi32", "accept = u32 <= pi32"),
+    ("cospec_oracle.c", "p[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;", "p[v] = p[v] - q[v];"),   # unclipped residual
+    ("__init__.py", "accept = uu[:, :K] < ratio", "accept = uu[:, :K] < 1.0 / ratio"),        # inverted ratio
+    ("__init__.py", "t = target_seq[s - 1: s]", "t = target_seq[s - 2: s - 1]"),           # resample wrong row
     ("__init__.py", "logp_tgt = _gather(target[:, :K, :], toks)", "logp_tgt = _gather(target[:, 1:, :], toks)"),
     ("__init__.py", "if ok[n] and depth[n] > depth[best]:", "if ok[n] and depth[n] >= depth[best]:"),
     ("__init__.py", "accept = pi32 > lam32", "accept = pi32 >= lam32"),        # non-strict threshold

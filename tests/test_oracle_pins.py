@@ -625,3 +625,78 @@ def test_verify_block_sampled_policy_and_rl():
     # sampled actions differ from the lambda = 0.5 threshold somewhere
     r2 = oracle.verify_block(t, d, toks, hid, head, 0.5)
     assert (r["accept"] != r2["accept"]).any()
+
+
+# ---------------------------------------------------------------- speculative sampling baseline
+
+def _logits_of(p):
+    return np.log(np.asarray(p, np.float64)).astype(np.float32)
+
+
+def test_sps_preserves_the_target_distribution():
+    # the defining property of speculative sampling: with the draft token drawn from
+    # p_D, the first emitted token is distributed as p_T.  Weight each draft token
+    # by p_D and sweep both uniforms over an n x n grid.
+    rng = np.random.default_rng(17)
+    V, n = 6, 64
+    t_logit = (rng.normal(size=V) * 1.5).astype(np.float32)
+    d_logit = (rng.normal(size=V) * 1.5).astype(np.float32)
+    pT = scipy.special.softmax(t_logit.astype(np.float64))
+    pD = scipy.special.softmax(d_logit.astype(np.float64))
+    g = (np.arange(n) + 0.5) / n
+    ua, ur = np.meshgrid(g, g, indexing="ij")
+    m = n * n
+    dist = np.zeros(V)
+    for y in range(V):
+        target = np.tile(t_logit, (m, 2, 1))
+        draft = np.tile(d_logit, (m, 1, 1))
+        toks = np.full((m, 1), y)
+        u = np.stack([ua.ravel(), ur.ravel()], axis=1)
+        r = oracle.sps_block(target, draft, toks, u)
+        first = r["tokens"][:, 0]
+        dist += pD[y] * np.bincount(first, minlength=V) / m
+    assert np.abs(dist - pT).max() <= 2.0 / n
+
+
+def test_sps_equal_models_accept_everything():
+    rng = np.random.default_rng(3)
+    B, K, V = 5, 4, 50
+    x = (rng.normal(size=(B, K + 1, V)) * 2).astype(np.float32)
+    toks = rng.integers(0, V, size=(B, K))
+    u = rng.random((B, K + 1)) * 0.999
+    r = oracle.sps_block(x, x[:, :K].copy(), toks, u)
+    assert (r["accept_len"] == K + 1).all()
+    np.testing.assert_allclose(r["ratio"], 1.0, rtol=1e-12)
+    cdf = np.cumsum(scipy.special.softmax(x[:, K].astype(np.float64), axis=-1), axis=-1)
+    for b in range(B):                      # the bonus token: inversion of p_T from row K
+        assert r["tokens"][b, K] == np.searchsorted(cdf[b], u[b, K], side="right")
+        assert list(r["tokens"][b, :K]) == list(toks[b])
+
+
+def test_sps_residual_closed_form():
+    pT = [0.5, 0.3, 0.2]
+    pD = [0.2, 0.5, 0.3]
+    target = np.stack([_logits_of(pT), _logits_of(pT)])[None]     # K = 1
+    draft = _logits_of(pD)[None, None]
+    # token 1: ratio 0.3 / 0.5 = 0.6.  u = 0.7 rejects it; the residual max(0, pT - pD)
+    # = (0.3, 0, 0) puts everything on token 0, whatever the second uniform
+    for u2 in (0.0, 0.5, 0.999):
+        r = oracle.sps_block(target, draft, np.array([[1]]), np.array([[0.7, u2]]))
+        assert r["accept_len"][0] == 1 and r["tokens"][0, 0] == 0
+        assert r["ratio"][0, 0] == pytest.approx(0.6, rel=1e-6)
+    r = oracle.sps_block(target, draft, np.array([[1]]), np.array([[0.5, 0.9]]))
+    assert r["accept_len"][0] == 2 and r["tokens"][0, 0] == 1      # accepted: bonus from p_T
+    assert r["tokens"][0, 1] == 2                                  # 0.9 > 0.5 + 0.3
+    # token 0: ratio 0.5 / 0.2 > 1, accepted for every u < 1
+    r = oracle.sps_block(target, draft, np.array([[0]]), np.array([[0.999, 0.1]]))
+    assert r["accept_len"][0] == 2
+
+
+def test_sps_ambiguous_stops():
+    pT = [0.5, 0.3, 0.2]
+    pD = [0.2, 0.5, 0.3]
+    target = np.tile(_logits_of(pT), (1, 3, 1))
+    draft = np.tile(_logits_of(pD), (1, 2, 1))
+    r = oracle.sps_block(target, draft, np.array([[1, 0]]), np.array([[0.6, 0.2, 0.4]]))
+    assert r["ambiguous"][0, 0] == (abs(0.6 - r["ratio"][0, 0]) <= oracle.SPS_BAND)
+    assert r["stops"][0] == ({1, 3} if r["ambiguous"][0, 0] else {r["accept_len"][0]})
