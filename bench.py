@@ -11,7 +11,8 @@ of the dominant kernel (the vocabulary reduction, timed with HIP events on the
 stream it runs on), and the CPU oracle timed on a bounded sample of the same
 workload on this host, with a parity re-check of the timed outputs.
 `--sample` times the temperature-1 variant (candidates sampled by inversion of
-seeded uniforms) instead of the greedy one.
+seeded uniforms) instead of the greedy one; `--sps` times the standard
+speculative-sampling baseline on the same workload.
 """
 from __future__ import annotations
 
@@ -56,6 +57,9 @@ def parse():
     ap.add_argument("--sample", action="store_true",
                     help="temperature-1 target candidates (inversion of seeded uniforms) instead "
                          "of the greedy argmax")
+    ap.add_argument("--sps", action="store_true",
+                    help="time the standard speculative-sampling baseline (chain workloads) instead "
+                         "of the CoSpec step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     return ap.parse_args()
@@ -87,6 +91,12 @@ def main():
         R = wl.N if tree else wl.K + 1
         u_host = torch.rand((wl.B, R), generator=torch.Generator().manual_seed(2024))
     u_dev = None if u_host is None else u_host.to(dev)
+    sps_u = None
+    if args.sps:
+        if tree:
+            print(json.dumps({"error": "--sps runs on chain workloads"}))
+            sys.exit(2)
+        sps_u = torch.rand((wl.B, wl.K + 1), generator=torch.Generator().manual_seed(2025))
     if tree:
         par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
         p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
@@ -100,8 +110,11 @@ def main():
         reduced_rows = rows + int(internal.sum())
     else:
         tok = wl.draft_tokens.to(dev)
-        p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
-                             overlap=args.overlap, sample_u=u_dev)
+        if args.sps:
+            p = cs.prepare_sps(tgt, drf, tok, sps_u.to(dev), features=True, splits=args.splits)
+        else:
+            p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
+                                 overlap=args.overlap, sample_u=u_dev)
         rows = wl.B * (wl.K + 1)
         reduced_rows = wl.B * (2 * wl.K + 1)
     elem = tgt.element_size()
@@ -171,7 +184,10 @@ def main():
             sub = wl.take(seqs)
             us = None if u_host is None else u_host[seqs].double().numpy()
             c0 = time.perf_counter()
-            if tree:
+            if args.sps:
+                ref = oracle.sps_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                       sps_u[seqs].double().numpy())
+            elif tree:
                 ref = oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
                                          sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam,
                                          sample_u=us)
@@ -180,6 +196,11 @@ def main():
                                           conv(sub.hidden), head_np, lam, sample_u=us)
             spent += time.perf_counter() - c0
             gsub = {k: v[seqs] for k, v in out.items()}
+            if args.sps:
+                parity.check_sps(gsub, ref, conv(sub.target), conv(sub.draft), sps_u[seqs].double().numpy())
+                checked += len(seqs)
+                done += len(seqs)
+                continue
             if us is not None:
                 # candidates at a cumulative boundary may differ; the check validates
                 # them and the rest of the step is compared on the GPU's candidates
@@ -215,14 +236,15 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
                    "splits": args.splits or "auto", "head_overlap": args.overlap,
-                   "temperature": 1 if args.sample else 0,
+                   "temperature": 1 if args.sample or args.sps else 0,
+                   "rule": "speculative sampling" if args.sps else "cospec",
                    "rows_per_step": rows,
                    "reduced_rows_per_step": reduced_rows},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
                                  if args.config == 4 and not args.splits and not args.sample
-                                 else None),
+                                 and not args.sps else None),
                      "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
                      "event_interval_ms": k_raw, "empty_event_interval_ms": ev_overhead,
                      "launches_per_step": launches, "algorithmic_bytes_per_launch": launch_bytes},

@@ -280,6 +280,36 @@ cospec_status cospec_verify_block_arbitrate(const void *target_logits, const voi
                                             const cospec_features *feats, const cospec_options *opts,
                                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Standard speculative sampling over B chain blocks: the distribution-
+ * preserving baseline the paper compares against at temperature 1 (Section 2,
+ * Appendix C.3), on the same reductions.  Draft token i (drawn by the caller
+ * from draft row i-1) is accepted when uniforms[b][i-1] < p_T(token) /
+ * p_D(token) (target and draft rows i-1), i.e. with probability min(1, ratio);
+ * the round stops at the first rejection s and emits draft tokens 1..s-1, then
+ * a sample of max(0, p_T - p_D) (normalised) from rows s-1, or, when all K are
+ * accepted, a sample of p_T from target row K; that sample inverts
+ * uniforms[b][K] through the distribution's cumulative weights in index order.
+ *
+ *  uniforms   [B][K+1] float in [0, 1) (device).
+ *  accept_len [B] out: s in [1, K+1]; out_tokens [B][K+1] out, -1 after s.
+ *  feats      optional: per target row and per draft row statistics, logp_tgt,
+ *             logp_drf, accept, and `policy` = min(1, ratio), the acceptance
+ *             probability (the other members are not written).
+ *  opts       only splits and the four reduction events apply (the second
+ *             pair is recorded back to back); any other member is an error.
+ * Sums are fp32: a uniform within about 1e-5 (tests: 1e-4) of a boundary may
+ * land on the neighbouring outcome.  An invalid draft token is rejected.
+ */
+size_t cospec_verify_block_sps_workspace_size(int32_t B, int32_t K, int32_t V);
+
+cospec_status cospec_verify_block_sps(const void *target_logits, const void *draft_logits,
+                                      cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
+                                      const float *uniforms, int32_t B, int32_t K, int32_t V,
+                                      int32_t *accept_len, int32_t *out_tokens, const cospec_features *feats,
+                                      const cospec_options *opts, void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
 /* Workspace bytes cospec_verify_tree needs (0 for invalid sizes). */
 size_t cospec_verify_tree_workspace_size(int32_t B, int32_t N, int32_t V, const cospec_head *head);
 

@@ -205,3 +205,50 @@ def check_rl(gpu: dict, ref: dict, correct, alpha: float, beta: float) -> dict:
     _close("rl_reward", gpu["rl_reward"], g, "logp", stats)
     _close("rl_return", gpu["rl_round_return"], J, "logp", stats)
     return stats
+
+
+def check_sps(gpu: dict, ref: dict, target, draft, u) -> dict:
+    """GPU result of cospec_verify_block_sps against oracle.sps_block: acceptance
+    tests outside SPS_BAND bit-exact, the round length one the ambiguous tests allow,
+    the draft prefix exact, and the last token inside its interval of the
+    distribution it is drawn from (residual or target row), up to CDF_TOL plus the
+    fp32 cancellation of p_T - p_D relative to the residual's total weight."""
+    from . import final_token, element, SPS_BAND  # noqa: F401
+    stats = {}
+    acc = _np(gpu["accept"]).astype(bool)
+    firm = ~ref["ambiguous"]
+    _exact("sps accept", acc, ref["accept"], firm)
+    s = _np(gpu["accept_len"]).astype(np.int64)
+    tok = _np(gpu["tokens"]).astype(np.int64)
+    B, K1 = tok.shape
+    K = K1 - 1
+    u = np.asarray(u, np.float64)
+    worst = 0.0
+    for b in range(B):
+        if int(s[b]) not in ref["stops"][b]:
+            raise ParityError(f"sequence {b}: round length {s[b]} not among {sorted(ref['stops'][b])}")
+        toks_in = np.asarray(ref["tokens"][b])
+        if s[b] == ref["accept_len"][b] and not np.array_equal(tok[b, : s[b] - 1], toks_in[: s[b] - 1]):
+            raise ParityError(f"sequence {b}: draft prefix differs")
+        if (tok[b, s[b]:] != -1).any():
+            raise ParityError(f"sequence {b}: tokens after the round are not -1")
+        lo, hi = final_token(target[b], draft[b], int(s[b]), u[b, K], query=int(tok[b, s[b] - 1]))
+        if s[b] <= K:
+            pt = np.exp(element(target[b, s[b] - 1]) - ref["tgt_lse"][b, s[b] - 1])
+            pd = np.exp(element(draft[b, s[b] - 1]) - ref["drf_lse"][b, s[b] - 1])
+            z = np.maximum(pt - pd, 0.0).sum()
+        else:
+            z = 1.0
+        tol = CDF_TOL + 3e-6 / z
+        if not (lo - tol <= u[b, K] < hi + tol):
+            raise ParityError(f"sequence {b}: last token {tok[b, s[b] - 1]} does not invert u={u[b, K]!r}: "
+                              f"interval [{lo!r}, {hi!r}), tolerance {tol:.1e}")
+        worst = max(worst, max(lo - u[b, K], u[b, K] - hi, 0.0))
+    stats["last_token_interval_excess"] = worst
+    _close("tgt_lse", gpu["tgt_lse"], ref["tgt_lse"], "lse", stats)
+    _close("drf_lse", gpu["drf_lse"], ref["drf_lse"], "lse", stats)
+    _close("logp_tgt", gpu["logp_tgt"], ref["logp_tgt"], "logp", stats)
+    _close("logp_drf", gpu["logp_drf"], ref["logp_drf"], "logp", stats)
+    _close("accept_prob", gpu["policy"], np.minimum(ref["ratio"], 1.0), "pi", stats)
+    stats["ambiguous_decisions"] = int(ref["ambiguous"].sum())
+    return stats

@@ -16,8 +16,9 @@ import torch
 from . import _build
 
 __all__ = ["lib", "verify_block", "verify_tree", "arbitrate", "CospecError", "Prepared",
-           "prepare_block", "prepare_tree", "SplitBlock", "status_string", "MAX_K", "MAX_N",
-           "MAX_SPLITS"]
+           "prepare_block", "prepare_tree", "prepare_sps", "SplitBlock", "sps_block", "status_string",
+           "MAX_K",
+           "MAX_N", "MAX_SPLITS"]
 
 MAX_K, MAX_N, MAX_SPLITS = 64, 256, 64
 _F32, _BF16 = 0, 1
@@ -101,6 +102,12 @@ def lib():
                                                  P, SZ, P]
         L.cospec_verify_block_arbitrate.restype = I32
         L.cospec_verify_block_arbitrate.argtypes = L.cospec_verify_block.argtypes
+        L.cospec_verify_block_sps_workspace_size.restype = SZ
+        L.cospec_verify_block_sps_workspace_size.argtypes = [I32, I32, I32]
+        L.cospec_verify_block_sps.restype = I32
+        L.cospec_verify_block_sps.argtypes = [P, P, I32, I64, P, P, I32, I32, I32, P, P,
+                                              ctypes.POINTER(_Features), ctypes.POINTER(_Options), P,
+                                              SZ, P]
         L.cospec_arbitrate.restype = I32
         L.cospec_arbitrate.argtypes = [P, I64, P, I64, HP, ctypes.c_float, P, P, P, SZ, P]
         _lib = L
@@ -448,3 +455,44 @@ class SplitBlock:
             out.update({"rl_" + k: v for k, v in rl[1].items()})
         self._keep += [hidden, pu, rl, hidden_row0]
         return out
+
+
+def prepare_sps(target, draft, draft_tokens, uniforms, features: bool = True,
+                splits: int = 0) -> Prepared:
+    """Pre-marshalled cospec_verify_block_sps (standard speculative sampling over
+    chain blocks).  uniforms: float32 [B, K+1] on the device (K acceptance tests,
+    then the draw of the last token).  The result holds accept_len, tokens and the
+    features; `policy` holds the acceptance probabilities min(1, p_T / p_D)."""
+    B, R, V = target.shape
+    K = R - 1
+    ld = _row_stride(target)
+    if K > 0 and (_row_stride(draft) != ld or tuple(draft.shape) != (B, K, V)
+                  or tuple(draft_tokens.shape) != (B, K) or draft_tokens.dtype != torch.int32
+                  or not draft_tokens.is_contiguous()):
+        raise ValueError("shape/dtype mismatch between target, draft and draft_tokens")
+    u = _uniforms(uniforms, B, K + 1)
+    if u is None:
+        raise ValueError("speculative sampling needs uniforms [B, K+1]")
+    dev = target.device
+    L = lib()
+    ws = torch.empty(max(L.cospec_verify_block_sps_workspace_size(B, K, V), 256), dtype=torch.uint8,
+                     device=dev)
+    outputs = dict(accept_len=torch.empty(B, dtype=torch.int32, device=dev),
+                   tokens=torch.empty((B, K + 1), dtype=torch.int32, device=dev))
+    feats, fst = _features(features, dev, B, K + 1, K, K)
+    unwritten = {}
+    if feats is not None:        # members the baseline leaves untouched (kept alive: fst points at them)
+        unwritten = {k: feats.pop(k) for k in ("z_tilde", "logp_action")}
+    args = (_ptr(target), _ptr(draft) if K > 0 else None, _dtype_code(target), ld,
+            _ptr(draft_tokens) if K > 0 else None, _ptr(u), B, K, V, _ptr(outputs["accept_len"]),
+            _ptr(outputs["tokens"]))
+    p = Prepared(L.cospec_verify_block_sps, args, outputs, feats, fst, ws, splits, False)
+    p._keep = [target, draft, draft_tokens, u, unwritten]
+    return p
+
+
+def sps_block(target, draft, draft_tokens, uniforms, features: bool = True, splits: int = 0) -> dict:
+    """cospec_verify_block_sps on device tensors (see prepare_sps)."""
+    p = prepare_sps(target, draft, draft_tokens, uniforms, features, splits)
+    p.launch()
+    return p.result()

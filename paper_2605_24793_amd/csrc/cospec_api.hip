@@ -54,7 +54,7 @@ cospec_status check_head(const cospec_head *hd) {
 }
 
 inline int32_t ksplit_for(int64_t m_cap, const cospec_head *hd) {
-    return head_ksplit(m_cap, hd->d, hd->h, elem_bytes(hd->dtype));
+    return hd ? head_ksplit(m_cap, hd->d, hd->h, elem_bytes(hd->dtype)) : 0;   // no head: no scratch
 }
 
 // Head scratch: k-slice partial pre-activations and the logits.
@@ -97,8 +97,8 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     L.count = off;    off += kAlign;
     L.logp = off;     off += round_up(static_cast<size_t>(B * D) * 4);
     const int64_t m_cap = B * D;
-    L.upart = off;    off += round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
-                                      static_cast<size_t>(hd->h) * 4);
+    L.upart = off;    off += hd ? round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
+                                           static_cast<size_t>(hd->h) * 4) : 0;
     L.z = off;        off += round_up(static_cast<size_t>(m_cap) * 4);
     L.total = off;
     return L;
@@ -455,6 +455,95 @@ cospec_status cospec_verify_block_arbitrate(const void *target_logits, const voi
     if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4))
         return COSPEC_ERR_INVALID_ARG;
     return run(c, kArbitratePhase, accept_len, out_tokens, nullptr);
+}
+
+size_t cospec_verify_block_sps_workspace_size(int32_t B, int32_t K, int32_t V) {
+    if (B < 0 || K < 0 || K > COSPEC_MAX_K || V < 1) return 0;
+    return layout(static_cast<int64_t>(B) * (2 * K + 1), B, K + 1, K, nullptr, V).total;
+}
+
+cospec_status cospec_verify_block_sps(const void *target_logits, const void *draft_logits,
+                                      cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
+                                      const float *uniforms, int32_t B, int32_t K, int32_t V,
+                                      int32_t *accept_len, int32_t *out_tokens, const cospec_features *feats,
+                                      const cospec_options *opts, void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+    if (!dtype_ok(logit_dtype) || B < 0 || K < 0 || V < 1) return COSPEC_ERR_INVALID_ARG;
+    if (K > COSPEC_MAX_K) return COSPEC_ERR_UNSUPPORTED;
+    if (B == 0) return COSPEC_OK;
+    cospec_status st;
+    if ((st = check_logits(target_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+    if (K > 0) {
+        if ((st = check_logits(draft_logits, logit_dtype, ld, V)) != COSPEC_OK) return st;
+        if (!draft_tokens || !aligned(draft_tokens, 4)) return COSPEC_ERR_INVALID_ARG;
+    }
+    if (!uniforms || !aligned(uniforms, 4) || !accept_len || !aligned(accept_len, 4) || !out_tokens ||
+        !aligned(out_tokens, 4) || !feats_aligned(feats))
+        return COSPEC_ERR_INVALID_ARG;
+    if (opts && (opts->aux_stream || opts->sample_uniform || opts->policy_uniform || opts->rl || opts->hidden_row0))
+        return COSPEC_ERR_INVALID_ARG;                  // only splits and the timing events apply
+    if (static_cast<int64_t>(B) * (2 * K + 1) > INT32_MAX / 2) return COSPEC_ERR_UNSUPPORTED;
+    const int eb = elem_bytes(logit_dtype);
+    const int64_t rows = static_cast<int64_t>(B) * (2 * K + 1);
+    const int64_t nvec = static_cast<int64_t>(V) * eb / 16;
+    int32_t splits = auto_splits(rows, nvec);
+    if (opts && opts->splits) {
+        if (opts->splits < 0 || opts->splits > COSPEC_MAX_SPLITS) return COSPEC_ERR_UNSUPPORTED;
+        splits = opts->splits;
+    }
+    const Layout L = layout(rows, B, K + 1, K, nullptr, V);
+    if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    if (!workspace || !aligned(workspace, kAlign) || workspace_bytes < L.total) return COSPEC_ERR_WORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    float4 *partials = reinterpret_cast<float4 *>(ws + L.partials);
+    const cospec_features F = feats ? *feats : cospec_features{};
+    const Dtype dt = static_cast<Dtype>(logit_dtype);
+
+    ReduceArgs ra{};
+    ra.tgt = static_cast<const char *>(target_logits);
+    ra.drf = static_cast<const char *>(draft_logits);
+    ra.ld_bytes = ld * eb;
+    ra.V = V;
+    ra.n_tgt_rows = B * (K + 1);
+    ra.row_offset = 0;
+    ra.n_rows = static_cast<int32_t>(rows);
+    ra.splits = splits;
+    ra.vec_per_split = static_cast<int32_t>((nvec + splits - 1) / splits);
+    ra.partials = partials;
+    ra.reset_counter = reinterpret_cast<int32_t *>(ws + L.count);
+    if (opts && opts->reduce_begin && hipEventRecord(opts->reduce_begin, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    if (launch_reduce(dt, ra, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    if (opts && opts->reduce_end && hipEventRecord(opts->reduce_end, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    // no second reduction launch here: the second pair brackets nothing, as in a whole step
+    if (opts && opts->reduce2_begin && hipEventRecord(opts->reduce2_begin, stream) != hipSuccess)
+        return COSPEC_ERR_HIP;
+    if (opts && opts->reduce2_end && hipEventRecord(opts->reduce2_end, stream) != hipSuccess) return COSPEC_ERR_HIP;
+
+    DecideArgs da{};
+    da.tgt = ra.tgt; da.ld_bytes = ra.ld_bytes; da.V = V; da.B = B; da.RT = K + 1; da.D = K;
+    da.tokens = draft_tokens; da.partials = partials; da.splits = splits;
+    da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
+    da.tgt_cand = F.tgt_candidate; da.logp_tgt = F.logp_tgt; da.delta = F.delta;
+    da.ws_tgt_arg = reinterpret_cast<int32_t *>(ws + L.tgt_arg);
+    da.ws_logp_tgt = reinterpret_cast<float *>(ws + L.logp);
+    da.ws_state = reinterpret_cast<uint8_t *>(ws + L.state);
+    da.ws_listpos = reinterpret_cast<int32_t *>(ws + L.listpos);
+    da.ws_list = reinterpret_cast<int32_t *>(ws + L.list);
+    da.ws_count = reinterpret_cast<int32_t *>(ws + L.count);
+    if (launch_decide(dt, da, stream) != hipSuccess) return COSPEC_ERR_HIP;
+
+    SpsArgs sa{};
+    sa.tgt = ra.tgt; sa.drf = ra.drf; sa.ld_bytes = ra.ld_bytes; sa.V = V; sa.B = B; sa.K = K;
+    sa.tokens = draft_tokens; sa.uniform = uniforms; sa.partials = partials; sa.splits = splits;
+    sa.drf_row0 = static_cast<int64_t>(B) * (K + 1);
+    sa.ws_state = da.ws_state; sa.ws_logp_tgt = da.ws_logp_tgt;
+    sa.seg_mass = reinterpret_cast<float *>(ws + L.seg);
+    sa.nseg = static_cast<int32_t>(n_segments(V, eb));
+    sa.accept_len = accept_len; sa.out_tokens = out_tokens;
+    sa.drf_argmax = F.drf_argmax; sa.drf_max = F.drf_max; sa.drf_lse = F.drf_lse; sa.drf_ent = F.drf_entropy;
+    sa.logp_drf = F.logp_drf; sa.accept_prob = F.policy; sa.accept = F.accept;
+    if (launch_sps(dt, sa, stream) != hipSuccess) return COSPEC_ERR_HIP;
+    return COSPEC_OK;
 }
 
 cospec_status cospec_verify_tree(const void *target_logits, const void *draft_logits,

@@ -130,6 +130,25 @@ struct FinishArgs {
     float *z_tilde; float *policy; uint8_t *accept;
 };
 
+// Speculative sampling baseline (k_sps_finish, k_sps_mass, k_sps_pick).
+struct SpsArgs {
+    const char *tgt, *drf;
+    int64_t ld_bytes;
+    int32_t V, B, K;
+    const int32_t *tokens;     // [B][K]
+    const float *uniform;      // [B][K+1]: K acceptance tests, then the last token's draw
+    const float4 *partials;
+    int32_t splits;
+    int64_t drf_row0;          // partial-row index of draft row 0 (= B * (K+1))
+    const uint8_t *ws_state;   // decide's state (invalid tokens are rejected)
+    const float *ws_logp_tgt;
+    float *seg_mass;           // [B][nseg] weights of the last token's distribution
+    int32_t nseg;
+    int32_t *accept_len; int32_t *out_tokens;
+    int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent; float *logp_drf;
+    float *accept_prob; uint8_t *accept;
+};
+
 struct ArbFinishArgs {
     int64_t n_sel, n_rows;
     const int32_t *row_index;
@@ -145,5 +164,6 @@ int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
 hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
+hipError_t launch_sps(Dtype dt, const SpsArgs &a, hipStream_t s);   // finish, weights, pick
 
 }  // namespace cospec

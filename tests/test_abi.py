@@ -162,6 +162,23 @@ def test_split_phase_arguments():
     assert a(*args[:11], None, FAKE, None, None, FAKE, 1 << 30, None) == INVALID   # accept_len missing
 
 
+def test_sps_arguments():
+    L = cs.lib()
+    assert L.cospec_verify_block_sps_workspace_size(64, 7, 151936) > 0
+    assert L.cospec_verify_block_sps_workspace_size(64, 65, 151936) == 0
+
+    def call(u=FAKE, opts=None, B=4, K=7, wsb=1 << 30):
+        return L.cospec_verify_block_sps(FAKE, FAKE, 1, 151936, FAKE, u, B, K, 151936, FAKE, FAKE, None,
+                                         opts, FAKE, wsb, None)
+    assert call(u=None) == INVALID
+    assert call(u=FAKE + 2) == INVALID
+    assert call(K=65) == UNSUPPORTED
+    assert call(wsb=100) == WORKSPACE
+    assert call(B=0, u=None) == OK
+    for bad in (binding._Options(policy_uniform=FAKE), binding._Options(sample_uniform=FAKE)):
+        assert call(opts=ctypes.byref(bad)) == INVALID
+
+
 def _tree(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
              lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30,

@@ -656,3 +656,58 @@ def test_packed_hidden_rows():
     for i in range(2, K):
         if not delta[i]:
             assert torch.isnan(zt[i]) and acc[i] == 0
+
+
+# ------------------------------------------------------------------ speculative sampling baseline
+
+def _sps(wl, seed, splits=0, pad=0):
+    u = _uniforms((wl.B, wl.K + 1), seed)
+    gpu = cs.sps_block(_padded(wl.target, pad), _padded(wl.draft, pad), wl.draft_tokens.to(DEV), u.to(DEV),
+                       splits=splits)
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in gpu.items()}
+    t, d = _conv(wl.target), _conv(wl.draft)
+    ref = oracle.sps_block(t, d, wl.draft_tokens.numpy(), u.double().numpy())
+    return gpu, parity.check_sps(gpu, ref, t, d, u.double().numpy())
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_sps_configs(cfg):
+    wl = workloads.make_config(cfg)
+    gpu, stats = _sps(wl, 400 + cfg)
+    _report(f"SpS config {cfg}", stats, gpu)
+
+
+@pytest.mark.parametrize("B,K,V,dtype,pad,splits", [(3, 1, 7, "f32", 1, 0), (4, 4, 9, "bf16", 0, 2),
+                                                     (5, 6, 4097, "bf16", 8, 3), (3, 5, 32001, "f32", 3, 0),
+                                                     (2, 0, 3000, "bf16", 0, 0), (6, 9, 151936, "bf16", 0, 5)])
+def test_sps_fuzz(B, K, V, dtype, pad, splits):
+    wl = workloads.make_chain(B=B, K=K, V=V, d=64, h=32, dtype=dtype, seed=V % 53 + K, noise=0.6,
+                              peaked=0.2)
+    gpu, stats = _sps(wl, V + K, splits=splits, pad=pad)
+    _report(f"SpS fuzz B={B} K={K} V={V} {dtype}", stats, gpu)
+
+
+def test_sps_preserves_the_target_distribution_on_gpu():
+    # draft token y drawn from p_D (weighted), both uniforms on an n x n grid: the first
+    # emitted token must follow p_T
+    V, n = 8, 64
+    g = torch.Generator().manual_seed(19)
+    t_logit = torch.randn(V, generator=g) * 1.5
+    d_logit = torch.randn(V, generator=g) * 1.5
+    pT = torch.softmax(t_logit.double(), 0).numpy()
+    pD = torch.softmax(d_logit.double(), 0).numpy()
+    grid = (torch.arange(n, dtype=torch.float64) + 0.5) / n
+    ua, ur = torch.meshgrid(grid, grid, indexing="ij")
+    m = n * n
+    u = torch.stack([ua.reshape(-1), ur.reshape(-1)], 1).float().to(DEV)
+    target = t_logit.expand(m, 2, V).contiguous().to(DEV)
+    draft = d_logit.expand(m, 1, V).contiguous().to(DEV)
+    dist = np.zeros(V)
+    for y in range(V):
+        toks = torch.full((m, 1), y, dtype=torch.int32, device=DEV)
+        out = cs.sps_block(target, draft, toks, u, features=False)
+        torch.cuda.synchronize()
+        first = out["tokens"][:, 0].cpu().numpy()
+        dist += pD[y] * np.bincount(first, minlength=V) / m
+    assert np.abs(dist - pT).max() <= 2.5 / n
