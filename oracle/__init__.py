@@ -44,7 +44,8 @@ __all__ = [
     "policy_accept", "chain_length", "chain_tokens", "tree_select", "verify_block",
     "verify_tree", "arbitrate", "chain_outcomes", "tree_outcomes", "RowStats", "sample_rows",
     "cdf_at", "candidates", "policy_sample", "action_logprob", "rl_round", "RL_ALPHA", "RL_BETA",
-    "residual_sample", "sps_block", "SPS_BAND",
+    "residual_sample", "sps_block", "SPS_BAND", "arbitrator_length", "hybrid_mask",
+    "hybrid_attention",
 ]
 
 F32, BF16 = 0, 1
@@ -649,3 +650,67 @@ def arbitrate(hidden, rows, head, lam: float) -> dict:
     z = head_logits(hidden2, rows, w1, b1, w2, b2)
     a, pi, amb = policy_accept(z, lam)
     return dict(z=z, pi=pi, accept=a, ambiguous=amb)
+
+
+# ---------------------------------------------------------------- the arbitrator's hybrid attention
+
+def arbitrator_length(ctx_len: int, K: int) -> int:
+    """Length of the arbitrator input q = [context, SEP, draft 1..K, SEP, candidates
+    1..K, SEP] (Eq. arb_input): l_c + 2K + 3."""
+    return int(ctx_len) + 2 * K + 3
+
+
+def hybrid_mask(ctx_len, K: int, L: int) -> np.ndarray:
+    """Attention mask of the arbitrator (Section 3.3) for a batch padded to length L:
+    mask[b, i, j] = 1 when query position i of sequence b may attend key position j.
+    Positions before l_c (the context) attend causally within the context; the
+    draft/target region, read here as starting at the first [SEP] (position l_c)
+    and ending at l = l_c + 2K + 3, attends to every position of the context and of
+    the region; nothing flows from the region back into the context.  Padding
+    positions i >= l attend only to themselves (no row is empty)."""
+    ctx = np.asarray(ctx_len, dtype=np.int64)
+    B = ctx.shape[0]
+    out = np.zeros((B, L, L), np.uint8)
+    for b in range(B):
+        lc = int(ctx[b])
+        ln = arbitrator_length(lc, K)
+        for i in range(L):
+            for j in range(L):
+                if i >= ln:
+                    out[b, i, j] = i == j
+                elif i < lc:
+                    out[b, i, j] = j <= i
+                else:
+                    out[b, i, j] = j < ln
+    return out
+
+
+def hybrid_attention(q, k, v, ctx_len, q_start, K: int, scale: float) -> np.ndarray:
+    """softmax(q k^T * scale + mask) v for the queries of each sequence, in fp64.
+
+    q [B, n_q, Hq, D]: queries at positions q_start[b] .. q_start[b] + n_q - 1;
+    k, v [B, L, Hkv, D]: keys and values of positions 0..L-1; Hq is a multiple of
+    Hkv and query head h reads key/value head h // (Hq / Hkv) (grouped queries).
+    The mask is hybrid_mask's rule for that sequence; queries at padding positions
+    (>= l) give zeros.  Arrays are float32 or uint16 bf16 bits."""
+    qf, kf, vf = element(np.asarray(q)), element(np.asarray(k)), element(np.asarray(v))
+    B, nq, Hq, D = qf.shape
+    L, Hkv = kf.shape[1], kf.shape[2]
+    grp = Hq // Hkv
+    out = np.zeros((B, nq, Hq, D))
+    for b in range(B):
+        lc = int(ctx_len[b])
+        ln = arbitrator_length(lc, K)
+        if ln > L:
+            raise ValueError(f"sequence {b}: input length {ln} exceeds the {L} cached positions")
+        for r in range(nq):
+            p = int(q_start[b]) + r
+            if p >= ln:
+                continue
+            vis = np.arange(p + 1) if p < lc else np.arange(ln)
+            for h in range(Hq):
+                kh = h // grp
+                s = (kf[b, vis, kh, :] @ qf[b, r, h, :]) * scale
+                w = np.exp(s - s.max())
+                out[b, r, h, :] = (w / w.sum()) @ vf[b, vis, kh, :]
+    return out

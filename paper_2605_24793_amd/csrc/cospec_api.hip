@@ -3,9 +3,9 @@
 //
 // verify_block / verify_tree enqueue, on the caller's stream:
 //   1. k_vocab_reduce   the target and draft rows (only the target rows when the
-//                       head overlaps step 4 on the aux stream), split over
-//                       `splits` workgroups per row -> partial (max, argmax, S, T);
-//                       zeroes the list counter
+//                       decision work overlaps step 4 on the aux stream), split
+//                       over `splits` workgroups per row -> partial (max, argmax,
+//                       S, T); zeroes the list counter
 //   1b. k_sample        temperature 1 only: one wave per target row samples the
 //                       candidate by inversion of its uniform (segment masses
 //                       written by step 1, then one segment re-read)
@@ -219,6 +219,9 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     // 1. target rows; the draft rows too in the same launch unless the head overlaps
     //    their reduction on the aux stream (one launch is cheaper than two)
     const bool split_reduce = aux && head;
+    // The decision work (sampling, decide, head) runs on the aux stream when given,
+    // overlapping the draft-row reduction; otherwise everything is on `stream`.
+    hipStream_t side = c.stream;
     if (do_reduce) {
     ReduceArgs rt = ra;
     rt.row_offset = 0;
@@ -227,6 +230,12 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     if (!record(c.opts ? c.opts->reduce_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rt, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (!record(c.opts ? c.opts->reduce_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
+    if (split_reduce) {
+        if (hipEventRecord(c.opts->aux_ready, c.stream) != hipSuccess ||
+            hipStreamWaitEvent(c.opts->aux_stream, c.opts->aux_ready, 0) != hipSuccess)
+            return COSPEC_ERR_HIP;
+        side = c.opts->aux_stream;
+    }
 
     // 1b. temperature-1 candidates
     if (uniform) {
@@ -241,7 +250,7 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         sa.nseg = ra.nseg;
         sa.uniform = uniform;
         sa.cand = tgt_arg;
-        if (launch_sample(dt, sa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        if (launch_sample(dt, sa, side) != hipSuccess) return COSPEC_ERR_HIP;
     }
 
     // 2. decide
@@ -268,7 +277,7 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     da.ws_listpos = listpos;
     da.ws_list = list;
     da.ws_count = count;
-    if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+    if (launch_decide(dt, da, side) != hipSuccess) return COSPEC_ERR_HIP;
     }
     if (!do_arbitrate) return COSPEC_OK;
 
@@ -289,26 +298,20 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ha.ksplit = ksplit_for(m_cap, c.head);
         ha.upart = upart;
         ha.z = zlog;
-        hipStream_t hs = c.stream;
-        if (aux) {
-            if (hipEventRecord(c.opts->aux_ready, c.stream) != hipSuccess ||
-                hipStreamWaitEvent(c.opts->aux_stream, c.opts->aux_ready, 0) != hipSuccess)
-                return COSPEC_ERR_HIP;
-            hs = c.opts->aux_stream;
-        }
-        if (launch_head(static_cast<Dtype>(c.head->dtype), ha, hs) != hipSuccess) return COSPEC_ERR_HIP;
-        if (aux && hipEventRecord(c.opts->aux_done, hs) != hipSuccess) return COSPEC_ERR_HIP;
+        if (launch_head(static_cast<Dtype>(c.head->dtype), ha, side) != hipSuccess) return COSPEC_ERR_HIP;
     }
+    if (split_reduce && hipEventRecord(c.opts->aux_done, side) != hipSuccess) return COSPEC_ERR_HIP;
 
     // 4. draft rows (features only), when they were not reduced with the target rows
     ReduceArgs rd = ra;
     rd.row_offset = ra.n_tgt_rows;
     rd.n_rows = split_reduce ? static_cast<int32_t>(c.B * c.RD) : 0;   // only in a whole step
     rd.reset_counter = nullptr;
+    rd.leave_room = split_reduce;          // one wave slot per SIMD stays free for the aux stream
     if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (!record(c.opts ? c.opts->reduce2_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
-    if (head && aux && hipStreamWaitEvent(c.stream, c.opts->aux_done, 0) != hipSuccess) return COSPEC_ERR_HIP;
+    if (split_reduce && hipStreamWaitEvent(c.stream, c.opts->aux_done, 0) != hipSuccess) return COSPEC_ERR_HIP;
 
     // 5. finish
     FinishArgs fa{};

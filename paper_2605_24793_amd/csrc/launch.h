@@ -39,6 +39,8 @@ struct ReduceArgs {
     float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
                                // target row, or null; needs vec_per_split % kSegVecs == 0
     int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
+    int32_t leave_room;        // cap the kernel at 7 waves per SIMD so that another stream's
+                               // workgroups find a slot on every CU
 };
 
 // Temperature-1 candidates: one wave per target row inverts its uniform through

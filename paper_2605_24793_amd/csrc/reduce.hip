@@ -255,8 +255,10 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
     }
 }
 
-template <int DT, bool SEG>
+template <int DT, bool SEG, bool ROOM>
 __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
+    // ROOM: claim registers up to v71 so that at most 7 waves per SIMD are resident
+    if (ROOM) asm volatile("" ::: "v71");
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     const int tid = threadIdx.x;
@@ -458,17 +460,23 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
 
 }  // namespace
 
+template <int DT>
+void launch_reduce_t(const ReduceArgs &a, dim3 grid, hipStream_t s) {
+    const bool seg = a.seg && a.row_offset < a.n_tgt_rows;
+    if (a.leave_room) {
+        if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true, true>), grid, dim3(kReduceThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_vocab_reduce<DT, false, true>), grid, dim3(kReduceThreads), 0, s, a);
+    } else {
+        if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true, false>), grid, dim3(kReduceThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_vocab_reduce<DT, false, false>), grid, dim3(kReduceThreads), 0, s, a);
+    }
+}
+
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(a.n_rows) * a.splits));
     if (grid.x == 0) return hipSuccess;
-    const bool seg = a.seg && a.row_offset < a.n_tgt_rows;
-    if (dt == kBF16) {
-        if (seg) hipLaunchKernelGGL((k_vocab_reduce<kBF16, true>), grid, dim3(kReduceThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_vocab_reduce<kBF16, false>), grid, dim3(kReduceThreads), 0, s, a);
-    } else {
-        if (seg) hipLaunchKernelGGL((k_vocab_reduce<kF32, true>), grid, dim3(kReduceThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_vocab_reduce<kF32, false>), grid, dim3(kReduceThreads), 0, s, a);
-    }
+    if (dt == kBF16) launch_reduce_t<kBF16>(a, grid, s);
+    else launch_reduce_t<kF32>(a, grid, s);
     return hipGetLastError();
 }
 

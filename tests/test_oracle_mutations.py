@@ -45,6 +45,10 @@ MUTATIONS = [
     ("__init__.py", "accept = u32 < pi32", "accept = u32 <= pi32"),
     ("cospec_oracle.c", "p[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;", "p[v] = p[v] - q[v];"),   # unclipped residual
     ("__init__.py", "accept = uu[:, :K] < ratio", "accept = uu[:, :K] < 1.0 / ratio"),        # inverted ratio
+    ("__init__.py", "vis = np.arange(p + 1) if p < lc else np.arange(ln)",
+     "vis = np.arange(p + 1) if p <= lc else np.arange(ln)"),                  # first SEP causal
+    ("__init__.py", "                    out[b, i, j] = j <= i\n", "                    out[b, i, j] = j < i + 2\n"),
+    ("__init__.py", "kh = h // grp", "kh = h % Hkv"),                             # wrong query-head group
     ("__init__.py", "t = target_seq[s - 1: s]", "t = target_seq[s - 2: s - 1]"),           # resample wrong row
     ("__init__.py", "logp_tgt = _gather(target[:, :K, :], toks)", "logp_tgt = _gather(target[:, 1:, :], toks)"),
     ("__init__.py", "if ok[n] and depth[n] > depth[best]:", "if ok[n] and depth[n] >= depth[best]:"),

@@ -700,3 +700,70 @@ def test_sps_ambiguous_stops():
     r = oracle.sps_block(target, draft, np.array([[1, 0]]), np.array([[0.6, 0.2, 0.4]]))
     assert r["ambiguous"][0, 0] == (abs(0.6 - r["ratio"][0, 0]) <= oracle.SPS_BAND)
     assert r["stops"][0] == ({1, 3} if r["ambiguous"][0, 0] else {r["accept_len"][0]})
+
+
+# ---------------------------------------------------------------- arbitrator hybrid attention
+
+def test_hybrid_mask_golden():
+    g = _load("hybrid_mask.json")
+    m = oracle.hybrid_mask([g["ctx_len"]], g["K"], g["L"])[0]
+    want = np.array([[int(c) for c in row] for row in g["rows"]], np.uint8)
+    np.testing.assert_array_equal(m, want)
+
+
+@pytest.mark.parametrize("lc,K,L", [(0, 1, 5), (5, 3, 16), (9, 7, 40)])
+def test_hybrid_mask_structure(lc, K, L):
+    m = oracle.hybrid_mask([lc], K, L)[0].astype(bool)
+    ln = lc + 2 * K + 3
+    assert ln == oracle.arbitrator_length(lc, K)
+    np.testing.assert_array_equal(m[:lc, :lc], np.tril(np.ones((lc, lc), bool)))   # causal context
+    assert not m[:lc, lc:].any()                       # no flow from the region into the context
+    assert m[lc:ln, :ln].all()                         # the region sees everything up to l
+    assert not m[:ln, ln:].any()                       # nobody sees padding
+    assert (m.sum(1) >= 1).all()                       # no empty row
+
+
+def _attn_inputs(B=2, nq=5, Hq=4, Hkv=2, D=16, L=12, seed=0):
+    rng = np.random.default_rng(seed)
+    q = rng.normal(size=(B, nq, Hq, D)).astype(np.float32)
+    k = rng.normal(size=(B, L, Hkv, D)).astype(np.float32)
+    v = rng.normal(size=(B, L, Hkv, D)).astype(np.float32)
+    return q, k, v
+
+
+def test_hybrid_attention_against_torch_sdpa():
+    # torch's scaled_dot_product_attention in float64 with a boolean mask built here
+    # from the rule (not from oracle.hybrid_mask) as an independent formulation
+    B, nq, Hq, Hkv, D, L, K = 3, 9, 4, 2, 16, 14, 2
+    q, k, v = _attn_inputs(B, nq, Hq, Hkv, D, L, seed=4)
+    ctx = [2, 5, 7]
+    qs = [0, 3, 5]
+    out = oracle.hybrid_attention(q, k, v, ctx, qs, K, 0.25)
+    for b in range(B):
+        ln = ctx[b] + 2 * K + 3
+        pos = np.arange(nq) + qs[b]
+        keys = np.arange(L)
+        allow = np.where((pos < ctx[b])[:, None], keys[None, :] <= pos[:, None], keys[None, :] < ln)
+        for h in range(Hq):
+            qq = torch.from_numpy(q[b, :, h].astype(np.float64))[None]
+            kk = torch.from_numpy(k[b, :, h // 2].astype(np.float64))[None]
+            vv = torch.from_numpy(v[b, :, h // 2].astype(np.float64))[None]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qq, kk, vv, attn_mask=torch.from_numpy(allow)[None], scale=0.25)[0].numpy()
+            valid = pos < ln
+            np.testing.assert_allclose(out[b, valid, h], ref[valid], rtol=1e-12, atol=1e-12)
+            assert (out[b, ~valid, h] == 0).all()
+
+
+def test_hybrid_attention_closed_forms():
+    q, k, v = _attn_inputs(B=1, nq=4, Hq=2, Hkv=1, D=8, L=10, seed=1)
+    # the first context position sees only key 0: the output is v_0 exactly
+    out = oracle.hybrid_attention(q, k, v, [5], [0], 1, 0.3)
+    np.testing.assert_allclose(out[0, 0, 0], v[0, 0, 0], rtol=0, atol=1e-15)
+    # all-equal keys: uniform weights, the mean of the visible values
+    k[:] = k[:, :1]
+    out = oracle.hybrid_attention(q, k, v, [4], [3], 1, 0.3)      # positions 3..6, l = 4 + 5 = 9
+    np.testing.assert_allclose(out[0, 0, 1], v[0, :4, 0].mean(0), rtol=1e-12)      # context row 3
+    np.testing.assert_allclose(out[0, 1, 0], v[0, :9, 0].mean(0), rtol=1e-12)      # region row, 9 keys
+    with pytest.raises(ValueError):
+        oracle.hybrid_attention(q, k, v, [6], [0], 1, 0.3)        # l = 11 > L = 10 keys
