@@ -763,7 +763,8 @@ def test_hybrid_attention_closed_forms():
     # all-equal keys: uniform weights, the mean of the visible values
     k[:] = k[:, :1]
     out = oracle.hybrid_attention(q, k, v, [4], [3], 1, 0.3)      # positions 3..6, l = 4 + 5 = 9
-    np.testing.assert_allclose(out[0, 0, 1], v[0, :4, 0].mean(0), rtol=1e-12)      # context row 3
-    np.testing.assert_allclose(out[0, 1, 0], v[0, :9, 0].mean(0), rtol=1e-12)      # region row, 9 keys
+    v64 = v.astype(np.float64)
+    np.testing.assert_allclose(out[0, 0, 1], v64[0, :4, 0].mean(0), rtol=1e-12)    # context row 3
+    np.testing.assert_allclose(out[0, 1, 0], v64[0, :9, 0].mean(0), rtol=1e-12)    # region row, 9 keys
     with pytest.raises(ValueError):
         oracle.hybrid_attention(q, k, v, [6], [0], 1, 0.3)        # l = 11 > L = 10 keys
