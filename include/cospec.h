@@ -349,6 +349,42 @@ cospec_status cospec_verify_tree(const void *target_logits, const void *draft_lo
                                  const cospec_options *opts, void *workspace,
                                  size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The arbitrator's hybrid attention (Section 3.3).  The arbitrator reads
+ * q = [context, SEP, draft 1..K, SEP, candidates 1..K, SEP] (Eq. arb_input),
+ * l = l_c + 2K + 3 positions, under a hybrid mask: context positions attend
+ * causally within the context; the draft/target region (read as starting at the
+ * first SEP, position l_c) attends to the whole context and bidirectionally
+ * within itself; nothing flows from the region back into the context.
+ *
+ * cospec_hybrid_mask writes that mask: mask[b][i][j] = 1 when position i of
+ * sequence b may attend position j, else 0, for a batch padded to L positions;
+ * padding positions (i >= l) attend only to themselves.
+ *  ctx_len  [B] int32, l_c of each sequence (negative values act as 0).
+ *  mask     [B][L][L] uint8 out.
+ */
+cospec_status cospec_hybrid_mask(const int32_t *ctx_len, int32_t B, int32_t K, int32_t L, uint8_t *mask,
+                                 hipStream_t stream);
+
+/*
+ * cospec_hybrid_attention: softmax(q k^T * scale + mask) v under the hybrid
+ * mask, computed from the rule (no mask array), for n_q consecutive query
+ * positions q_start[b] .. q_start[b] + n_q - 1 of each sequence.  Per round the
+ * region's 2K+3 positions (q_start = l_c) are the new queries; their keys and
+ * values are the cached context plus the region.
+ *  q        [B][n_q][Hq][D] bf16;  k, v  [B][L][Hkv][D] bf16, positions 0..L-1.
+ *  Hq a multiple of Hkv (query head h reads key/value head h / (Hq / Hkv));
+ *  D 64 or 128; pointers 16-byte aligned.
+ *  out      [B][n_q][Hq][D] bf16.  A query at a position outside [0, l) gets
+ *           zeros; keys at positions >= L do not exist (l is clamped to L).
+ * bf16 inputs, fp32 accumulation; the attention weights enter the second
+ * product rounded to bf16.
+ */
+cospec_status cospec_hybrid_attention(const void *q, const void *k, const void *v, const int32_t *ctx_len,
+                                      const int32_t *q_start, int32_t B, int32_t n_q, int32_t L, int32_t Hq,
+                                      int32_t Hkv, int32_t D, int32_t K, float scale, void *out,
+                                      hipStream_t stream);
+
 /* Workspace bytes cospec_arbitrate needs (0 for invalid sizes). */
 size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head);
 

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libcospec.so")
-SOURCES = ["cospec_api.hip", "reduce.hip", "sample.hip", "head.hip", "scan.hip", "sps.hip"]
+SOURCES = ["cospec_api.hip", "reduce.hip", "sample.hip", "head.hip", "scan.hip", "sps.hip", "attention.hip"]
 HEADERS = [os.path.join(CSRC, "launch.h"), os.path.join(INCLUDE, "cospec.h")]
 
 

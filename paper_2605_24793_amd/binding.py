@@ -16,8 +16,8 @@ import torch
 from . import _build
 
 __all__ = ["lib", "verify_block", "verify_tree", "arbitrate", "CospecError", "Prepared",
-           "prepare_block", "prepare_tree", "prepare_sps", "SplitBlock", "sps_block", "status_string",
-           "MAX_K",
+           "prepare_block", "prepare_tree", "prepare_sps", "SplitBlock", "sps_block", "hybrid_mask",
+           "hybrid_attention", "status_string", "MAX_K",
            "MAX_N", "MAX_SPLITS"]
 
 MAX_K, MAX_N, MAX_SPLITS = 64, 256, 64
@@ -108,6 +108,11 @@ def lib():
         L.cospec_verify_block_sps.argtypes = [P, P, I32, I64, P, P, I32, I32, I32, P, P,
                                               ctypes.POINTER(_Features), ctypes.POINTER(_Options), P,
                                               SZ, P]
+        L.cospec_hybrid_mask.restype = I32
+        L.cospec_hybrid_mask.argtypes = [P, I32, I32, I32, P, P]
+        L.cospec_hybrid_attention.restype = I32
+        L.cospec_hybrid_attention.argtypes = [P, P, P, P, P, I32, I32, I32, I32, I32, I32, I32,
+                                              ctypes.c_float, P, P]
         L.cospec_arbitrate.restype = I32
         L.cospec_arbitrate.argtypes = [P, I64, P, I64, HP, ctypes.c_float, P, P, P, SZ, P]
         _lib = L
@@ -496,3 +501,37 @@ def sps_block(target, draft, draft_tokens, uniforms, features: bool = True, spli
     p = prepare_sps(target, draft, draft_tokens, uniforms, features, splits)
     p.launch()
     return p.result()
+
+
+def _i32(t: torch.Tensor, n: int, what: str) -> torch.Tensor:
+    if tuple(t.shape) != (n,) or t.dtype != torch.int32 or not t.is_cuda:
+        raise ValueError(f"{what} must be an int32 device tensor [{n}]")
+    return t.contiguous()
+
+
+def hybrid_mask(ctx_len: torch.Tensor, K: int, L: int) -> torch.Tensor:
+    """cospec_hybrid_mask: the arbitrator's attention mask [B, L, L] (uint8, 1 = attend)."""
+    B = ctx_len.shape[0]
+    ctx = _i32(ctx_len, B, "ctx_len")
+    out = torch.empty((B, L, L), dtype=torch.uint8, device=ctx.device)
+    _check(lib().cospec_hybrid_mask(_ptr(ctx), B, int(K), int(L), _ptr(out), _stream()), "cospec_hybrid_mask")
+    return out
+
+
+def hybrid_attention(q, k, v, ctx_len, q_start, K: int, scale: float) -> torch.Tensor:
+    """cospec_hybrid_attention: q [B, n_q, Hq, D], k and v [B, L, Hkv, D] (bf16, contiguous)
+    -> [B, n_q, Hq, D] bf16, under the arbitrator's hybrid mask."""
+    B, nq, Hq, D = q.shape
+    L, Hkv = k.shape[1], k.shape[2]
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("q, k and v must be contiguous bf16 device tensors")
+    if tuple(k.shape) != (B, L, Hkv, D) or tuple(v.shape) != (B, L, Hkv, D):
+        raise ValueError("k and v must be [B, L, Hkv, D]")
+    ctx = _i32(ctx_len, B, "ctx_len")
+    qs = _i32(q_start, B, "q_start")
+    out = torch.empty_like(q)
+    code = lib().cospec_hybrid_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(ctx), _ptr(qs), B, nq, L, Hq, Hkv,
+                                         D, int(K), float(scale), _ptr(out), _stream())
+    _check(code, "cospec_hybrid_attention")
+    return out

@@ -1,0 +1,234 @@
+// The arbitrator's hybrid attention (Section 3.3).  The arbitrator reads
+// q = [context, SEP, draft 1..K, SEP, candidates 1..K, SEP] (Eq. arb_input) of
+// length l = l_c + 2K + 3 under a hybrid mask: context positions attend causally
+// within the context; the draft/target region, read as starting at the first SEP
+// (position l_c), attends to the whole context and bidirectionally within itself;
+// nothing flows from the region back into the context.
+//
+// k_hybrid_mask writes that mask densely ([B][L][L] bytes, 1 = attend; padding
+// rows attend only to themselves) for attention code that takes explicit masks.
+//
+// k_hybrid_attention computes softmax(q k^T * scale + mask) v for a range of query
+// positions of each sequence straight from the rule (no mask in memory), with
+// grouped query heads, bf16 inputs and fp32 accumulation on the matrix cores.
+// Per round only the region's 2K+3 queries are new: their keys and values are
+// the cached context plus the region itself.
+//
+// Work split: a workgroup takes 64 query rows (position x head of one key/value
+// group) of one sequence, four waves of 16.  Keys stream in blocks of 64 through
+// LDS: K row-major (rows padded to D*2+16 bytes) and V transposed (rows of 64 keys
+// padded to 136 bytes).  Each wave computes S^T = K Q^T (v_mfma_f32_16x16x32_bf16,
+// A = K rows, B = its queries' columns kept in registers), so lane l owns query
+// column l % 16 of S^T and keeps that query's running max and sum (online
+// softmax).  P^T is packed to bf16 in the same lanes and O^T += V^T P^T leaves
+// O^T[d][query] in the same lane too, so rescaling needs no exchange.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "launch.h"
+
+namespace cospec {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float floatx4;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kKeyBlock = 64;
+constexpr int kQueryRows = 64;        // per workgroup: 4 waves x 16
+constexpr int kVtPitch = 136;         // bytes per row of V^T in LDS (64 keys + 8 pad)
+constexpr float kLog2eA = 1.4426950408889634f;
+
+__device__ inline floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   c, 0, 0, 0);
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ inline uint32_t bf16_bits(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__global__ __launch_bounds__(256) void k_hybrid_mask(MaskArgs a) {
+    const int64_t row = blockIdx.x;                         // b * L + i
+    const int b = static_cast<int>(row / a.L), i = static_cast<int>(row % a.L);
+    const int lc = max(a.ctx_len[b], 0);
+    const int64_t ln = static_cast<int64_t>(lc) + 2 * a.K + 3;
+    uint8_t *out = a.mask + row * a.L;
+    for (int j = threadIdx.x; j < a.L; j += blockDim.x) {
+        bool m;
+        if (i >= ln) m = j == i;
+        else if (i < lc) m = j <= i;
+        else m = j < ln;
+        out[j] = m;
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_hybrid_attention(AttnArgs a) {
+    constexpr int KP = D * 2 + 16;                          // bytes per K row in LDS
+    constexpr int DS = D / 32;                              // MFMA k-steps over d
+    constexpr int DT = D / 16;                              // d tiles of the output
+    __shared__ __attribute__((aligned(16))) char s_k[kKeyBlock * KP];
+    __shared__ __attribute__((aligned(16))) char s_vt[D * kVtPitch];
+
+    const int grp = a.Hq / a.Hkv;
+    const int rows = a.n_q * grp;                           // query rows of one (sequence, kv head)
+    const int wgs_per = (rows + kQueryRows - 1) / kQueryRows;
+    const int b = blockIdx.x / (a.Hkv * wgs_per);
+    const int h = (blockIdx.x / wgs_per) % a.Hkv;
+    const int q0 = (blockIdx.x % wgs_per) * kQueryRows;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, l16 = lane & 15;
+
+    const int lc = max(a.ctx_len[b], 0);
+    const int ln = static_cast<int>(min(static_cast<int64_t>(lc) + 2 * a.K + 3, static_cast<int64_t>(a.L)));
+    const int qs = a.q_start[b];
+    // the last key any query of this workgroup sees
+    const int r_hi = min(q0 + kQueryRows, rows) - 1;
+    const int p_hi = qs + r_hi / grp;
+    const int kend = p_hi >= lc ? ln : min(p_hi + 1, ln);
+
+    // this lane's query column
+    const int qi = q0 + wave * 16 + l16;
+    const bool qvalid = qi < rows;
+    const int r = qvalid ? qi / grp : 0;
+    const int hq = h * grp + (qvalid ? qi % grp : 0);
+    const int p = qs + r;
+    const bool live = qvalid && p >= 0 && p < ln;
+    const int vis = p < lc ? p + 1 : ln;                   // keys [0, vis) are visible
+    u32x4 qf[DS];
+    const char *qrow = static_cast<const char *>(a.q) + ((static_cast<int64_t>(b) * a.n_q + r) * a.Hq + hq) * D * 2;
+#pragma unroll
+    for (int s = 0; s < DS; ++s)
+        qf[s] = live ? *reinterpret_cast<const u32x4 *>(qrow + (32 * s + 8 * g) * 2) : u32x4{0, 0, 0, 0};
+
+    floatx4 o[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, l = 0.f;
+    const float sc = a.scale * kLog2eA;
+
+    const int64_t kv_row = static_cast<int64_t>(a.Hkv) * D * 2;     // bytes between positions
+    const char *kbase = static_cast<const char *>(a.k) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
+    const char *vbase = static_cast<const char *>(a.v) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
+
+    for (int k0 = 0; k0 < kend; k0 += kKeyBlock) {
+        __syncthreads();                                    // the previous block is consumed
+        // K block, row-major: thread t moves 16-byte chunk (t % (D/8)) of keys t / (D/8) + ...
+        constexpr int CH = D / 8;                           // 16-byte chunks per row
+        for (int e = tid; e < kKeyBlock * CH; e += 256) {
+            const int key = e / CH, ch = e % CH;
+            u32x4 x{0, 0, 0, 0};
+            if (k0 + key < kend) x = *reinterpret_cast<const u32x4 *>(kbase + (k0 + key) * kv_row + ch * 16);
+            *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = x;
+        }
+        // V block, transposed: pairs of keys, 8 values of d each, as 32-bit pairs
+        for (int e = tid; e < (kKeyBlock / 2) * CH; e += 256) {
+            const int kp = e / CH, ch = e % CH;
+            u32x4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
+            if (k0 + 2 * kp < kend) x0 = *reinterpret_cast<const u32x4 *>(vbase + (k0 + 2 * kp) * kv_row + ch * 16);
+            if (k0 + 2 * kp + 1 < kend) x1 = *reinterpret_cast<const u32x4 *>(vbase + (k0 + 2 * kp + 1) * kv_row + ch * 16);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const uint32_t lo = x0[w], hi = x1[w];
+                const int d = ch * 8 + 2 * w;
+                *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = (lo & 0xffffu) | (hi << 16);
+                *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) = (lo >> 16) | (hi & 0xffff0000u);
+            }
+        }
+        __syncthreads();
+
+        // S^T[key][query] for the 64 keys: tile c holds keys 16c + 4g + j in element j
+        floatx4 st[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            st[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                const u32x4 kf = *reinterpret_cast<const u32x4 *>(s_k + (16 * c + l16) * KP + (32 * s + 8 * g) * 2);
+                st[c] = mfma(kf, qf[s], st[c]);
+            }
+        }
+        // online softmax over this block, for the query in this lane's column
+        float bm = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = k0 + 16 * c + 4 * g + j;
+                const float s2 = key < vis ? st[c][j] * sc : -INFINITY;
+                st[c][j] = s2;
+                bm = fmaxf(bm, s2);
+            }
+        bm = fmaxf(bm, __shfl_xor(bm, 16));
+        bm = fmaxf(bm, __shfl_xor(bm, 32));
+        const float mn = fmaxf(m, bm);
+        const float alpha = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m - mn);
+        float ps = 0.f;
+        uint32_t pk[4][2];                                   // P^T as bf16 pairs, tile c
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float pv[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                pv[j] = mn == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(st[c][j] - mn);
+                ps += pv[j];
+            }
+            pk[c][0] = bf16_bits(pv[0]) | (bf16_bits(pv[1]) << 16);
+            pk[c][1] = bf16_bits(pv[2]) | (bf16_bits(pv[3]) << 16);
+        }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        l = alpha * l + ps;
+        m = mn;
+#pragma unroll
+        for (int t = 0; t < DT; ++t) o[t] *= alpha;
+        // O^T[d][query] += V^T[d][keys] P^T[keys][query]; step u covers tiles 2u, 2u+1
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const u32x4 pb{pk[2 * u][0], pk[2 * u][1], pk[2 * u + 1][0], pk[2 * u + 1][1]};
+#pragma unroll
+            for (int t = 0; t < DT; ++t) {
+                const char *vr = s_vt + (16 * t + l16) * kVtPitch;
+                const u32x2 lo = *reinterpret_cast<const u32x2 *>(vr + (32 * u + 4 * g) * 2);
+                const u32x2 hi = *reinterpret_cast<const u32x2 *>(vr + (32 * u + 16 + 4 * g) * 2);
+                o[t] = mfma(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, o[t]);
+            }
+        }
+    }
+
+    if (!qvalid) return;
+    // O^T tile t, element j: d = 16t + 4g + j of this lane's query
+    char *orow = static_cast<char *>(a.out) + ((static_cast<int64_t>(b) * a.n_q + r) * a.Hq + hq) * D * 2;
+    const float inv = live && l > 0.f ? 1.f / l : 0.f;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) {
+        const uint32_t w0 = bf16_bits(o[t][0] * inv) | (bf16_bits(o[t][1] * inv) << 16);
+        const uint32_t w1 = bf16_bits(o[t][2] * inv) | (bf16_bits(o[t][3] * inv) << 16);
+        *reinterpret_cast<u32x2 *>(orow + (16 * t + 4 * g) * 2) = u32x2{w0, w1};
+    }
+}
+
+}  // namespace
+
+hipError_t launch_hybrid_mask(const MaskArgs &a, hipStream_t s) {
+    const int64_t rows = static_cast<int64_t>(a.B) * a.L;
+    if (rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_hybrid_mask, dim3(static_cast<unsigned>(rows)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_hybrid_attention(const AttnArgs &a, hipStream_t s) {
+    const int64_t rows = static_cast<int64_t>(a.n_q) * (a.Hq / a.Hkv);
+    const int64_t wgs = static_cast<int64_t>(a.B) * a.Hkv * ((rows + kQueryRows - 1) / kQueryRows);
+    if (wgs == 0) return hipSuccess;
+    if (a.D == 128) hipLaunchKernelGGL(k_hybrid_attention<128>, dim3(static_cast<unsigned>(wgs)), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_hybrid_attention<64>, dim3(static_cast<unsigned>(wgs)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace cospec

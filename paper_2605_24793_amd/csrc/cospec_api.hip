@@ -578,6 +578,33 @@ cospec_status cospec_verify_tree(const void *target_logits, const void *draft_lo
     return run(c, kWhole, accept_len, out_tokens, out_path);
 }
 
+cospec_status cospec_hybrid_mask(const int32_t *ctx_len, int32_t B, int32_t K, int32_t L, uint8_t *mask,
+                                 hipStream_t stream) {
+    if (B < 0 || K < 0 || L < 0) return COSPEC_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(B) * L == 0) return COSPEC_OK;
+    if (!ctx_len || !aligned(ctx_len, 4) || !mask) return COSPEC_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(B) * L > UINT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    MaskArgs a{ctx_len, B, K, L, mask};
+    return launch_hybrid_mask(a, stream) == hipSuccess ? COSPEC_OK : COSPEC_ERR_HIP;
+}
+
+cospec_status cospec_hybrid_attention(const void *q, const void *k, const void *v, const int32_t *ctx_len,
+                                      const int32_t *q_start, int32_t B, int32_t n_q, int32_t L, int32_t Hq,
+                                      int32_t Hkv, int32_t D, int32_t K, float scale, void *out,
+                                      hipStream_t stream) {
+    if (B < 0 || n_q < 0 || L < 0 || K < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !isfinite(scale))
+        return COSPEC_ERR_INVALID_ARG;
+    if (D != 64 && D != 128) return COSPEC_ERR_UNSUPPORTED;
+    if (static_cast<int64_t>(B) * n_q == 0) return COSPEC_OK;
+    if (!q || !aligned(q, 16) || !k || !aligned(k, 16) || !v || !aligned(v, 16) || !out || !aligned(out, 16) ||
+        !ctx_len || !aligned(ctx_len, 4) || !q_start || !aligned(q_start, 4))
+        return COSPEC_ERR_INVALID_ARG;
+    const int64_t wgs = static_cast<int64_t>(B) * Hkv * ((static_cast<int64_t>(n_q) * (Hq / Hkv) + 63) / 64);
+    if (wgs > UINT32_MAX || static_cast<int64_t>(L) * Hkv * D > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    AttnArgs a{q, k, v, ctx_len, q_start, B, n_q, L, Hq, Hkv, D, K, scale, out};
+    return launch_hybrid_attention(a, stream) == hipSuccess ? COSPEC_OK : COSPEC_ERR_HIP;
+}
+
 size_t cospec_arbitrate_workspace_size(int64_t n_sel, const cospec_head *head) {
     if (n_sel < 0 || check_head(head) != COSPEC_OK) return 0;
     return head_bytes(n_sel, head);

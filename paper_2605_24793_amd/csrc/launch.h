@@ -151,6 +151,21 @@ struct SpsArgs {
     float *accept_prob; uint8_t *accept;
 };
 
+// The arbitrator's hybrid mask and attention (attention.hip).
+struct MaskArgs {
+    const int32_t *ctx_len;    // [B]
+    int32_t B, K, L;
+    uint8_t *mask;             // [B][L][L]
+};
+
+struct AttnArgs {
+    const void *q, *k, *v;     // q [B][n_q][Hq][D], k and v [B][L][Hkv][D], bf16
+    const int32_t *ctx_len, *q_start;
+    int32_t B, n_q, L, Hq, Hkv, D, K;
+    float scale;
+    void *out;                 // [B][n_q][Hq][D] bf16
+};
+
 struct ArbFinishArgs {
     int64_t n_sel, n_rows;
     const int32_t *row_index;
@@ -167,5 +182,7 @@ hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + 
 hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
 hipError_t launch_sps(Dtype dt, const SpsArgs &a, hipStream_t s);   // finish, weights, pick
+hipError_t launch_hybrid_mask(const MaskArgs &a, hipStream_t s);
+hipError_t launch_hybrid_attention(const AttnArgs &a, hipStream_t s);
 
 }  // namespace cospec

@@ -179,6 +179,22 @@ def test_sps_arguments():
         assert call(opts=ctypes.byref(bad)) == INVALID
 
 
+def test_hybrid_attention_arguments():
+    L = cs.lib()
+    assert L.cospec_hybrid_mask(None, 2, 1, 8, FAKE, None) == INVALID
+    assert L.cospec_hybrid_mask(FAKE, 0, 1, 8, None, None) == OK
+    assert L.cospec_hybrid_mask(FAKE, -1, 1, 8, FAKE, None) == INVALID
+
+    def attn(Hq=8, Hkv=2, D=128, q=FAKE, scale=0.1, n_q=17):
+        return L.cospec_hybrid_attention(q, FAKE, FAKE, FAKE, FAKE, 2, n_q, 100, Hq, Hkv, D, 7, scale, FAKE,
+                                         None)
+    assert attn(Hq=6, Hkv=4) == INVALID            # Hq not a multiple of Hkv
+    assert attn(D=96) == UNSUPPORTED
+    assert attn(q=FAKE + 8) == INVALID
+    assert attn(scale=math.inf) == INVALID
+    assert attn(n_q=0) == OK
+
+
 def _tree(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, par=FAKE, toks=FAKE, hid=FAKE, head=_head(),
              lam=0.5, B=4, N=60, V=151936, alen=FAKE, otok=FAKE, path=None, ws=FAKE, wsb=1 << 30,

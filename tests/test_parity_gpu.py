@@ -711,3 +711,55 @@ def test_sps_preserves_the_target_distribution_on_gpu():
         first = out["tokens"][:, 0].cpu().numpy()
         dist += pD[y] * np.bincount(first, minlength=V) / m
     assert np.abs(dist - pT).max() <= 2.5 / n
+
+
+# ------------------------------------------------------------------ arbitrator hybrid attention
+
+def test_hybrid_mask_matches_oracle():
+    ctx = torch.tensor([0, 5, 20, -3], dtype=torch.int32)
+    for K, L in ((2, 40), (7, 64), (1, 5)):
+        got = cs.hybrid_mask(ctx.to(DEV), K, L).cpu().numpy()
+        np.testing.assert_array_equal(got, oracle.hybrid_mask(np.maximum(ctx.numpy(), 0), K, L))
+
+
+def _attn_case(B, nq, Hq, Hkv, D, L, ctx, qs, K, seed):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(B, nq, Hq, D, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, L, Hkv, D, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, L, Hkv, D, generator=g).to(torch.bfloat16)
+    ctx_t, qs_t = torch.tensor(ctx, dtype=torch.int32), torch.tensor(qs, dtype=torch.int32)
+    scale = 1.0 / np.sqrt(D)
+    out = cs.hybrid_attention(q.to(DEV), k.to(DEV), v.to(DEV), ctx_t.to(DEV), qs_t.to(DEV), K, scale)
+    torch.cuda.synchronize()
+    ref = oracle.hybrid_attention(bf16_bits(q), bf16_bits(k), bf16_bits(v), ctx, qs, K, scale)
+    got = out.float().cpu().numpy()
+    # P enters the second product as bf16 (relative 2^-9) and the output is stored as bf16:
+    # |error| <= about 2 * 2^-9 * max|v| per element; 6e-3 * max|v| leaves margin
+    tol = 6e-3 * float(v.float().abs().max())
+    err = np.abs(got - ref).max()
+    print(f"[hybrid attention B={B} n_q={nq} Hq={Hq} Hkv={Hkv} D={D} L={L}] max err {err:.2e} (tol {tol:.2e})",
+          flush=True)
+    assert err <= tol
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_hybrid_attention_region_queries(D):
+    K = 7
+    ctx = [37, 100, 0]
+    L = 100 + 2 * K + 3 + 5
+    _attn_case(3, 2 * K + 3, 8, 2, D, L, ctx, ctx, K, seed=D)
+
+
+def test_hybrid_attention_whole_input_prefill():
+    # every position of q at once: causal context rows, region rows, padding rows
+    K = 3
+    ctx = [10, 70]
+    L = 70 + 2 * K + 3 + 4
+    _attn_case(2, L, 4, 4, 128, L, ctx, [0, 0], K, seed=3)
+
+
+def test_hybrid_attention_long_context_gqa():
+    K = 7
+    ctx = [1000, 2041]
+    L = 2041 + 2 * K + 3
+    _attn_case(2, 2 * K + 3, 64, 8, 128, L, ctx, ctx, K, seed=9)
