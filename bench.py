@@ -60,9 +60,76 @@ def parse():
     ap.add_argument("--sps", action="store_true",
                     help="time the standard speculative-sampling baseline (chain workloads) instead "
                          "of the CoSpec step")
+    ap.add_argument("--attention", action="store_true",
+                    help="time the arbitrator's hybrid attention over the region queries "
+                         "(B=64 sequences, 2048 context tokens, K=7, 32 query / 8 key-value heads, "
+                         "D=128) instead of the verify step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     return ap.parse_args()
+
+
+def bench_attention(args):
+    """The arbitrator's hybrid attention for one round's region queries: each sequence's
+    2K+3 new positions attend to its cached context and the region (bf16, fp32
+    accumulation).  Roofline: the key/value bytes every launch must read."""
+    import numpy as np
+    import torch
+
+    import paper_2605_24793_amd as cs
+    from paper_2605_24793_amd.workloads import bf16_bits
+    dev = torch.device("cuda:0")
+    B, ctx_len, K, Hq, Hkv, D = 64, 2048, 7, 32, 8, 128
+    nq = 2 * K + 3
+    l = ctx_len + nq
+    L = (l + 15) // 16 * 16
+    g = torch.Generator().manual_seed(11)
+    q = (torch.randn(B, nq, Hq, D, generator=g)).to(torch.bfloat16)
+    k = (torch.randn(B, L, Hkv, D, generator=g)).to(torch.bfloat16)
+    v = (torch.randn(B, L, Hkv, D, generator=g)).to(torch.bfloat16)
+    ctx = torch.full((B,), ctx_len, dtype=torch.int32)
+    qd, kd, vd, cd = q.to(dev), k.to(dev), v.to(dev), ctx.to(dev)
+    scale = 1.0 / np.sqrt(D)
+    for _ in range(args.warmup):
+        out = cs.hybrid_attention(qd, kd, vd, cd, cd, K, scale)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(args.steps):
+        out = cs.hybrid_attention(qd, kd, vd, cd, cd, K, scale)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    kv_bytes = B * Hkv * l * D * 2 * 2                   # keys and values each sequence's group reads
+    flops = B * Hq * nq * l * D * 2 * 2                  # q k^T and p v
+    achieved = kv_bytes / (ms * 1e-3) / 1e9
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        got = out.float().cpu().numpy()
+        c0 = time.perf_counter()
+        n = 0
+        while n < B and time.perf_counter() - c0 < args.cpu_seconds:
+            ref = oracle.hybrid_attention(bf16_bits(q[n:n + 1]), bf16_bits(k[n:n + 1]), bf16_bits(v[n:n + 1]),
+                                          [ctx_len], [ctx_len], K, scale)
+            tol = 6e-3 * float(v[n].float().abs().max())
+            assert np.abs(got[n:n + 1] - ref).max() <= tol, "attention parity re-check failed"
+            n += 1
+        spent = time.perf_counter() - c0
+        cpu = {"value": n * nq / spent, "unit": "query positions/s", "cores": 1, "kind": "oracle",
+               "sample": f"first {n} of {B} sequences, fp64 oracle, single thread, {spent:.1f} s"}
+    line = {"metric": "hybrid-attention region queries/sec", "value": B * nq / (ms * 1e-3),
+            "unit": "query positions/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"arbitrator region attention B={B} context={ctx_len} K={K} Hq={Hq} "
+                                   f"Hkv={Hkv} D={D}"},
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "kernel": "k_hybrid_attention", "kernel_ms": ms,
+                         "algorithmic_bytes_per_launch": kv_bytes},
+            "tflops": flops / (ms * 1e-3) / 1e12, "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
 
 
 def main():
@@ -71,6 +138,9 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.attention:
+        bench_attention(args)
+        return
     import numpy as np
     import torch
 

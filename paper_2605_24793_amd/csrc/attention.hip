@@ -14,8 +14,10 @@
 // Per round only the region's 2K+3 queries are new: their keys and values are
 // the cached context plus the region itself.
 //
-// Work split: a workgroup takes 64 query rows (position x head of one key/value
-// group) of one sequence, four waves of 16.  Keys stream in blocks of 64 through
+// Work split: the query rows (position x head) that share one key/value head of
+// one sequence go to one workgroup of up to 16 waves, 16 rows per wave, so each
+// key and value is read once per group (more rows: more workgroups).  Keys
+// stream in blocks of 64 through
 // LDS: K row-major (rows padded to D*2+16 bytes) and V transposed (rows of 64 keys
 // padded to 136 bytes).  Each wave computes S^T = K Q^T (v_mfma_f32_16x16x32_bf16,
 // A = K rows, B = its queries' columns kept in registers), so lane l owns query
@@ -37,7 +39,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kKeyBlock = 64;
-constexpr int kQueryRows = 64;        // per workgroup: 4 waves x 16
+constexpr int kMaxWaves = 16;         // per workgroup, 16 query rows each
 constexpr int kVtPitch = 136;         // bytes per row of V^T in LDS (64 keys + 8 pad)
 constexpr float kLog2eA = 1.4426950408889634f;
 
@@ -68,7 +70,7 @@ __global__ __launch_bounds__(256) void k_hybrid_mask(MaskArgs a) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void k_hybrid_attention(AttnArgs a) {
+__global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a) {
     constexpr int KP = D * 2 + 16;                          // bytes per K row in LDS
     constexpr int DS = D / 32;                              // MFMA k-steps over d
     constexpr int DT = D / 16;                              // d tiles of the output
@@ -77,10 +79,11 @@ __global__ __launch_bounds__(256) void k_hybrid_attention(AttnArgs a) {
 
     const int grp = a.Hq / a.Hkv;
     const int rows = a.n_q * grp;                           // query rows of one (sequence, kv head)
-    const int wgs_per = (rows + kQueryRows - 1) / kQueryRows;
+    const int nthr = blockDim.x, wg_rows = nthr / 4;       // 16 rows per wave
+    const int wgs_per = (rows + wg_rows - 1) / wg_rows;
     const int b = blockIdx.x / (a.Hkv * wgs_per);
     const int h = (blockIdx.x / wgs_per) % a.Hkv;
-    const int q0 = (blockIdx.x % wgs_per) * kQueryRows;
+    const int q0 = (blockIdx.x % wgs_per) * wg_rows;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, l16 = lane & 15;
 
@@ -88,7 +91,7 @@ __global__ __launch_bounds__(256) void k_hybrid_attention(AttnArgs a) {
     const int ln = static_cast<int>(min(static_cast<int64_t>(lc) + 2 * a.K + 3, static_cast<int64_t>(a.L)));
     const int qs = a.q_start[b];
     // the last key any query of this workgroup sees
-    const int r_hi = min(q0 + kQueryRows, rows) - 1;
+    const int r_hi = min(q0 + wg_rows, rows) - 1;
     const int p_hi = qs + r_hi / grp;
     const int kend = p_hi >= lc ? ln : min(p_hi + 1, ln);
 
@@ -120,14 +123,14 @@ __global__ __launch_bounds__(256) void k_hybrid_attention(AttnArgs a) {
         __syncthreads();                                    // the previous block is consumed
         // K block, row-major: thread t moves 16-byte chunk (t % (D/8)) of keys t / (D/8) + ...
         constexpr int CH = D / 8;                           // 16-byte chunks per row
-        for (int e = tid; e < kKeyBlock * CH; e += 256) {
+        for (int e = tid; e < kKeyBlock * CH; e += nthr) {
             const int key = e / CH, ch = e % CH;
             u32x4 x{0, 0, 0, 0};
             if (k0 + key < kend) x = *reinterpret_cast<const u32x4 *>(kbase + (k0 + key) * kv_row + ch * 16);
             *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = x;
         }
         // V block, transposed: pairs of keys, 8 values of d each, as 32-bit pairs
-        for (int e = tid; e < (kKeyBlock / 2) * CH; e += 256) {
+        for (int e = tid; e < (kKeyBlock / 2) * CH; e += nthr) {
             const int kp = e / CH, ch = e % CH;
             u32x4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
             if (k0 + 2 * kp < kend) x0 = *reinterpret_cast<const u32x4 *>(vbase + (k0 + 2 * kp) * kv_row + ch * 16);
@@ -224,10 +227,15 @@ hipError_t launch_hybrid_mask(const MaskArgs &a, hipStream_t s) {
 
 hipError_t launch_hybrid_attention(const AttnArgs &a, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(a.n_q) * (a.Hq / a.Hkv);
-    const int64_t wgs = static_cast<int64_t>(a.B) * a.Hkv * ((rows + kQueryRows - 1) / kQueryRows);
+    // as many waves as the group's rows need, at most kMaxWaves, spread evenly
+    const int64_t per_max = 16 * kMaxWaves;
+    const int64_t nwg = (rows + per_max - 1) / per_max;
+    const int64_t waves = (((rows + nwg - 1) / nwg) + 15) / 16;
+    const int64_t wgs = static_cast<int64_t>(a.B) * a.Hkv * ((rows + 16 * waves - 1) / (16 * waves));
     if (wgs == 0) return hipSuccess;
-    if (a.D == 128) hipLaunchKernelGGL(k_hybrid_attention<128>, dim3(static_cast<unsigned>(wgs)), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_hybrid_attention<64>, dim3(static_cast<unsigned>(wgs)), dim3(256), 0, s, a);
+    const dim3 block(static_cast<unsigned>(64 * waves));
+    if (a.D == 128) hipLaunchKernelGGL(k_hybrid_attention<128>, dim3(static_cast<unsigned>(wgs)), block, 0, s, a);
+    else hipLaunchKernelGGL(k_hybrid_attention<64>, dim3(static_cast<unsigned>(wgs)), block, 0, s, a);
     return hipGetLastError();
 }
 

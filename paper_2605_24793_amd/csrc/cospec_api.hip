@@ -599,7 +599,7 @@ cospec_status cospec_hybrid_attention(const void *q, const void *k, const void *
     if (!q || !aligned(q, 16) || !k || !aligned(k, 16) || !v || !aligned(v, 16) || !out || !aligned(out, 16) ||
         !ctx_len || !aligned(ctx_len, 4) || !q_start || !aligned(q_start, 4))
         return COSPEC_ERR_INVALID_ARG;
-    const int64_t wgs = static_cast<int64_t>(B) * Hkv * ((static_cast<int64_t>(n_q) * (Hq / Hkv) + 63) / 64);
+    const int64_t wgs = static_cast<int64_t>(B) * Hkv * ((static_cast<int64_t>(n_q) * (Hq / Hkv) + 15) / 16);
     if (wgs > UINT32_MAX || static_cast<int64_t>(L) * Hkv * D > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
     AttnArgs a{q, k, v, ctx_len, q_start, B, n_q, L, Hq, Hkv, D, K, scale, out};
     return launch_hybrid_attention(a, stream) == hipSuccess ? COSPEC_OK : COSPEC_ERR_HIP;
