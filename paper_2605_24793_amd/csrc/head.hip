@@ -6,11 +6,12 @@
 // for fp32), fp32 accumulation.
 //
 // k_head_gemm: a workgroup owns a 128 x 128 tile of U and one of `ksplit`
-// slices of d.  Its 256 threads stage 128-byte k-slices of the 128 gathered
-// hidden rows and 128 W1 rows through LDS (double-buffered, rows padded to
-// 144 bytes), and each of its four waves accumulates a 64 x 64 sub-tile
-// (4 x 4 MFMA tiles).  The slice's partial U goes to the workspace.  M (the
-// number of mismatches) is read on the device; workgroups past it exit.
+// slices of d.  Its 512 threads stream 128-byte k-slices of the 128 gathered
+// hidden rows and 128 W1 rows into a 4-stage LDS ring with direct loads, and
+// each of its eight waves (two per SIMD, so one wave's LDS reads overlap the
+// other's MFMAs) accumulates a 64 x 32 sub-tile (4 x 2 MFMA tiles).  The
+// slice's partial U goes to the workspace.  M (the number of mismatches) is
+// read on the device; workgroups past it exit.
 //
 // k_head_epilogue: one wave per row adds the k-slices in a fixed order, then
 // b1, the ReLU, w2 and b2, so z is bit-identical run to run.
@@ -34,7 +35,9 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStageBytes = 128;                  // bytes of k per row per stage
 constexpr int kRing = 4;                          // LDS stages: three in flight while one is used
-constexpr int kWaveTile = 64;
+constexpr int kWaveTile = 64;                    // rows of a wave's sub-tile
+constexpr int kWaveCols = 32;                    // columns of a wave's sub-tile
+constexpr int kGemmWaves = 8;                    // 2 x 4 waves per workgroup: two per SIMD
 
 template <int DT> __device__ inline float scalar_at(const void *p, int64_t i);
 template <> __device__ inline float scalar_at<kBF16>(const void *p, int64_t i) {
@@ -79,7 +82,7 @@ __device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
 }
 
 template <int DT>
-__global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
+__global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
     constexpr int BK = kStageBytes / EB;          // elements of k per stage
     constexpr int VE = 16 / EB;                   // elements per 16-byte vector
@@ -98,22 +101,22 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     const int nst = k1 > k0 ? (k1 - k0 + BK - 1) / BK : 0;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wr = wave >> 2, wc = wave & 3;
     const int g = lane >> 4, l16 = lane & 15;
 
     // LDS ring of kRing stages; a stage holds 128 rows of A then 128 rows of B, 128 bytes
     // each, the 16-byte slot s of row r holding k-vector (s ^ (r & 7)) of the stage
     __shared__ __attribute__((aligned(16))) char ring[kRing][2 * kHeadTileM * kStageBytes];
 
-    // async loader: per stage, wave w fills 1 KB blocks w*4+i of A and of B (8 rows each);
-    // lane l brings row 8*(w*4+i) + l/8, k-vector (l%8) ^ (row%8)
+    // async loader: per stage, wave w fills 1 KB blocks w*2+i of A and of B (8 rows each);
+    // lane l brings row 8*(w*2+i) + l/8, k-vector (l%8) ^ (row%8)
     const int lrow = lane >> 3, lslot = lane & 7;
-    const char *ga[4];
-    const char *gb[4];
-    int lvec[4];
+    const char *ga[2];
+    const char *gb[2];
+    int lvec[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int row = 8 * (wave * 4 + i) + lrow;
+    for (int i = 0; i < 2; ++i) {
+        const int row = 8 * (wave * 2 + i) + lrow;
         lvec[i] = lslot ^ (row & 7);
         int64_t m = m_base + row;
         if (m >= M) m = M - 1;                     // garbage rows are computed, never stored
@@ -127,10 +130,10 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     auto issue = [&](int st) {
         char *slot = ring[st % kRing];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 2; ++i) {
             const int e = k0 + st * BK + lvec[i] * VE;          // first element of the vector
-            char *la = slot + (wave * 4 + i) * 1024;
-            char *lb = slot + kHeadTileM * kStageBytes + (wave * 4 + i) * 1024;
+            char *la = slot + (wave * 2 + i) * 1024;
+            char *lb = slot + kHeadTileM * kStageBytes + (wave * 2 + i) * 1024;
             if (e < k1) {                                       // d is a multiple of VE
                 __builtin_amdgcn_global_load_lds(ga[i] + static_cast<int64_t>(e) * EB, (lds_char *)la, 16, 0, 0);
                 __builtin_amdgcn_global_load_lds(gb[i] + static_cast<int64_t>(e) * EB, (lds_char *)lb, 16, 0, 0);
@@ -141,11 +144,11 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
         }
     };
 
-    floatx4 acc[4][4];
+    floatx4 acc[4][2];
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < 2; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
     for (int st = 0; st < kRing - 1; ++st)
@@ -153,8 +156,8 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
     for (int st = 0; st < nst; ++st) {
         // this wave's loads of stage st are done once at most the later stages' remain
         const int later = min(kRing - 2, nst - 1 - st);
-        if (later >= 2) wait_vm<16>();
-        else if (later == 1) wait_vm<8>();
+        if (later >= 2) wait_vm<8>();                 // 4 loads per wave and stage
+        else if (later == 1) wait_vm<4>();
         else wait_vm<0>();
         lds_barrier();                            // every wave's part of stage st has landed
         if (st + kRing - 1 < nst) issue(st + kRing - 1);   // refills the slot of stage st-1
@@ -162,21 +165,21 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
         const char *sb = sa + kHeadTileM * kStageBytes;
 #pragma unroll
         for (int kk = 0; kk < kStageBytes / 16; kk += 4) {
-            u32x4 av[4], bv[4];
+            u32x4 av[4], bv[2];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int row = wr * kWaveTile + r * 16 + l16;
                 av[r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
             }
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int row = wc * kWaveTile + c * 16 + l16;
+            for (int c = 0; c < 2; ++c) {
+                const int row = wc * kWaveCols + c * 16 + l16;
                 bv[c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int c = 0; c < 4; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
+                for (int c = 0; c < 2; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
         }
     }
 
@@ -189,8 +192,8 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs a) {
             const int64_t m = m_base + wr * kWaveTile + r * 16 + 4 * g + j;
             if (m < M) {
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int n = n_base + wc * kWaveTile + c * 16 + l16;
+                for (int c = 0; c < 2; ++c) {
+                    const int n = n_base + wc * kWaveCols + c * 16 + l16;
                     if (n < a.h) up[m * a.h + n] = acc[r][c][j];
                 }
             }
@@ -272,11 +275,12 @@ hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(tiles * a.ksplit));
     if (grid.x == 0) return hipSuccess;
     const dim3 egrid(static_cast<unsigned>((a.m_cap + 3) / 4));
+    const dim3 block(64 * kGemmWaves);
     if (dt == kBF16) {
-        hipLaunchKernelGGL(k_head_gemm<kBF16>, grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_head_gemm<kBF16>, grid, block, 0, s, a);
         hipLaunchKernelGGL(k_head_epilogue<kBF16>, egrid, dim3(256), 0, s, a);
     } else {
-        hipLaunchKernelGGL(k_head_gemm<kF32>, grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_head_gemm<kF32>, grid, block, 0, s, a);
         hipLaunchKernelGGL(k_head_epilogue<kF32>, egrid, dim3(256), 0, s, a);
     }
     return hipGetLastError();
