@@ -15,7 +15,7 @@
 // the cached context plus the region itself.
 //
 // Work split: the query rows (position x head) that share one key/value head of
-// one sequence go to one workgroup of up to 16 waves, 16 rows per wave, so each
+// one sequence go to one workgroup of up to 8 waves, 16 rows per wave, so each
 // key and value is read once per group (more rows: more workgroups).  Keys
 // stream in blocks of 64 through
 // LDS: K row-major (rows padded to D*2+16 bytes) and V transposed (rows of 64 keys
@@ -28,6 +28,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "launch.h"
 
 namespace cospec {
@@ -39,7 +41,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kKeyBlock = 64;
-constexpr int kMaxWaves = 16;         // per workgroup, 16 query rows each
+constexpr int kMaxWaves = 8;          // per workgroup, 16 query rows each (register budget)
 constexpr int kVtPitch = 136;         // bytes per row of V^T in LDS (64 keys + 8 pad)
 constexpr float kLog2eA = 1.4426950408889634f;
 
@@ -119,31 +121,59 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
     const char *kbase = static_cast<const char *>(a.k) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
     const char *vbase = static_cast<const char *>(a.v) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
 
+    // Key/value blocks are prefetched into registers one block ahead: the loads of
+    // block k0 + 64 are in flight while block k0 is computed from LDS.  A workgroup
+    // has at least four waves, so each thread carries at most KPT key chunks and
+    // VPT value pairs.
+    constexpr int CH = D / 8;                               // 16-byte chunks per row
+    constexpr int KPT = kKeyBlock * CH / 256;
+    constexpr int VPT = (kKeyBlock / 2) * CH / 256;
+    u32x4 kr[KPT], v0r[VPT], v1r[VPT];
+    auto fetch = [&](int kb) {
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+            const int e = tid + i * nthr, key = e / CH, ch = e % CH;
+            kr[i] = u32x4{0, 0, 0, 0};
+            if (e < kKeyBlock * CH && kb + key < kend)
+                kr[i] = *reinterpret_cast<const u32x4 *>(kbase + (kb + key) * kv_row + ch * 16);
+        }
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+            const int e = tid + i * nthr, kp = e / CH, ch = e % CH;
+            v0r[i] = u32x4{0, 0, 0, 0};
+            v1r[i] = u32x4{0, 0, 0, 0};
+            if (e < (kKeyBlock / 2) * CH) {
+                if (kb + 2 * kp < kend) v0r[i] = *reinterpret_cast<const u32x4 *>(vbase + (kb + 2 * kp) * kv_row + ch * 16);
+                if (kb + 2 * kp + 1 < kend)
+                    v1r[i] = *reinterpret_cast<const u32x4 *>(vbase + (kb + 2 * kp + 1) * kv_row + ch * 16);
+            }
+        }
+    };
+    if (kend > 0) fetch(0);
+
     for (int k0 = 0; k0 < kend; k0 += kKeyBlock) {
         __syncthreads();                                    // the previous block is consumed
-        // K block, row-major: thread t moves 16-byte chunk (t % (D/8)) of keys t / (D/8) + ...
-        constexpr int CH = D / 8;                           // 16-byte chunks per row
-        for (int e = tid; e < kKeyBlock * CH; e += nthr) {
-            const int key = e / CH, ch = e % CH;
-            u32x4 x{0, 0, 0, 0};
-            if (k0 + key < kend) x = *reinterpret_cast<const u32x4 *>(kbase + (k0 + key) * kv_row + ch * 16);
-            *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = x;
-        }
-        // V block, transposed: pairs of keys, 8 values of d each, as 32-bit pairs
-        for (int e = tid; e < (kKeyBlock / 2) * CH; e += nthr) {
-            const int kp = e / CH, ch = e % CH;
-            u32x4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
-            if (k0 + 2 * kp < kend) x0 = *reinterpret_cast<const u32x4 *>(vbase + (k0 + 2 * kp) * kv_row + ch * 16);
-            if (k0 + 2 * kp + 1 < kend) x1 = *reinterpret_cast<const u32x4 *>(vbase + (k0 + 2 * kp + 1) * kv_row + ch * 16);
+        // K block row-major; V block transposed, pairs of keys as 32-bit words
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const uint32_t lo = x0[w], hi = x1[w];
-                const int d = ch * 8 + 2 * w;
-                *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = (lo & 0xffffu) | (hi << 16);
-                *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) = (lo >> 16) | (hi & 0xffff0000u);
+        for (int i = 0; i < KPT; ++i) {
+            const int e = tid + i * nthr, key = e / CH, ch = e % CH;
+            if (e < kKeyBlock * CH) *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = kr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+            const int e = tid + i * nthr, kp = e / CH, ch = e % CH;
+            if (e < (kKeyBlock / 2) * CH) {
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const uint32_t lo = v0r[i][w], hi = v1r[i][w];
+                    const int d = ch * 8 + 2 * w;
+                    *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = (lo & 0xffffu) | (hi << 16);
+                    *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) = (lo >> 16) | (hi & 0xffff0000u);
+                }
             }
         }
         __syncthreads();
+        if (k0 + kKeyBlock < kend) fetch(k0 + kKeyBlock);
 
         // S^T[key][query] for the 64 keys: tile c holds keys 16c + 4g + j in element j
         floatx4 st[4];
@@ -230,7 +260,7 @@ hipError_t launch_hybrid_attention(const AttnArgs &a, hipStream_t s) {
     // as many waves as the group's rows need, at most kMaxWaves, spread evenly
     const int64_t per_max = 16 * kMaxWaves;
     const int64_t nwg = (rows + per_max - 1) / per_max;
-    const int64_t waves = (((rows + nwg - 1) / nwg) + 15) / 16;
+    const int64_t waves = std::max<int64_t>(4, (((rows + nwg - 1) / nwg) + 15) / 16);   // >= 4: loaders
     const int64_t wgs = static_cast<int64_t>(a.B) * a.Hkv * ((rows + 16 * waves - 1) / (16 * waves));
     if (wgs == 0) return hipSuccess;
     const dim3 block(static_cast<unsigned>(64 * waves));
