@@ -9,7 +9,7 @@
 // k_sps_mass: for every sequence, the weight of every segment of kSegVecs
 //   16-byte vectors of the distribution its last token is drawn from: the
 //   residual max(0, p_T - p_D) of rows s-1 when s <= K, p_T of target row K
-//   otherwise.  One wave per segment.
+//   otherwise.  One wave per four segments, all of its loads issued first.
 // k_sps_pick (one wave per sequence): inverts the sequence's last uniform
 //   through the segment weights, then through the elements of that segment.
 #include <hip/hip_runtime.h>
@@ -22,7 +22,8 @@
 namespace cospec {
 namespace {
 
-constexpr int kMassSegsPerBlock = 4;          // one segment per wave
+constexpr int kMassSegsPerWave = 4;
+constexpr int kMassSegsPerBlock = 4 * kMassSegsPerWave;
 constexpr float kBelowOne = 0x1.fffffep-1f;
 
 // p(x) = exp((x - max) - ln S) of a merged row, in fp32 via exp2.
@@ -115,26 +116,50 @@ __global__ __launch_bounds__(256) void k_sps_mass(SpsArgs a) {
     const int lane = threadIdx.x & 63;
     const int per_seq = (a.nseg + kMassSegsPerBlock - 1) / kMassSegsPerBlock;
     const int b = blockIdx.x / per_seq;
-    const int seg = (blockIdx.x % per_seq) * kMassSegsPerBlock + (threadIdx.x >> 6);
-    if (seg >= a.nseg) return;                             // whole wave leaves
+    const int seg0 = (blockIdx.x % per_seq) * kMassSegsPerBlock + (threadIdx.x >> 6) * kMassSegsPerWave;
+    if (seg0 >= a.nseg) return;                            // whole wave leaves
     const LastRows r = last_rows(a, b);
     const int nvec = static_cast<int>((static_cast<int64_t>(a.V) * E::kBytes) / 16);
     const int nmain = (nvec + kSegVecs - 1) / kSegVecs;
-    float m = 0.f;
-    if (seg < nmain) {
-        const int v = seg * kSegVecs + lane;
-        if (v < nvec) {
-            float w[NV];
-            vec_weights<DT>(r, v, w);
+    // all of this wave's loads first (kMassSegsPerWave segments of both rows), then
+    // the weights: the loads overlap instead of one segment's round trip at a time
+    u32x4 tq[kMassSegsPerWave], dq[kMassSegsPerWave];
 #pragma unroll
-            for (int k = 0; k < NV; ++k) m += w[k];
+    for (int j = 0; j < kMassSegsPerWave; ++j) {
+        const int v = (seg0 + j) * kSegVecs + lane;
+        tq[j] = u32x4{0, 0, 0, 0};
+        dq[j] = u32x4{0, 0, 0, 0};
+        if (seg0 + j < nmain && v < nvec) {
+            tq[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(r.t) + v);
+            if (r.d) dq[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(r.d) + v);
         }
-    } else {
-        const int64_t i = static_cast<int64_t>(nvec) * NV + lane;
-        if (i < a.V) m = elem_weight<DT>(r, i);
     }
-    m = wave_sum(m);
-    if (lane == 0) a.seg_mass[static_cast<int64_t>(b) * a.nseg + seg] = m;
+#pragma unroll
+    for (int j = 0; j < kMassSegsPerWave; ++j) {
+        const int seg = seg0 + j;
+        if (seg >= a.nseg) break;                          // wave-uniform
+        float m = 0.f;
+        if (seg < nmain) {
+            if (seg * kSegVecs + lane < nvec) {
+                float x[NV], w[NV];
+                E::unpack(tq[j], x);
+#pragma unroll
+                for (int k = 0; k < NV; ++k) w[k] = prob(x[k], r.ts);
+                if (r.d) {
+                    E::unpack(dq[j], x);
+#pragma unroll
+                    for (int k = 0; k < NV; ++k) w[k] = fmaxf(w[k] - prob(x[k], r.ds), 0.f);
+                }
+#pragma unroll
+                for (int k = 0; k < NV; ++k) m += w[k];
+            }
+        } else {
+            const int64_t i = static_cast<int64_t>(nvec) * NV + lane;
+            if (i < a.V) m = elem_weight<DT>(r, i);
+        }
+        m = wave_sum(m);
+        if (lane == 0) a.seg_mass[static_cast<int64_t>(b) * a.nseg + seg] = m;
+    }
 }
 
 __device__ inline float wave_incl_scan(float x, int lane) {
