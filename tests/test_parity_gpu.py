@@ -763,3 +763,92 @@ def test_hybrid_attention_long_context_gqa():
     ctx = [1000, 2041]
     L = 2041 + 2 * K + 3
     _attn_case(2, 2 * K + 3, 64, 8, 128, L, ctx, ctx, K, seed=9)
+
+
+# ------------------------------------------------------------------ option combinations
+
+@pytest.mark.parametrize("splits,pad,dtype", [(0, 0, "bf16"), (5, 24, "bf16"), (3, 4, "f32")])
+def test_t1_with_sampled_arbitration_and_rl(splits, pad, dtype):
+    wl = workloads.make_chain(B=12, K=6, V=20011, d=64, h=32, dtype=dtype, seed=91 + splits, bias=True,
+                              noise=0.6, peaked=0.2)
+    u = _uniforms((wl.B, wl.K + 1), 500 + splits)
+    pu = _uniforms((wl.B, wl.K), 600 + splits)
+    corr = (torch.arange(wl.B) % 3 == 0).to(torch.uint8)
+    out = cs.verify_block(_padded(wl.target, pad), _padded(wl.draft, pad), wl.draft_tokens.to(DEV),
+                          wl.hidden.to(DEV), _head_dev(wl.head), 0.5, splits=splits, sample_u=u.to(DEV),
+                          policy_u=pu.to(DEV), correct=corr.to(DEV), alpha=1.5, beta=0.3)
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in out.items()}
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(wl.target), u.double().numpy(), stats)
+    ref = oracle.verify_block(_conv(wl.target), _conv(wl.draft), wl.draft_tokens.numpy(), _conv(wl.hidden),
+                              _head_np(wl.head), 0.5, sample_u=u.double().numpy(), cand_override=cand,
+                              policy_u=pu.double().numpy())
+    stats.update(parity.check_block(gpu, ref))
+    stats.update(parity.check_rl(gpu, ref, corr.numpy(), 1.5, 0.3))
+    _report(f"T=1 + sampled arbitration + RL, splits={splits} pad={pad} {dtype}", stats, gpu)
+
+
+@pytest.mark.parametrize("shape,N,splits", [("random", 60, 0), ("random", 37, 6), ("star", 20, 2)])
+def test_t1_trees_with_sampled_arbitration(shape, N, splits):
+    tr = workloads.make_random_tree(B=4, N=N, V=4099, d=64, h=48, shape=shape, seed=N + 7, bias=True,
+                                    noise=0.5)
+    u = _uniforms((tr.B, tr.N), 700 + N)
+    pu = _uniforms((tr.B, tr.N), 800 + N)
+    out = cs.verify_tree(_padded(tr.target, 4), _padded(tr.draft, 4), tr.parent.to(DEV), tr.node_tokens.to(DEV),
+                         tr.hidden.to(DEV), _head_dev(tr.head), 0.5, splits=splits, sample_u=u.to(DEV),
+                         policy_u=pu.to(DEV))
+    torch.cuda.synchronize()
+    gpu = {k: v.cpu() for k, v in out.items()}
+    stats = {}
+    cand = parity.check_candidates(gpu["tgt_candidate"], _conv(tr.target), u.double().numpy(), stats)
+    ref = oracle.verify_tree(_conv(tr.target), _conv(tr.draft), tr.parent.numpy(), tr.node_tokens.numpy(),
+                             _conv(tr.hidden), _head_np(tr.head), 0.5, sample_u=u.double().numpy(),
+                             cand_override=cand, policy_u=pu.double().numpy())
+    stats.update(parity.check_tree(gpu, ref))
+    _report(f"T=1 + sampled arbitration, tree {shape} N={N} splits={splits}", stats, gpu)
+
+
+def test_split_phases_with_everything():
+    wl = workloads.make_config(3, B=10)
+    B, K = wl.B, wl.K
+    u = _uniforms((B, K + 1), 71)
+    pu = _uniforms((B, K), 72)
+    corr = torch.ones(B, dtype=torch.uint8)
+    head = _head_dev(wl.head)
+    tgt, drf, tok = wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV)
+    whole = cs.verify_block(tgt, drf, tok, wl.hidden.to(DEV), head, 0.5, splits=7, sample_u=u.to(DEV),
+                            policy_u=pu.to(DEV), correct=corr.to(DEV))
+    # packed hidden rows: q = [context, SEP, draft, SEP, candidates, SEP] per sequence
+    ctx = torch.randint(1, 30, (B,), generator=torch.Generator().manual_seed(3))
+    qlen = ctx + 2 * K + 3
+    start = torch.cumsum(qlen, 0) - qlen
+    packed = torch.randn(int(qlen.sum()), wl.head.d, generator=torch.Generator().manual_seed(4)).to(wl.hidden.dtype)
+    row0 = start + ctx + 1
+    for b in range(B):
+        packed[row0[b]:row0[b] + K] = wl.hidden[b]
+    sb = cs.SplitBlock(tgt, drf, tok, head, splits=7, sample_u=u.to(DEV))
+    split = sb.arbitrate(packed.to(DEV), 0.5, policy_u=pu.to(DEV), correct=corr.to(DEV),
+                         hidden_row0=row0.to(DEV))
+    torch.cuda.synchronize()
+    _same(whole, split, [k for k in whole if k in split])
+    # a second arbitration on the same phase 1 (another threshold) equals a whole step at it
+    again = sb.arbitrate(packed.to(DEV), 0.3, hidden_row0=row0.to(DEV))
+    whole2 = cs.verify_block(tgt, drf, tok, wl.hidden.to(DEV), head, 0.3, splits=7, sample_u=u.to(DEV))
+    torch.cuda.synchronize()
+    _same(whole2, again, ["accept_len", "tokens", "z_tilde", "accept"])
+
+
+def test_sps_long_blocks():
+    wl = workloads.make_chain(B=5, K=64, V=2053, d=64, h=32, dtype="bf16", seed=17, noise=0.2)
+    gpu, stats = _sps(wl, 77)
+    _report("SpS K=64", stats, gpu)
+    assert gpu["accept_len"].max() > 8                # low noise: long accepted runs
+
+
+def test_hybrid_attention_long_prefill_several_workgroups():
+    # 300 positions x 1 head per group: three workgroups share each group's keys
+    K = 2
+    ctx = [250, 120]
+    L = 250 + 2 * K + 3 + 9
+    _attn_case(2, L, 2, 2, 64, L, ctx, [0, 0], K, seed=21)
