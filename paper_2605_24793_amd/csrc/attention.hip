@@ -50,11 +50,33 @@ __device__ inline floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
                                                    c, 0, 0, 0);
 }
 
-// fp32 -> bf16 bits, round to nearest even (finite inputs).
-__device__ inline uint32_t bf16_bits(float x) {
-    const uint32_t u = __float_as_uint(x);
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+// Two fp32 values -> one word of two bf16 (lo in bits 0-15), round to nearest even
+// (v_cvt_pk_bf16_f32).
+__device__ inline uint32_t bf16_pair(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, bf16x2{static_cast<__bf16>(lo), static_cast<__bf16>(hi)});
 }
+
+// max over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the rows of 16 lanes), in the VALU
+__device__ inline float max_rows(float x) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+    const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+
+__device__ inline float sum_rows(float x) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+    const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
+// The running max of a query is only raised when a block's max exceeds it by more
+// than this (log2 units), so that the accumulators are rarely rescaled; weights stay
+// below 2^kLazyRescale.
+constexpr float kLazyRescale = 8.0f;
 
 __global__ __launch_bounds__(256) void k_hybrid_mask(MaskArgs a) {
     const int64_t row = blockIdx.x;                         // b * L + i
@@ -110,70 +132,78 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
 #pragma unroll
     for (int s = 0; s < DS; ++s)
         qf[s] = live ? *reinterpret_cast<const u32x4 *>(qrow + (32 * s + 8 * g) * 2) : u32x4{0, 0, 0, 0};
+    // the query loads complete here, not at their first use inside the key loop (where
+    // the wait would also cover every key/value prefetch issued after them)
+#pragma unroll
+    for (int s = 0; s < DS; ++s) asm volatile("" : "+v"(qf[s]));
 
     floatx4 o[DT];
 #pragma unroll
     for (int t = 0; t < DT; ++t) o[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // m: running max of the scaled scores (log2 units), common to the four lanes of a
+    // query column; l: this lane's share of the running sum (its keys 4g + j)
     float m = -INFINITY, l = 0.f;
     const float sc = a.scale * kLog2eA;
+    // blocks that end at or below every lane's visible length need no mask
+    int vis_min = vis;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) vis_min = min(vis_min, __shfl_xor(vis_min, off));
 
     const int64_t kv_row = static_cast<int64_t>(a.Hkv) * D * 2;     // bytes between positions
     const char *kbase = static_cast<const char *>(a.k) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
     const char *vbase = static_cast<const char *>(a.v) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
 
     // Key/value blocks are prefetched into registers one block ahead: the loads of
-    // block k0 + 64 are in flight while block k0 is computed from LDS.  A workgroup
-    // has at least four waves, so each thread carries at most KPT key chunks and
-    // VPT value pairs.
+    // block k0 + 64 are in flight while block k0 is computed from LDS.  The first
+    // four waves load (a workgroup has at least four), KPT key chunks and VPT value
+    // pairs per thread.  Rows past kend are read as row kend - 1 (no branches around
+    // the loads): every query's mask ends at or before kend, so their weights are 0.
     constexpr int CH = D / 8;                               // 16-byte chunks per row
     constexpr int KPT = kKeyBlock * CH / 256;
     constexpr int VPT = (kKeyBlock / 2) * CH / 256;
+    const bool loader = tid < 256;
     u32x4 kr[KPT], v0r[VPT], v1r[VPT];
     auto fetch = [&](int kb) {
+        const int last = kend - 1;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) {
-            const int e = tid + i * nthr, key = e / CH, ch = e % CH;
-            kr[i] = u32x4{0, 0, 0, 0};
-            if (e < kKeyBlock * CH && kb + key < kend)
-                kr[i] = *reinterpret_cast<const u32x4 *>(kbase + (kb + key) * kv_row + ch * 16);
+            const int e = tid + i * 256, key = min(kb + e / CH, last), ch = e % CH;
+            kr[i] = *reinterpret_cast<const u32x4 *>(kbase + key * kv_row + ch * 16);
         }
 #pragma unroll
         for (int i = 0; i < VPT; ++i) {
-            const int e = tid + i * nthr, kp = e / CH, ch = e % CH;
-            v0r[i] = u32x4{0, 0, 0, 0};
-            v1r[i] = u32x4{0, 0, 0, 0};
-            if (e < (kKeyBlock / 2) * CH) {
-                if (kb + 2 * kp < kend) v0r[i] = *reinterpret_cast<const u32x4 *>(vbase + (kb + 2 * kp) * kv_row + ch * 16);
-                if (kb + 2 * kp + 1 < kend)
-                    v1r[i] = *reinterpret_cast<const u32x4 *>(vbase + (kb + 2 * kp + 1) * kv_row + ch * 16);
-            }
+            const int e = tid + i * 256, k2 = kb + 2 * (e / CH), ch = e % CH;
+            v0r[i] = *reinterpret_cast<const u32x4 *>(vbase + min(k2, last) * kv_row + ch * 16);
+            v1r[i] = *reinterpret_cast<const u32x4 *>(vbase + min(k2 + 1, last) * kv_row + ch * 16);
         }
     };
-    if (kend > 0) fetch(0);
+    if (kend > 0 && loader) fetch(0);
 
     for (int k0 = 0; k0 < kend; k0 += kKeyBlock) {
         __syncthreads();                                    // the previous block is consumed
         // K block row-major; V block transposed, pairs of keys as 32-bit words
+        if (loader) {
 #pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-            const int e = tid + i * nthr, key = e / CH, ch = e % CH;
-            if (e < kKeyBlock * CH) *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = kr[i];
-        }
+            for (int i = 0; i < KPT; ++i) {
+                const int e = tid + i * 256, key = e / CH, ch = e % CH;
+                *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = kr[i];
+            }
 #pragma unroll
-        for (int i = 0; i < VPT; ++i) {
-            const int e = tid + i * nthr, kp = e / CH, ch = e % CH;
-            if (e < (kKeyBlock / 2) * CH) {
+            for (int i = 0; i < VPT; ++i) {
+                const int e = tid + i * 256, kp = e / CH, ch = e % CH;
 #pragma unroll
                 for (int w = 0; w < 4; ++w) {
                     const uint32_t lo = v0r[i][w], hi = v1r[i][w];
                     const int d = ch * 8 + 2 * w;
-                    *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = (lo & 0xffffu) | (hi << 16);
-                    *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) = (lo >> 16) | (hi & 0xffff0000u);
+                    // (lo & 0xffff) | (hi << 16) and (lo >> 16) | (hi & 0xffff0000)
+                    *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+                    *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) =
+                        __builtin_amdgcn_perm(hi, lo, 0x07060302u);
                 }
             }
         }
         __syncthreads();
-        if (k0 + kKeyBlock < kend) fetch(k0 + kKeyBlock);
+        if (loader && k0 + kKeyBlock < kend) fetch(k0 + kKeyBlock);
 
         // S^T[key][query] for the 64 keys: tile c holds keys 16c + 4g + j in element j
         floatx4 st[4];
@@ -188,38 +218,47 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
         }
         // online softmax over this block, for the query in this lane's column
         float bm = -INFINITY;
+        if (k0 + kKeyBlock <= vis_min) {                     // wave-uniform: no key masked
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < 4; ++c)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int key = k0 + 16 * c + 4 * g + j;
-                const float s2 = key < vis ? st[c][j] * sc : -INFINITY;
-                st[c][j] = s2;
-                bm = fmaxf(bm, s2);
-            }
-        bm = fmaxf(bm, __shfl_xor(bm, 16));
-        bm = fmaxf(bm, __shfl_xor(bm, 32));
-        const float mn = fmaxf(m, bm);
-        const float alpha = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m - mn);
-        float ps = 0.f;
+                for (int j = 0; j < 4; ++j) {
+                    st[c][j] *= sc;
+                    bm = fmaxf(bm, st[c][j]);
+                }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int key = k0 + 16 * c + 4 * g + j;
+                    st[c][j] = key < vis ? st[c][j] * sc : -INFINITY;
+                    bm = fmaxf(bm, st[c][j]);
+                }
+        }
+        bm = max_rows(bm);
+        const bool raise = bm > m + kLazyRescale;            // always when m is still -inf
+        if (__builtin_expect(__ballot(raise) != 0, 0)) {
+            const float alpha = raise ? __builtin_amdgcn_exp2f(m - bm) : 1.f;   // 0 from -inf
+            if (raise) m = bm;
+            l *= alpha;
+#pragma unroll
+            for (int t = 0; t < DT; ++t) o[t] *= alpha;
+        }
+        // a lane whose keys so far are all masked keeps m = -inf and adds nothing
+        const float mm = m == -INFINITY ? INFINITY : m;
         uint32_t pk[4][2];                                   // P^T as bf16 pairs, tile c
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             float pv[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                pv[j] = mn == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(st[c][j] - mn);
-                ps += pv[j];
+                pv[j] = __builtin_amdgcn_exp2f(st[c][j] - mm);
+                l += pv[j];
             }
-            pk[c][0] = bf16_bits(pv[0]) | (bf16_bits(pv[1]) << 16);
-            pk[c][1] = bf16_bits(pv[2]) | (bf16_bits(pv[3]) << 16);
+            pk[c][0] = bf16_pair(pv[0], pv[1]);
+            pk[c][1] = bf16_pair(pv[2], pv[3]);
         }
-        ps += __shfl_xor(ps, 16);
-        ps += __shfl_xor(ps, 32);
-        l = alpha * l + ps;
-        m = mn;
-#pragma unroll
-        for (int t = 0; t < DT; ++t) o[t] *= alpha;
         // O^T[d][query] += V^T[d][keys] P^T[keys][query]; step u covers tiles 2u, 2u+1
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
@@ -234,14 +273,15 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
         }
     }
 
+    l = sum_rows(l);
     if (!qvalid) return;
     // O^T tile t, element j: d = 16t + 4g + j of this lane's query
     char *orow = static_cast<char *>(a.out) + ((static_cast<int64_t>(b) * a.n_q + r) * a.Hq + hq) * D * 2;
     const float inv = live && l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
-        const uint32_t w0 = bf16_bits(o[t][0] * inv) | (bf16_bits(o[t][1] * inv) << 16);
-        const uint32_t w1 = bf16_bits(o[t][2] * inv) | (bf16_bits(o[t][3] * inv) << 16);
+        const uint32_t w0 = bf16_pair(o[t][0] * inv, o[t][1] * inv);
+        const uint32_t w1 = bf16_pair(o[t][2] * inv, o[t][3] * inv);
         *reinterpret_cast<u32x2 *>(orow + (16 * t + 4 * g) * 2) = u32x2{w0, w1};
     }
 }
