@@ -16,14 +16,19 @@
 //
 // Work split: the query rows (position x head) that share one key/value head of
 // one sequence go to one workgroup of up to 8 waves, 16 rows per wave, so each
-// key and value is read once per group (more rows: more workgroups).  Keys
-// stream in blocks of 64 through
-// LDS: K row-major (rows padded to D*2+16 bytes) and V transposed (rows of 64 keys
-// padded to 136 bytes).  Each wave computes S^T = K Q^T (v_mfma_f32_16x16x32_bf16,
-// A = K rows, B = its queries' columns kept in registers), so lane l owns query
-// column l % 16 of S^T and keeps that query's running max and sum (online
-// softmax).  P^T is packed to bf16 in the same lanes and O^T += V^T P^T leaves
-// O^T[d][query] in the same lane too, so rescaling needs no exchange.
+// key and value is read once per group (more rows: more workgroups).  Keys and
+// values stream through a ring of kStages LDS stages of kKeyBlock rows, filled
+// straight from HBM by raw buffer loads into LDS (no register staging): the
+// buffers end after the group's last visible row, so the hardware range check
+// fills later rows with zeros.  Both tiles are stored row-major with an XOR
+// swizzle of their 16- or 32-byte units so that the fragment reads below hit
+// distinct LDS banks.  Each wave computes S^T = K Q^T
+// (v_mfma_f32_16x16x32_bf16, A = K rows from LDS, B = its queries' columns kept
+// in registers), so lane l owns query column l % 16 of S^T and keeps that query's
+// running max and sum (online softmax).  P^T is packed to bf16 in the same lanes
+// and O^T += V^T P^T takes its A operand (V^T) from the row-major V tile with the
+// gfx950 transposing LDS read (ds_read_b64_tr_b16), leaving O^T[d][query] in the
+// lane that owns the query, so rescaling needs no exchange.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -40,10 +45,69 @@ typedef __attribute__((ext_vector_type(4))) float floatx4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kKeyBlock = 64;
+constexpr int kKeyBlock = 32;         // key rows per LDS stage
+constexpr int kStages = 4;            // LDS ring: three stages in flight while one is used
+constexpr int kLoaders = 4;           // waves that issue the loads (a workgroup has at least 4)
 constexpr int kMaxWaves = 8;          // per workgroup, 16 query rows each (register budget)
-constexpr int kVtPitch = 136;         // bytes per row of V^T in LDS (64 keys + 8 pad)
 constexpr float kLog2eA = 1.4426950408889634f;
+
+// Word 3 of a raw (unswizzled, stride 0) buffer resource: 32-bit data format.
+constexpr int kRawBuffer = 0x00020000;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from a raw buffer into LDS at base + 16 * lane (zeros past the
+// buffer's end).
+__device__ inline void load_lds16(__amdgpu_buffer_rsrc_t r, uint32_t off, const char *lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, static_cast<int>(off), 0, 0, 0);
+}
+
+// Waits until at most N vector-memory operations of this wave are outstanding.
+template <int N> __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Waits until this wave has at most PER * later of its loads in flight, later <= MAXL.
+template <int PER, int MAXL> __device__ inline void wait_later(int later) {
+    if constexpr (MAXL > 0) {
+        if (later >= MAXL) wait_vm<PER * MAXL>();
+        else wait_later<PER, MAXL - 1>(later);
+    } else {
+        wait_vm<0>();
+    }
+}
+
+// Workgroup barrier that does not wait for the stages still in flight (as the fence
+// of __syncthreads would); the compiler may not move memory accesses across it.
+__device__ inline void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Transposing LDS read: within each row of 16 lanes, lane j receives element j % 4 of
+// the 8-byte chunks addressed by lanes 4k + j / 4, k = 0..3 (in that order).  Issued
+// as inline assembly: the compiler does not know which LDS the builtin reads and
+// would wait for every load into LDS still in flight before it.  The caller waits for
+// the result with lds_wait().
+typedef __attribute__((address_space(3))) const char lds_cchar;
+__device__ inline u32x2 read_tr(const char *lds) {
+    const uint32_t addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_cchar *)lds));
+    u32x2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+    return r;
+}
+
+// Waits for this wave's LDS reads; the values passed through are only used after it.
+template <int N> __device__ inline void lds_wait(u32x2 (&x)[N], u32x2 (&y)[N]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < N; ++i) asm volatile("" : "+v"(x[i]), "+v"(y[i]));
+}
+
+// XOR swizzles of the LDS tiles (rows of RB = 2D bytes).  K: 16-byte units, so that
+// 16 consecutive rows read at one column hit distinct banks; V: 32-byte units, so
+// that the 8 rows of a transposing read do.
+template <int RB> __device__ inline int swz_k(int row) { return RB == 256 ? (row & 15) : ((row >> 1) & 7); }
+template <int RB> __device__ inline int swz_v(int row) { return RB == 256 ? (row & 7) : ((row >> 1) & 3); }
 
 __device__ inline floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
@@ -95,11 +159,14 @@ __global__ __launch_bounds__(256) void k_hybrid_mask(MaskArgs a) {
 
 template <int D>
 __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a) {
-    constexpr int KP = D * 2 + 16;                          // bytes per K row in LDS
+    constexpr int RB = D * 2;                               // bytes per key/value row
+    constexpr int SB = kKeyBlock * RB;                      // bytes of one tile per stage
+    constexpr int LPW = SB / 1024 / kLoaders;               // 1 KB load instructions per tile and loader
     constexpr int DS = D / 32;                              // MFMA k-steps over d
     constexpr int DT = D / 16;                              // d tiles of the output
-    __shared__ __attribute__((aligned(16))) char s_k[kKeyBlock * KP];
-    __shared__ __attribute__((aligned(16))) char s_vt[D * kVtPitch];
+    static_assert(LPW >= 1 && kKeyBlock == 32, "stage shape");
+    __shared__ __attribute__((aligned(16))) char s_k[kStages][SB];
+    __shared__ __attribute__((aligned(16))) char s_v[kStages][SB];
 
     const int grp = a.Hq / a.Hkv;
     const int rows = a.n_q * grp;                           // query rows of one (sequence, kv head)
@@ -133,7 +200,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
     for (int s = 0; s < DS; ++s)
         qf[s] = live ? *reinterpret_cast<const u32x4 *>(qrow + (32 * s + 8 * g) * 2) : u32x4{0, 0, 0, 0};
     // the query loads complete here, not at their first use inside the key loop (where
-    // the wait would also cover every key/value prefetch issued after them)
+    // the wait would also cover every key/value load issued after them)
 #pragma unroll
     for (int s = 0; s < DS; ++s) asm volatile("" : "+v"(qf[s]));
 
@@ -149,91 +216,85 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) vis_min = min(vis_min, __shfl_xor(vis_min, off));
 
-    const int64_t kv_row = static_cast<int64_t>(a.Hkv) * D * 2;     // bytes between positions
-    const char *kbase = static_cast<const char *>(a.k) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
-    const char *vbase = static_cast<const char *>(a.v) + (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
+    // raw buffers over this group's keys and values, ending after row kend - 1;
+    // offsets are 32-bit (L * Hkv * D * 2 < 2^32)
+    const uint32_t row_b = static_cast<uint32_t>(a.Hkv) * D * 2;   // bytes between positions
+    const int64_t head0 = (static_cast<int64_t>(b) * a.L * a.Hkv + h) * D * 2;
+    const int nbytes = kend > 0 ? static_cast<int>((kend - 1) * row_b + RB) : 0;
+    const __amdgpu_buffer_rsrc_t krs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(static_cast<const char *>(a.k) + head0), 0, nbytes, kRawBuffer);
+    const __amdgpu_buffer_rsrc_t vrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(static_cast<const char *>(a.v) + head0), 0, nbytes, kRawBuffer);
 
-    // Key/value blocks are prefetched into registers one block ahead: the loads of
-    // block k0 + 64 are in flight while block k0 is computed from LDS.  The first
-    // four waves load (a workgroup has at least four), KPT key chunks and VPT value
-    // pairs per thread.  Rows past kend are read as row kend - 1 (no branches around
-    // the loads): every query's mask ends at or before kend, so their weights are 0.
-    constexpr int CH = D / 8;                               // 16-byte chunks per row
-    constexpr int KPT = kKeyBlock * CH / 256;
-    constexpr int VPT = (kKeyBlock / 2) * CH / 256;
-    const bool loader = tid < 256;
-    u32x4 kr[KPT], v0r[VPT], v1r[VPT];
-    auto fetch = [&](int kb) {
-        const int last = kend - 1;
+    // loader wave w, instruction q fills bytes (w * LPW + q) KB of a tile: lane l the
+    // 16 bytes at 16 l of that KB, i.e. row `lrow`, physical unit `pch` of the tile,
+    // which holds logical unit pch ^ swizzle(row)
+    const bool loader = wave < kLoaders;
+    uint32_t koff[LPW], voff[LPW];
 #pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-            const int e = tid + i * 256, key = min(kb + e / CH, last), ch = e % CH;
-            kr[i] = *reinterpret_cast<const u32x4 *>(kbase + key * kv_row + ch * 16);
-        }
+    for (int q = 0; q < LPW; ++q) {
+        const int o16 = ((wave * LPW + q) * 1024 + lane * 16);
+        const int lrow = o16 / RB, pch = (o16 % RB) / 16;
+        koff[q] = lrow * row_b + (pch ^ swz_k<RB>(lrow)) * 16;
+        voff[q] = lrow * row_b + (((pch >> 1) ^ swz_v<RB>(lrow)) * 2 + (pch & 1)) * 16;
+    }
+    const int nblk = (kend + kKeyBlock - 1) / kKeyBlock;
+    auto issue = [&](int j) {
+        const uint32_t off = static_cast<uint32_t>(j * kKeyBlock) * row_b;
+        const char *lk = s_k[j % kStages] + wave * LPW * 1024;
+        const char *lv = s_v[j % kStages] + wave * LPW * 1024;
 #pragma unroll
-        for (int i = 0; i < VPT; ++i) {
-            const int e = tid + i * 256, k2 = kb + 2 * (e / CH), ch = e % CH;
-            v0r[i] = *reinterpret_cast<const u32x4 *>(vbase + min(k2, last) * kv_row + ch * 16);
-            v1r[i] = *reinterpret_cast<const u32x4 *>(vbase + min(k2 + 1, last) * kv_row + ch * 16);
+        for (int q = 0; q < LPW; ++q) {
+            load_lds16(krs, koff[q] + off, lk + q * 1024);
+            load_lds16(vrs, voff[q] + off, lv + q * 1024);
         }
     };
-    if (kend > 0 && loader) fetch(0);
+    if (loader) {
+#pragma unroll
+        for (int j = 0; j < kStages - 1; ++j)
+            if (j < nblk) issue(j);
+    }
 
-    for (int k0 = 0; k0 < kend; k0 += kKeyBlock) {
-        __syncthreads();                                    // the previous block is consumed
-        // K block row-major; V block transposed, pairs of keys as 32-bit words
-        if (loader) {
-#pragma unroll
-            for (int i = 0; i < KPT; ++i) {
-                const int e = tid + i * 256, key = e / CH, ch = e % CH;
-                *reinterpret_cast<u32x4 *>(s_k + key * KP + ch * 16) = kr[i];
-            }
-#pragma unroll
-            for (int i = 0; i < VPT; ++i) {
-                const int e = tid + i * 256, kp = e / CH, ch = e % CH;
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const uint32_t lo = v0r[i][w], hi = v1r[i][w];
-                    const int d = ch * 8 + 2 * w;
-                    // (lo & 0xffff) | (hi << 16) and (lo >> 16) | (hi & 0xffff0000)
-                    *reinterpret_cast<uint32_t *>(s_vt + d * kVtPitch + kp * 4) = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
-                    *reinterpret_cast<uint32_t *>(s_vt + (d + 1) * kVtPitch + kp * 4) =
-                        __builtin_amdgcn_perm(hi, lo, 0x07060302u);
-                }
-            }
-        }
-        __syncthreads();
-        if (loader && k0 + kKeyBlock < kend) fetch(k0 + kKeyBlock);
+    for (int j = 0; j < nblk; ++j) {
+        // this wave's loads of stage j are done once at most the later stages' remain
+        wait_later<2 * LPW, kStages - 2>(min(kStages - 2, nblk - 1 - j));   // 2 LPW loads per stage
+        lds_barrier();                                      // stage j landed; stage j-1 consumed
+        if (loader && j + kStages - 1 < nblk) issue(j + kStages - 1);
+        const char *sk = s_k[j % kStages];
+        const char *sv = s_v[j % kStages];
+        const int k0 = j * kKeyBlock;
 
-        // S^T[key][query] for the 64 keys: tile c holds keys 16c + 4g + j in element j
-        floatx4 st[4];
+        // S^T[key][query] for the block: tile c holds keys 16c + 4g + jj in element jj
+        floatx4 st[2];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < 2; ++c) {
+            const int row = 16 * c + l16;
+            u32x4 kf[DS];
+#pragma unroll
+            for (int s = 0; s < DS; ++s)
+                kf[s] = *reinterpret_cast<const u32x4 *>(sk + row * RB + ((4 * s + g) ^ swz_k<RB>(row)) * 16);
             st[c] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                const u32x4 kf = *reinterpret_cast<const u32x4 *>(s_k + (16 * c + l16) * KP + (32 * s + 8 * g) * 2);
-                st[c] = mfma(kf, qf[s], st[c]);
-            }
+            for (int s = 0; s < DS; ++s) st[c] = mfma(kf[s], qf[s], st[c]);
         }
         // online softmax over this block, for the query in this lane's column
         float bm = -INFINITY;
         if (k0 + kKeyBlock <= vis_min) {                     // wave-uniform: no key masked
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < 2; ++c)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    st[c][j] *= sc;
-                    bm = fmaxf(bm, st[c][j]);
+                for (int jj = 0; jj < 4; ++jj) {
+                    st[c][jj] *= sc;
+                    bm = fmaxf(bm, st[c][jj]);
                 }
         } else {
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < 2; ++c)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int key = k0 + 16 * c + 4 * g + j;
-                    st[c][j] = key < vis ? st[c][j] * sc : -INFINITY;
-                    bm = fmaxf(bm, st[c][j]);
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int key = k0 + 16 * c + 4 * g + jj;
+                    st[c][jj] = key < vis ? st[c][jj] * sc : -INFINITY;
+                    bm = fmaxf(bm, st[c][jj]);
                 }
         }
         bm = max_rows(bm);
@@ -247,30 +308,34 @@ __global__ __launch_bounds__(64 * kMaxWaves) void k_hybrid_attention(AttnArgs a)
         }
         // a lane whose keys so far are all masked keeps m = -inf and adds nothing
         const float mm = m == -INFINITY ? INFINITY : m;
-        uint32_t pk[4][2];                                   // P^T as bf16 pairs, tile c
+        uint32_t pk[2][2];                                   // P^T as bf16 pairs, tile c
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < 2; ++c) {
             float pv[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                pv[j] = __builtin_amdgcn_exp2f(st[c][j] - mm);
-                l += pv[j];
+            for (int jj = 0; jj < 4; ++jj) {
+                pv[jj] = __builtin_amdgcn_exp2f(st[c][jj] - mm);
+                l += pv[jj];
             }
             pk[c][0] = bf16_pair(pv[0], pv[1]);
             pk[c][1] = bf16_pair(pv[2], pv[3]);
         }
-        // O^T[d][query] += V^T[d][keys] P^T[keys][query]; step u covers tiles 2u, 2u+1
+        // O^T[d][query] += V^T[d][keys] P^T[keys][query].  The B operand of lane
+        // group g holds keys 4g + 0..3 and 16 + 4g + 0..3; the transposing reads give
+        // lane (g, d) the same keys of V column d: lane 4k + c of the group addresses
+        // key 4g + k (or 16 + 4g + k), values 16t + 4c .. 16t + 4c + 3.
+        const u32x4 pb{pk[0][0], pk[0][1], pk[1][0], pk[1][1]};
+        const int vr0 = 4 * g + (l16 >> 2), vr1 = vr0 + 16;
+        const int vb = 8 * (l16 & 3);
+        u32x2 lo[DT], hi[DT];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const u32x4 pb{pk[2 * u][0], pk[2 * u][1], pk[2 * u + 1][0], pk[2 * u + 1][1]};
-#pragma unroll
-            for (int t = 0; t < DT; ++t) {
-                const char *vr = s_vt + (16 * t + l16) * kVtPitch;
-                const u32x2 lo = *reinterpret_cast<const u32x2 *>(vr + (32 * u + 4 * g) * 2);
-                const u32x2 hi = *reinterpret_cast<const u32x2 *>(vr + (32 * u + 16 + 4 * g) * 2);
-                o[t] = mfma(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, o[t]);
-            }
+        for (int t = 0; t < DT; ++t) {
+            lo[t] = read_tr(sv + vr0 * RB + (t ^ swz_v<RB>(vr0)) * 32 + vb);
+            hi[t] = read_tr(sv + vr1 * RB + (t ^ swz_v<RB>(vr1)) * 32 + vb);
         }
+        lds_wait(lo, hi);
+#pragma unroll
+        for (int t = 0; t < DT; ++t) o[t] = mfma(u32x4{lo[t][0], lo[t][1], hi[t][0], hi[t][1]}, pb, o[t]);
     }
 
     l = sum_rows(l);

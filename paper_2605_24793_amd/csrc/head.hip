@@ -163,24 +163,31 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
         if (st + kRing - 1 < nst) issue(st + kRing - 1);   // refills the slot of stage st-1
         const char *sa = ring[st % kRing];
         const char *sb = sa + kHeadTileM * kStageBytes;
+        // every fragment of the stage is read before the first product, so the LDS
+        // latency is paid once per stage rather than once per k-step
+        constexpr int KS = kStageBytes / 64;                // 64-byte k-steps per stage
+        u32x4 av[KS][4], bv[KS][2];
 #pragma unroll
-        for (int kk = 0; kk < kStageBytes / 16; kk += 4) {
-            u32x4 av[4], bv[2];
+        for (int q = 0; q < KS; ++q) {
+            const int kk = 4 * q;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int row = wr * kWaveTile + r * 16 + l16;
-                av[r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+                av[q][r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
             }
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
                 const int row = wc * kWaveCols + c * 16 + l16;
-                bv[c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+                bv[q][c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
             }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < KS; ++q)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int c = 0; c < 2; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
-        }
+                for (int c = 0; c < 2; ++c) acc[r][c] = mma<DT>(av[q][r], bv[q][c], acc[r][c]);
     }
 
     // partial U of this k-slice: upart[ks][m][n]
