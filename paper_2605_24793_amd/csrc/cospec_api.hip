@@ -281,10 +281,12 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     }
     if (!do_arbitrate) return COSPEC_OK;
 
-    // 3. head, on the aux stream when given
+    // 3. head, on the aux stream when given; for chains the finish computes its
+    //    second layer (the logits of each sequence's mismatches) itself
     const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
+    const bool fuse_head = head && !c.is_tree;
+    HeadArgs ha{};
     if (head) {
-        HeadArgs ha{};
         ha.hidden = c.hidden;
         ha.n_rows = hidden_rows;
         ha.row0 = hidden_row0;
@@ -298,7 +300,9 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ha.ksplit = ksplit_for(m_cap, c.head);
         ha.upart = upart;
         ha.z = zlog;
-        if (launch_head(static_cast<Dtype>(c.head->dtype), ha, side) != hipSuccess) return COSPEC_ERR_HIP;
+        const Dtype hdt = static_cast<Dtype>(c.head->dtype);
+        if ((fuse_head ? launch_head_gemm(hdt, ha, side) : launch_head(hdt, ha, side)) != hipSuccess)
+            return COSPEC_ERR_HIP;
     }
     if (split_reduce && hipEventRecord(c.opts->aux_done, side) != hipSuccess) return COSPEC_ERR_HIP;
 
@@ -341,6 +345,9 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     fa.logp_action = F.logp_action;
     fa.policy_u = policy_u;
     fa.ws_logp_tgt = ws_logp;
+    fa.fuse_head = fuse_head;
+    fa.head_dt = head ? c.head->dtype : 0;
+    fa.hd = ha;
     if (rl) {
         fa.rl_on = 1;
         fa.rl_correct = rl->correct; fa.rl_alpha = rl->alpha; fa.rl_beta = rl->beta;

@@ -24,6 +24,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include "head_z.h"
 #include "launch.h"
 
 namespace cospec {
@@ -38,14 +39,6 @@ constexpr int kRing = 4;                          // LDS stages: three in flight
 constexpr int kWaveTile = 64;                    // rows of a wave's sub-tile
 constexpr int kWaveCols = 32;                    // columns of a wave's sub-tile
 constexpr int kGemmWaves = 8;                    // 2 x 4 waves per workgroup: two per SIMD
-
-template <int DT> __device__ inline float scalar_at(const void *p, int64_t i);
-template <> __device__ inline float scalar_at<kBF16>(const void *p, int64_t i) {
-    return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t *>(p)[i]) << 16);
-}
-template <> __device__ inline float scalar_at<kF32>(const void *p, int64_t i) {
-    return static_cast<const float *>(p)[i];
-}
 
 // One 64-byte k-step of a 16x16 tile: one 16-byte operand vector per lane.
 template <int DT> __device__ inline floatx4 mma(u32x4 a, u32x4 b, floatx4 c);
@@ -74,12 +67,7 @@ __device__ inline void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Hidden row of list entry m (see HeadArgs::row0).
-__device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
-    int64_t id = a.list ? static_cast<int64_t>(a.list[m]) : m;
-    if (a.row0 && id >= 0) id = a.row0[id / a.slots] + id % a.slots;
-    return id;
-}
+using headz::hidden_row;
 
 template <int DT>
 __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
@@ -208,43 +196,13 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
 }
 
 // z[m] = w2 . relu(sum_ks upart[ks][m] + b1) + b2, one wave per row, fixed order.
-// Every partial the lane needs is loaded before any is summed (h <= 64 * kEpiCols).
-constexpr int kEpiCols = 8;
 template <int DT>
 __global__ __launch_bounds__(256) void k_head_epilogue(HeadArgs a) {
     const int64_t M = a.count_dev ? static_cast<int64_t>(*a.count_dev) : a.count_host;
     const int64_t m = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
     if (m >= M) return;
-    const int lane = threadIdx.x & 63;
-    float acc = 0.f;
-    for (int n0 = 0; n0 < a.h; n0 += 64 * kEpiCols) {
-        float u[kEpiCols][kHeadMaxSplit];
-#pragma unroll
-        for (int i = 0; i < kEpiCols; ++i)
-#pragma unroll
-            for (int ks = 0; ks < kHeadMaxSplit; ++ks) {
-                const int n = n0 + i * 64 + lane;
-                u[i][ks] = (ks < a.ksplit && n < a.h)
-                               ? a.upart[(static_cast<int64_t>(ks) * a.m_cap + m) * a.h + n] : 0.f;
-            }
-#pragma unroll
-        for (int i = 0; i < kEpiCols; ++i) {
-            const int n = n0 + i * 64 + lane;
-            if (n < a.h) {
-                float v = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < kHeadMaxSplit; ++ks) v += u[i][ks];
-                const float bias = a.b1 ? scalar_at<DT>(a.b1, n) : 0.f;
-                acc += fmaxf(v + bias, 0.f) * scalar_at<DT>(a.w2, n);
-            }
-        }
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-    if (lane == 0) {
-        const int64_t id = hidden_row(a, m);
-        a.z[m] = id >= 0 && id < a.n_rows ? acc + a.b2 : NAN;
-    }
+    const float z = headz::head_z<DT>(a, m, threadIdx.x & 63);
+    if ((threadIdx.x & 63) == 0) a.z[m] = z;
 }
 
 __global__ __launch_bounds__(256) void k_arb_finish(ArbFinishArgs a) {
@@ -277,19 +235,23 @@ int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes) {
     return static_cast<int32_t>(ks);
 }
 
-hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s) {
+hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s) {
     const int64_t tiles = ((a.m_cap + kHeadTileM - 1) / kHeadTileM) * ((a.h + kHeadTileN - 1) / kHeadTileN);
     const dim3 grid(static_cast<unsigned>(tiles * a.ksplit));
     if (grid.x == 0) return hipSuccess;
-    const dim3 egrid(static_cast<unsigned>((a.m_cap + 3) / 4));
     const dim3 block(64 * kGemmWaves);
-    if (dt == kBF16) {
-        hipLaunchKernelGGL(k_head_gemm<kBF16>, grid, block, 0, s, a);
-        hipLaunchKernelGGL(k_head_epilogue<kBF16>, egrid, dim3(256), 0, s, a);
-    } else {
-        hipLaunchKernelGGL(k_head_gemm<kF32>, grid, block, 0, s, a);
-        hipLaunchKernelGGL(k_head_epilogue<kF32>, egrid, dim3(256), 0, s, a);
-    }
+    if (dt == kBF16) hipLaunchKernelGGL(k_head_gemm<kBF16>, grid, block, 0, s, a);
+    else hipLaunchKernelGGL(k_head_gemm<kF32>, grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s) {
+    const dim3 egrid(static_cast<unsigned>((a.m_cap + 3) / 4));
+    if (egrid.x == 0) return hipSuccess;
+    const hipError_t e = launch_head_gemm(dt, a, s);
+    if (e != hipSuccess) return e;
+    if (dt == kBF16) hipLaunchKernelGGL(k_head_epilogue<kBF16>, egrid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_head_epilogue<kF32>, egrid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -130,6 +130,11 @@ struct FinishArgs {
     int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
     int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent; float *logp_drf;
     float *z_tilde; float *policy; uint8_t *accept;
+    // chain only: the head's second layer is computed here from its k-slice partials
+    // (hd, head dtype head_dt) instead of being read from z
+    int32_t fuse_head;
+    int32_t head_dt;
+    HeadArgs hd;
 };
 
 // Speculative sampling baseline (k_sps_finish, k_sps_mass, k_sps_pick).
@@ -179,6 +184,7 @@ hipError_t launch_sample(Dtype dt, const SampleArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
+hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM only
 hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
 hipError_t launch_sps(Dtype dt, const SpsArgs &a, hipStream_t s);   // finish, weights, pick

@@ -23,6 +23,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
+
+#include "head_z.h"
 #include "launch.h"
 #include "rowstat.h"
 
@@ -38,9 +41,10 @@ struct Verdict {
 // log sigma(x) without overflow for either sign of x.
 __device__ inline float log_sigmoid(float x) { return fminf(x, 0.f) - log1pf(expf(-fabsf(x))); }
 
-// Verdict of one decision slot from its decide state and the head's logits: the
-// threshold (Eq. infer_thre), or with uniforms a sampled action (u < pi).
-__device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int head_ran, float lambda,
+// Verdict of one decision slot from its decide state and its head logit z (read
+// only when the head ran and the slot is in its list, pos >= 0): the threshold
+// (Eq. infer_thre), or with uniforms a sampled action (u < pi).
+__device__ inline Verdict verdict(uint8_t state, int pos, float z, int head_ran, float lambda,
                                   const float *pu, int64_t di) {
     Verdict v;
     if (state == kStateMatch) {
@@ -51,7 +55,6 @@ __device__ inline Verdict verdict(uint8_t state, int pos, const float *zs, int h
         // head skipped: lambda >= 1 or lambda < 0 decides every mismatch by itself
         v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
     } else {
-        const float z = zs[pos];
         const float pi = 1.0f / (1.0f + expf(-z));
         v.pass = pu ? pu[di] < pi : pi > lambda;
         v.z_tilde = z; v.policy = pi;
@@ -67,40 +70,60 @@ __device__ inline void write_drf(const FinishArgs &a, int64_t r, const RowStat &
     if (a.drf_ent) a.drf_ent[r] = rs.ent;
 }
 
+// The chain finish of sequence b by one wave, lane i-1 owning decision i, in two
+// parts: what needs no head logit (the loads, the draft-row statistics), then the
+// verdicts, the stop, the emission and the RL statistics.
+struct ChainLane {
+    uint8_t st;
+    int pos;          // list position of the decision, -1 if not in the head's list
+    float lpt;        // log p_T of the draft token
+    int tok_d, tok_t; // draft token of slot `lane`, target candidate of row `lane`
+};
+
 template <int DT>
-__global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
+__device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
     using E = Elt<DT>;
-    const int lane = threadIdx.x & 63;
-    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (b >= a.B) return;                                  // whole wave leaves together
     const int K = a.D;
     const int64_t di = static_cast<int64_t>(b) * K + lane;  // decision lane+1, draft row lane
-    bool fail = false, mism = false;
-    float lpt = NAN;
+    ChainLane c{kStateMatch, -1, NAN, -1, -1};
     if (lane < K) {
-        const uint8_t st = a.ws_state[di];
-        const bool valid = st != kStateReject;
-        mism = st != kStateMatch;
-        const float xd = valid ? E::at(a.drf + di * a.ld_bytes, a.tokens[di]) : 0.f;
+        c.st = a.ws_state[di];
+        const bool valid = c.st != kStateReject;
+        c.tok_d = a.tokens[di];
+        const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
         const RowStat rs = merge_row(a.partials + (a.drf_row0 + di) * a.splits, a.splits);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
-        const Verdict v = verdict(st, a.ws_listpos[di], a.z, a.head_ran, a.lambda, a.policy_u, di);
+        c.pos = a.ws_listpos[di];
+        c.lpt = a.ws_logp_tgt[di];
+    }
+    if (lane <= K) c.tok_t = a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + lane];
+    return c;
+}
+
+// z: the head logit of the lane's decision (read only when it is in the list).
+__device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const ChainLane &c, float z) {
+    const int K = a.D;
+    const int64_t di = static_cast<int64_t>(b) * K + lane;
+    bool fail = false;
+    const bool mism = lane < K && c.st != kStateMatch;
+    const float lpt = c.lpt;
+    if (lane < K) {
+        const Verdict v = verdict(c.st, c.pos, z, a.head_ran, a.lambda, a.policy_u, di);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
         if (a.policy) a.policy[di] = v.policy;
         if (a.accept) a.accept[di] = v.pass;
         if (a.logp_action) a.logp_action[di] = v.logp_action;
-        lpt = a.ws_logp_tgt[di];
     }
     const uint64_t rej = __ballot(fail);
     const int s = rej ? __builtin_ctzll(rej) + 1 : K + 1;
     if (lane == 0) a.accept_len[b] = s;
+    // slot j emits draft token j+1 before the stop, the target's token at it
     for (int j = lane; j <= K; j += 64) {
-        int tok = -1;
-        if (j < s - 1) tok = a.tokens[static_cast<int64_t>(b) * K + j];
-        else if (j == s - 1) tok = a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + j];
-        a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = tok;
+        const int td = j == lane ? c.tok_d : (j < K ? a.tokens[static_cast<int64_t>(b) * K + j] : -1);
+        const int tt = j == lane ? c.tok_t : a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + j];
+        a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = j < s - 1 ? td : j == s - 1 ? tt : -1;
     }
     if (!a.rl_on) return;
     // Section 3.2: effective actions up to the stop, rho, S_acc / S_rej and the
@@ -127,6 +150,48 @@ __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
         if (a.rl_rho) a.rl_rho[b] = rho;
         if (a.rl_return) a.rl_return[b] = J;
     }
+}
+
+// zd: the sequence's head logits by decision slot (computed by the calling kernel),
+// or null to read them from a.z by list position.
+template <int DT>
+__device__ inline void chain_finish_wave(const FinishArgs &a, int b, int lane, const float *zd) {
+    const ChainLane c = chain_prefix<DT>(a, b, lane);
+    const float z = lane >= a.D || !a.head_ran || c.pos < 0 ? NAN : zd ? zd[lane] : a.z[c.pos];
+    chain_suffix(a, b, lane, c, z);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (b >= a.B) return;                                  // whole wave leaves together
+    chain_finish_wave<DT>(a, b, threadIdx.x & 63, nullptr);
+}
+
+// One workgroup per sequence: wave 0 issues the finish's loads while waves
+// 1, 2, ... compute the head logits of the decision slots in the head's list (slot
+// t by wave 1 + t mod (waves - 1)); then wave 0 finishes the sequence.
+constexpr int kFinishWaves = 8;
+template <int DT>
+__global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishArgs a) {
+    __shared__ float s_z[64];                              // K <= 64
+    const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int waves = blockDim.x >> 6;                     // >= 2
+    ChainLane c{};
+    if (wave == 0) {
+        c = chain_prefix<DT>(a, b, lane);
+    } else {
+        for (int t = wave - 1; t < a.D; t += waves - 1) {
+            const int pos = a.ws_listpos[static_cast<int64_t>(b) * a.D + t];   // wave-uniform
+            if (pos >= 0) {
+                const float z = a.head_dt == kBF16 ? headz::head_z<kBF16>(a.hd, pos, lane)
+                                                   : headz::head_z<kF32>(a.hd, pos, lane);
+                if (lane == 0) s_z[t] = z;
+            }
+        }
+    }
+    __syncthreads();
+    if (wave == 0) chain_suffix(a, b, lane, c, lane < a.D && c.pos >= 0 ? s_z[lane] : NAN);
 }
 
 template <int DT>
@@ -175,8 +240,9 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
 
     int anc = -1, dep = 0, ok = 1;
     if (n < N) {
-        const Verdict v = verdict(st, a.ws_listpos[base + n], a.z, a.head_ran, a.lambda, a.policy_u,
-                                  base + n);
+        const int pos = a.ws_listpos[base + n];
+        const float z = !a.head_ran || pos < 0 ? NAN : a.z[pos];
+        const Verdict v = verdict(st, pos, z, a.head_ran, a.lambda, a.policy_u, base + n);
         if (n > 0) {
             anc = par;
             dep = 1;
@@ -249,9 +315,15 @@ hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s) {
         if (dt == kBF16) hipLaunchKernelGGL(k_tree_finish<kBF16>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
         else hipLaunchKernelGGL(k_tree_finish<kF32>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
     } else {
-        const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
-        if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish<kBF16>, dim3(blocks), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL(k_chain_finish<kF32>, dim3(blocks), dim3(256), 0, s, a);
+        if (a.fuse_head) {
+            const dim3 block(64 * std::min(a.D + 1, kFinishWaves));   // D >= 1 when the head ran
+            if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish_head<kBF16>, dim3(a.B), block, 0, s, a);
+            else hipLaunchKernelGGL(k_chain_finish_head<kF32>, dim3(a.B), block, 0, s, a);
+        } else {
+            const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
+            if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish<kBF16>, dim3(blocks), dim3(256), 0, s, a);
+            else hipLaunchKernelGGL(k_chain_finish<kF32>, dim3(blocks), dim3(256), 0, s, a);
+        }
     }
     return hipGetLastError();
 }
