@@ -159,10 +159,19 @@ __device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, La
             consume<NV>(x, v + u * kReduceThreads, st);
         }
     }
-    for (; v < v1; v += kReduceThreads) {
-        float x[NV];
-        E::unpack(__builtin_nontemporal_load(rv + v), x);
-        consume<NV>(x, v, st);
+    // the rest: at most kUnroll - 1 vectors per lane, every load issued before the
+    // first is used (one memory round trip, not one per vector)
+    u32x4 q[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        if (v + u * kReduceThreads < v1) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        if (v + u * kReduceThreads < v1) {
+            float x[NV];
+            E::unpack(q[u], x);
+            consume<NV>(x, v + u * kReduceThreads, st);
+        }
     }
 }
 
@@ -225,33 +234,52 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
         const float tot = transpose_sum8(m, lane);
         if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, st.ref);
     }
-    for (; w < v1; w += kReduceThreads) {
-        const bool ok = w + lane < v1;
-        float x[NV];
-        if (ok) {
-            E::unpack(__builtin_nontemporal_load(rv + w + lane), x);
-        } else {
+    // the rest: fewer than kUnroll segments of this wave, the last one possibly
+    // partial; every load is issued before the first is used
+    if (w < v1) {
+        u32x4 q[kUnroll];
 #pragma unroll
-            for (int k = 0; k < NV; ++k) x[k] = -INFINITY;
+        for (int u = 0; u < kUnroll; ++u)
+            if (w + u * kReduceThreads + lane < v1) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+        float m[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            m[u] = 0.f;
+            if (w + u * kReduceThreads >= v1) continue;            // wave-uniform: no such segment
+            const int vi = w + u * kReduceThreads + lane;
+            const bool ok = vi < v1;
+            float x[NV];
+            if (ok) {
+                E::unpack(q[u], x);
+            } else {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) x[k] = -INFINITY;
+            }
+            float cm = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
+            if (cm > st.best) { st.best = cm; st.chunk = vi; }
+            if (__ballot(cm > st.thresh) != 0) {
+                const float f = rescale_wave(st, cm);
+#pragma unroll
+                for (int j = 0; j < u; ++j) m[j] *= f;
+            }
+            const float nref = -st.ref;
+            float mu = 0.f;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                // lanes past the end add exp2(-huge) = 0 and 0 * (finite t) = 0
+                const float t = fmaf(ok ? x[k] : kFarBelow, kLog2e, nref);
+                const float e = __builtin_amdgcn_exp2f(t);
+                mu += e;
+                st.T = fmaf(e, t, st.T);
+            }
+            m[u] = mu;
+            st.S += mu;
         }
-        float cm = -INFINITY;
-#pragma unroll
-        for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
-        if (cm > st.best) { st.best = cm; st.chunk = w + lane; }
-        if (__ballot(cm > st.thresh) != 0) rescale_wave(st, cm);
-        const float nref = -st.ref;
-        float mu = 0.f;
-#pragma unroll
-        for (int k = 0; k < NV; ++k) {
-            // lanes past the end add exp2(-huge) = 0 and 0 * (finite t) = 0
-            const float t = fmaf(ok ? x[k] : kFarBelow, kLog2e, nref);
-            const float e = __builtin_amdgcn_exp2f(t);
-            mu += e;
-            st.T = fmaf(e, t, st.T);
-        }
-        st.S += mu;
-        const float tot = wave_sum_valu(mu);
-        if (lane == 0) seg[w / kSegVecs] = make_float2(tot, st.ref);
+        const float tot = transpose_sum8(m, lane);
+        const int ws = w + (lane >> 3) * kReduceThreads;           // segment of value lane >> 3
+        if ((lane & 7) == 0 && ws < v1) seg[ws / kSegVecs] = make_float2(tot, st.ref);
     }
 }
 
