@@ -58,6 +58,16 @@ typedef __attribute__((address_space(3))) char lds_char;
 // Waits until at most N vector-memory operations of this wave are outstanding.
 template <int N> __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
+// Waits until this wave has at most PER * later of its loads in flight, later <= MAXL.
+template <int PER, int MAXL> __device__ inline void wait_later(int later) {
+    if constexpr (MAXL > 0) {
+        if (later >= MAXL) wait_vm<PER * MAXL>();
+        else wait_later<PER, MAXL - 1>(later);
+    } else {
+        wait_vm<0>();
+    }
+}
+
 // Workgroup barrier without the memory fence of __syncthreads (which would also wait
 // for the stages still in flight); LDS writes of this wave are drained first and the
 // compiler may not move memory accesses across it.
@@ -143,10 +153,7 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
         if (st < nst) issue(st);
     for (int st = 0; st < nst; ++st) {
         // this wave's loads of stage st are done once at most the later stages' remain
-        const int later = min(kRing - 2, nst - 1 - st);
-        if (later >= 2) wait_vm<8>();                 // 4 loads per wave and stage
-        else if (later == 1) wait_vm<4>();
-        else wait_vm<0>();
+        wait_later<4, kRing - 2>(min(kRing - 2, nst - 1 - st));   // 4 loads per wave and stage
         lds_barrier();                            // every wave's part of stage st has landed
         if (st + kRing - 1 < nst) issue(st + kRing - 1);   // refills the slot of stage st-1
         const char *sa = ring[st % kRing];
