@@ -34,6 +34,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
 constexpr int64_t kAutoBlocks = 2048;         // aim: 8 workgroups per CU on 256 CUs
+constexpr int kOverlapBlocksPerCU = 3;        // draft-row reduction beside the aux stream
 
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -102,6 +103,41 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     L.z = off;        off += round_up(static_cast<size_t>(m_cap) * 4);
     L.total = off;
     return L;
+}
+
+// The draft-row reduction beside the aux stream's kernels (decide, head GEMM): a grid of
+// kOverlapBlocksPerCU workgroups per CU, so that each SIMD keeps three reduction waves
+// (measured: the same bandwidth as a full grid) and has wave slots, registers and LDS
+// left for a head GEMM workgroup.  The split count, among those whose partials fit,
+// minimises the longest workgroup's work: rounds over the grid times vectors per unit.
+struct DraftPlan {
+    int32_t splits, blocks;
+};
+
+// Compute units of the current device (MI355X: 256).
+int32_t cu_count() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 256;
+    return cus;
+}
+
+DraftPlan draft_plan(int64_t rows, int64_t nvec, int64_t free_slots) {
+    const int64_t cap = static_cast<int64_t>(kOverlapBlocksPerCU) * cu_count();
+    DraftPlan best{1, static_cast<int32_t>(rows < cap ? rows : cap)};
+    int64_t best_cost = INT64_MAX;
+    for (int64_t sp = 1; sp <= COSPEC_MAX_SPLITS; ++sp) {
+        const int64_t units = rows * sp;
+        if (units > free_slots || units > INT32_MAX || (sp > 1 && nvec / sp < kReduceThreads)) break;
+        const int64_t blocks = units < cap ? units : cap;
+        const int64_t cost = (units + blocks - 1) / blocks * ((nvec + sp - 1) / sp);
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = DraftPlan{static_cast<int32_t>(sp), static_cast<int32_t>(blocks)};
+        }
+    }
+    return best;
 }
 
 int32_t auto_splits(int64_t rows, int64_t nvec) {
@@ -219,10 +255,41 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     // 1. target rows; the draft rows too in the same launch unless the head overlaps
     //    their reduction on the aux stream (one launch is cheaper than two)
     const bool split_reduce = aux && head;
+    const int64_t n_drf = static_cast<int64_t>(c.B) * c.RD;
+    const int64_t drf_base = static_cast<int64_t>(ra.n_tgt_rows) * splits;   // first draft partial
+    DraftPlan dp{splits, 0};
+    if (split_reduce) {
+        dp = c.opts->splits ? DraftPlan{splits, kOverlapBlocksPerCU * cu_count()}   // override: as given
+                            : draft_plan(n_drf, nvec, L.partial_slots - drf_base);
+    }
     // The decision work (sampling, decide, head) runs on the aux stream when given,
     // overlapping the draft-row reduction; otherwise everything is on `stream`.
     hipStream_t side = c.stream;
     if (do_reduce) {
+    // the decide step's arguments (its launch follows the reductions)
+    DecideArgs da{};
+    da.tgt = ra.tgt;
+    da.ld_bytes = ra.ld_bytes;
+    da.V = c.V;
+    da.B = c.B;
+    da.RT = static_cast<int32_t>(c.RT);
+    da.D = static_cast<int32_t>(c.D);
+    da.is_tree = c.is_tree;
+    da.parent = c.parent;
+    da.tokens = c.tokens;
+    da.partials = partials;
+    da.splits = splits;
+    da.score_mismatch = phase == kReducePhase ? decisions : head;   // phase 2 may need the list
+    da.sampled = uniform != nullptr;
+    da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
+    da.tgt_cand = F.tgt_candidate;
+    da.logp_tgt = F.logp_tgt; da.delta = F.delta;
+    da.ws_tgt_arg = tgt_arg;
+    da.ws_logp_tgt = ws_logp;
+    da.ws_state = state;
+    da.ws_listpos = listpos;
+    da.ws_list = list;
+    da.ws_count = count;
     ReduceArgs rt = ra;
     rt.row_offset = 0;
     rt.n_rows = split_reduce ? ra.n_tgt_rows : static_cast<int32_t>(c.B * (c.RT + c.RD));
@@ -254,29 +321,6 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     }
 
     // 2. decide
-    DecideArgs da{};
-    da.tgt = ra.tgt;
-    da.ld_bytes = ra.ld_bytes;
-    da.V = c.V;
-    da.B = c.B;
-    da.RT = static_cast<int32_t>(c.RT);
-    da.D = static_cast<int32_t>(c.D);
-    da.is_tree = c.is_tree;
-    da.parent = c.parent;
-    da.tokens = c.tokens;
-    da.partials = partials;
-    da.splits = splits;
-    da.score_mismatch = phase == kReducePhase ? decisions : head;   // phase 2 may need the list
-    da.sampled = uniform != nullptr;
-    da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
-    da.tgt_cand = F.tgt_candidate;
-    da.logp_tgt = F.logp_tgt; da.delta = F.delta;
-    da.ws_tgt_arg = tgt_arg;
-    da.ws_logp_tgt = ws_logp;
-    da.ws_state = state;
-    da.ws_listpos = listpos;
-    da.ws_list = list;
-    da.ws_count = count;
     if (launch_decide(dt, da, side) != hipSuccess) return COSPEC_ERR_HIP;
     }
     if (!do_arbitrate) return COSPEC_OK;
@@ -306,12 +350,16 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     }
     if (split_reduce && hipEventRecord(c.opts->aux_done, side) != hipSuccess) return COSPEC_ERR_HIP;
 
-    // 4. draft rows (features only), when they were not reduced with the target rows
+    // 4. draft rows (features only), when they were not reduced with the target rows:
+    //    a capped grid, so that the aux stream's kernels find room on every CU
     ReduceArgs rd = ra;
     rd.row_offset = ra.n_tgt_rows;
-    rd.n_rows = split_reduce ? static_cast<int32_t>(c.B * c.RD) : 0;   // only in a whole step
+    rd.n_rows = split_reduce ? static_cast<int32_t>(n_drf) : 0;   // only in a whole step
     rd.reset_counter = nullptr;
-    rd.leave_room = split_reduce;          // one wave slot per SIMD stays free for the aux stream
+    rd.splits = dp.splits;
+    rd.vec_per_split = static_cast<int32_t>((nvec + dp.splits - 1) / dp.splits);
+    rd.part_base = drf_base;
+    rd.max_blocks = dp.blocks;
     if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (!record(c.opts ? c.opts->reduce2_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
@@ -329,9 +377,8 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     fa.is_tree = c.is_tree;
     fa.parent = c.parent;
     fa.tokens = c.tokens;
-    fa.partials = partials;
-    fa.splits = splits;
-    fa.drf_row0 = static_cast<int64_t>(c.B) * c.RT;
+    fa.drf_partials = partials + drf_base;
+    fa.drf_splits = split_reduce ? dp.splits : splits;
     fa.ws_state = state;
     fa.ws_listpos = listpos;
     fa.z = zlog;

@@ -22,42 +22,6 @@ enum Dtype : int32_t { kF32 = 0, kBF16 = 1 };
 // Per-decision state byte written by the decide kernel.
 enum : uint8_t { kStateMismatch = 0, kStateMatch = 1, kStateReject = 2 };
 
-struct ReduceArgs {
-    const char *tgt;           // target rows
-    const char *drf;           // draft rows
-    int64_t ld_bytes;          // row stride in bytes (multiple of 16)
-    int32_t V;
-    int32_t n_tgt_rows;        // B * target rows per sequence; rows past it are draft rows
-    int32_t row_offset;        // first row of this launch (target rows, then draft rows)
-    int32_t n_rows;            // rows in this launch
-    const int32_t *parent;     // tree: [B][N]; draft rows of leaves are skipped
-    int32_t N;                 // tree nodes per tree
-    int32_t splits;            // workgroups per row
-    int32_t vec_per_split;     // 16-byte vectors per split
-    float4 *partials;          // [rows][splits] {max, argmax bits, S, T}
-    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter), or null
-    float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
-                               // target row, or null; needs vec_per_split % kSegVecs == 0
-    int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
-    int32_t leave_room;        // cap the kernel at 7 waves per SIMD so that another stream's
-                               // workgroups find a slot on every CU
-};
-
-// Temperature-1 candidates: one wave per target row inverts its uniform through
-// the segment masses, then through the elements of the segment it lands in.
-struct SampleArgs {
-    const char *tgt;
-    int64_t ld_bytes;
-    int32_t V;
-    int32_t n_rows;            // target rows
-    const float4 *partials;
-    int32_t splits;
-    const float2 *seg;
-    int32_t nseg;
-    const float *uniform;      // [n_rows]
-    int32_t *cand;             // [n_rows] out
-};
-
 struct DecideArgs {
     const char *tgt;
     int64_t ld_bytes;
@@ -81,6 +45,45 @@ struct DecideArgs {
     int32_t *ws_list;          // [B*D] compacted hidden-row ids
     int32_t *ws_count;         // compacted length M
 };
+
+struct ReduceArgs {
+    const char *tgt;           // target rows
+    const char *drf;           // draft rows
+    int64_t ld_bytes;          // row stride in bytes (multiple of 16)
+    int32_t V;
+    int32_t n_tgt_rows;        // B * target rows per sequence; rows past it are draft rows
+    int32_t row_offset;        // first row of this launch (target rows, then draft rows)
+    int32_t n_rows;            // rows in this launch
+    const int32_t *parent;     // tree: [B][N]; draft rows of leaves are skipped
+    int32_t N;                 // tree nodes per tree
+    int32_t splits;            // units per row of this launch
+    int32_t vec_per_split;     // 16-byte vectors per split
+    float4 *partials;          // {max, argmax bits, S, T} per unit
+    int64_t part_base;         // slot of the launch's first unit; unit u (split fastest)
+                               // writes partials[part_base + u]
+    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter), or null
+    float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
+                               // target row, or null; needs vec_per_split % kSegVecs == 0
+    int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
+    int32_t max_blocks;        // grid cap (0 = one workgroup per unit): each workgroup then
+                               // takes every max_blocks-th unit
+};
+
+// Temperature-1 candidates: one wave per target row inverts its uniform through
+// the segment masses, then through the elements of the segment it lands in.
+struct SampleArgs {
+    const char *tgt;
+    int64_t ld_bytes;
+    int32_t V;
+    int32_t n_rows;            // target rows
+    const float4 *partials;
+    int32_t splits;
+    const float2 *seg;
+    int32_t nseg;
+    const float *uniform;      // [n_rows]
+    int32_t *cand;             // [n_rows] out
+};
+
 
 struct HeadArgs {
     const void *hidden;        // [n_rows][d]
@@ -110,9 +113,8 @@ struct FinishArgs {
     int32_t is_tree;
     const int32_t *parent;     // tree only
     const int32_t *tokens;     // chain [B][K], tree [B][N]
-    const float4 *partials;
-    int32_t splits;
-    int64_t drf_row0;          // partial-row index of draft row 0 (= B * RT)
+    const float4 *drf_partials; // partials of the draft rows: draft row j (B * RD of them)
+    int32_t drf_splits;         // owns drf_partials[j * drf_splits, (j + 1) * drf_splits)
     const uint8_t *ws_state;
     const int32_t *ws_listpos;
     const float *z;            // head logits by compacted position

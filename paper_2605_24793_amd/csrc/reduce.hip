@@ -28,6 +28,11 @@
 #include "launch.h"
 #include "rowstat.h"
 
+// Products and sums are rounded as written in this file: the references (x * log2e
+// rounded) must be the same numbers in every kernel that forms them, so no
+// multiply-add may be fused unless written as fmaf.
+#pragma clang fp contract(off)
+
 namespace cospec {
 namespace {
 
@@ -100,16 +105,6 @@ __device__ inline float swap32_sum(float x, float y) {
 __device__ inline float swap16_sum(float x, float y) {
     const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
     return __uint_as_float(p[0]) + __uint_as_float(p[1]);
-}
-
-// Whole-wave sum in every lane.
-__device__ inline float wave_sum_valu(float x) {
-    x += dpp<kDppXor1>(x);
-    x += dpp<kDppXor2>(x);
-    x += dpp<kDppXor7>(x);
-    x += dpp<kDppXor15>(x);
-    x = swap16_sum(x, x);
-    return swap32_sum(x, x);
 }
 
 __device__ inline float wave_max_valu(float x) {
@@ -283,16 +278,12 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
     }
 }
 
-template <int DT, bool SEG, bool ROOM>
-__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
-    // ROOM: claim registers up to v71 so that at most 7 waves per SIMD are resident
-    if (ROOM) asm volatile("" ::: "v71");
+// One unit of work: split `split` of row `row`, whose partial goes to slot `slot`.
+template <int DT, bool SEG>
+__device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int split, int64_t slot) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     const int tid = threadIdx.x;
-    const int row = a.row_offset + static_cast<int>(blockIdx.x) / a.splits;
-    const int split = static_cast<int>(blockIdx.x) % a.splits;
-    if (blockIdx.x == 0 && tid == 0 && a.reset_counter) *a.reset_counter = 0;
 
     const char *rp;
     if (row < a.n_tgt_rows) {
@@ -399,8 +390,21 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     if (tid == 0) {
         float SS = s_S[0], TT = s_T[0];
         for (int w = 1; w < kReduceThreads / 64; ++w) { SS += s_S[w]; TT += s_T[w]; }
-        a.partials[static_cast<int64_t>(row) * a.splits + split] =
-            make_float4(M, __int_as_float(s_idx[0]), SS, TT);
+        a.partials[slot] = make_float4(M, __int_as_float(s_idx[0]), SS, TT);
+    }
+}
+
+// Units are (row, split) pairs of the launch's rows, split fastest.  Normally there is
+// one workgroup per unit; with a capped grid each workgroup takes every gridDim.x-th
+// unit, which bounds how many of its waves share a CU with another stream's kernels.
+template <int DT, bool SEG>
+__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.reset_counter) *a.reset_counter = 0;
+    const int units = a.n_rows * a.splits;
+    for (int u = blockIdx.x; u < units; u += gridDim.x) {
+        const int r = u / a.splits, split = u - r * a.splits;
+        reduce_unit<DT, SEG>(a, a.row_offset + r, split, a.part_base + u);
+        __syncthreads();            // the workgroup's LDS is reused by the next unit
     }
 }
 
@@ -491,17 +495,14 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
 template <int DT>
 void launch_reduce_t(const ReduceArgs &a, dim3 grid, hipStream_t s) {
     const bool seg = a.seg && a.row_offset < a.n_tgt_rows;
-    if (a.leave_room) {
-        if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true, true>), grid, dim3(kReduceThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_vocab_reduce<DT, false, true>), grid, dim3(kReduceThreads), 0, s, a);
-    } else {
-        if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true, false>), grid, dim3(kReduceThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_vocab_reduce<DT, false, false>), grid, dim3(kReduceThreads), 0, s, a);
-    }
+    if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true>), grid, dim3(kReduceThreads), 0, s, a);
+    else hipLaunchKernelGGL((k_vocab_reduce<DT, false>), grid, dim3(kReduceThreads), 0, s, a);
 }
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(a.n_rows) * a.splits));
+    int64_t units = static_cast<int64_t>(a.n_rows) * a.splits;
+    if (a.max_blocks > 0 && units > a.max_blocks) units = a.max_blocks;
+    const dim3 grid(static_cast<unsigned>(units));
     if (grid.x == 0) return hipSuccess;
     if (dt == kBF16) launch_reduce_t<kBF16>(a, grid, s);
     else launch_reduce_t<kF32>(a, grid, s);

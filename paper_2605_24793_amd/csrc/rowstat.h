@@ -60,8 +60,12 @@ struct RowStat {
     int arg;
 };
 
-// Fixed-order merge of one row's split partials.
+// Fixed-order merge of one row's split partials.  Every operation is rounded as
+// written (fma only where written, no contraction by the compiler), so that the
+// kernels that inline it (decide, the reduction's fused decide, finish, sampling)
+// give bit-identical statistics for the same partials.
 __device__ inline RowStat merge_row(const float4 *p, int splits) {
+#pragma clang fp contract(off)
     float M = -INFINITY;
     int arg = INT_MAX;
     for (int s = 0; s < splits; ++s) {
@@ -73,10 +77,11 @@ __device__ inline RowStat merge_row(const float4 *p, int splits) {
     for (int s = 0; s < splits; ++s) {
         const float4 q = p[s];
         if (q.z > 0.f) {
-            const float dr = __fmul_rn(q.x, kLog2e) - R;     // the split's reference, as k_vocab_reduce rounded it
+            const float dr = __fmul_rn(q.x, kLog2e) - R;   // the split's reference, as
+                                                           // k_vocab_reduce rounded it
             const float f = __builtin_amdgcn_exp2f(dr);
-            S += f * q.z;
-            T += f * fmaf(dr, q.z, q.w);
+            S = fmaf(f, q.z, S);
+            T = fmaf(f, fmaf(dr, q.z, q.w), T);
         }
     }
     // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the

@@ -91,7 +91,7 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
         const bool valid = c.st != kStateReject;
         c.tok_d = a.tokens[di];
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
-        const RowStat rs = merge_row(a.partials + (a.drf_row0 + di) * a.splits, a.splits);
+        const RowStat rs = merge_row(a.drf_partials + di * a.drf_splits, a.drf_splits);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
         c.pos = a.ws_listpos[di];
@@ -231,7 +231,7 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
     // draft rows were reduced for nodes with a child only
     if (n < N) {
         RowStat rs{NAN, NAN, NAN, NAN, -1};
-        if (s_child[n]) rs = merge_row(a.partials + (a.drf_row0 + base + n) * a.splits, a.splits);
+        if (s_child[n]) rs = merge_row(a.drf_partials + (base + n) * a.drf_splits, a.drf_splits);
         write_drf(a, base + n, rs);
         s_dmax[n] = rs.max;
         s_dlogs[n] = rs.log_s;

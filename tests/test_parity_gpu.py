@@ -278,19 +278,35 @@ def test_always_accept_on_gpu(lam):
     assert torch.equal(gpu["tokens"][:, : wl.K], wl.draft_tokens)
 
 
-def test_overlap_stream_gives_identical_results():
+# Beside the aux stream the draft rows may be reduced in another number of splits,
+# which changes the fp32 summation order of their sums and nothing else.
+_DRAFT_SUMS = ("drf_lse", "drf_entropy", "logp_drf")
+
+
+def _same_up_to_draft_sums(a, b):
+    for k in a:
+        if k in _DRAFT_SUMS:
+            torch.testing.assert_close(a[k], b[k], rtol=1e-5, atol=1e-5, equal_nan=True)
+        else:
+            assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
+                               b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
+
+
+def test_overlap_stream_gives_the_same_results():
     wl = workloads.make_chain(B=40, K=7, V=30001, d=256, h=128, seed=12, bias=True, noise=1.2)
     a = _gpu_block(wl, 0.5)
     b = _gpu_block(wl, 0.5, overlap=True)
-    for k in a:
-        assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
-                           b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
+    _same_up_to_draft_sums(a, b)
+    parity.check_block(b, _ref_block(wl, 0.5))
+    # the large chain batch's shape: target rows in one launch, the draft rows in
+    # another beside the head, each compared with the serial step on every sequence
+    big = workloads.make_chain(B=256, K=7, V=151936 // 8, d=512, h=128, seed=14, noise=1.0)
+    _same_up_to_draft_sums(_gpu_block(big, 0.5), _gpu_block(big, 0.5, overlap=True))
     tr = workloads.make_random_tree(B=6, N=40, V=3001, d=64, h=32, seed=13, bias=True)
     a = _gpu_tree(tr, 0.5)
     b = _gpu_tree(tr, 0.5, overlap=True)
-    for k in a:
-        assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
-                           b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
+    _same_up_to_draft_sums(a, b)
+    parity.check_tree(b, _ref_tree(tr, 0.5))
 
 
 @pytest.mark.parametrize("logit_dtype,head_dtype", [("bf16", "f32"), ("f32", "bf16")])
