@@ -420,6 +420,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     __shared__ int s_targ[kMaxSeqRows];
     __shared__ int s_wave_cnt[kDecideThreads / 64];
     __shared__ int s_base;
+    __shared__ float4 s_parts[kStageParts];
 
     // this thread's decision slot (D <= kDecideThreads): chain slot t is decision t+1,
     // verified by target row t; tree slot t is node t, verified by its parent's row.
@@ -438,9 +439,17 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
             xt = E::at(a.tgt + (static_cast<int64_t>(b) * a.RT + p) * a.ld_bytes, tok);
         }
     }
+    // the sequence's target partials are contiguous: staged in LDS when rows are split
+    const int64_t np = static_cast<int64_t>(a.RT) * a.splits;
+    const float4 *seq_parts = a.partials + static_cast<int64_t>(b) * np;
+    const bool staged = a.splits > 1 && np <= kStageParts;
+    if (staged) {
+        stage_partials(seq_parts, np, s_parts, t, kDecideThreads);
+        __syncthreads();
+    }
     for (int j = t; j < a.RT; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RT + j;
-        const RowStat rs = merge_row(a.partials + r * a.splits, a.splits);
+        const RowStat rs = merge_row((staged ? s_parts : seq_parts) + static_cast<int64_t>(j) * a.splits, a.splits);
         // the verification candidate: the argmax, or the temperature-1 sample
         // k_sample left in ws_tgt_arg
         const int cand = a.sampled ? a.ws_tgt_arg[r] : rs.arg;

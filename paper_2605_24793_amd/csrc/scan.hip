@@ -80,18 +80,29 @@ struct ChainLane {
     int tok_d, tok_t; // draft token of slot `lane`, target candidate of row `lane`
 };
 
+// stage: LDS room for `cap` partials of this wave, into which the sequence's draft-row
+// partials are copied first when the rows are split (and they fit).
 template <int DT>
-__device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
+__device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, float4 *stage, int cap) {
     using E = Elt<DT>;
     const int K = a.D;
     const int64_t di = static_cast<int64_t>(b) * K + lane;  // decision lane+1, draft row lane
+    const int64_t np = static_cast<int64_t>(K) * a.drf_splits;
+    const float4 *seq_parts = a.drf_partials + static_cast<int64_t>(b) * np;
+    const bool staged = a.drf_splits > 1 && np <= cap;
+    if (staged) {                 // one wave writes and then reads: LDS keeps the wave's order
+        stage_partials(seq_parts, np, stage, lane, 64);
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+    }
     ChainLane c{kStateMatch, -1, NAN, -1, -1};
     if (lane < K) {
         c.st = a.ws_state[di];
         const bool valid = c.st != kStateReject;
         c.tok_d = a.tokens[di];
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
-        const RowStat rs = merge_row(a.drf_partials + di * a.drf_splits, a.drf_splits);
+        const RowStat rs =
+            merge_row((staged ? stage : seq_parts) + static_cast<int64_t>(lane) * a.drf_splits, a.drf_splits);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
         c.pos = a.ws_listpos[di];
@@ -155,17 +166,20 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
 // zd: the sequence's head logits by decision slot (computed by the calling kernel),
 // or null to read them from a.z by list position.
 template <int DT>
-__device__ inline void chain_finish_wave(const FinishArgs &a, int b, int lane, const float *zd) {
-    const ChainLane c = chain_prefix<DT>(a, b, lane);
+__device__ inline void chain_finish_wave(const FinishArgs &a, int b, int lane, const float *zd, float4 *stage,
+                                         int cap) {
+    const ChainLane c = chain_prefix<DT>(a, b, lane, stage, cap);
     const float z = lane >= a.D || !a.head_ran || c.pos < 0 ? NAN : zd ? zd[lane] : a.z[c.pos];
     chain_suffix(a, b, lane, c, z);
 }
 
 template <int DT>
 __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
+    constexpr int kCap = kStageParts / 4;
+    __shared__ float4 s_parts[4][kCap];
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= a.B) return;                                  // whole wave leaves together
-    chain_finish_wave<DT>(a, b, threadIdx.x & 63, nullptr);
+    chain_finish_wave<DT>(a, b, threadIdx.x & 63, nullptr, s_parts[threadIdx.x >> 6], kCap);
 }
 
 // One workgroup per sequence: wave 0 issues the finish's loads while waves
@@ -175,11 +189,12 @@ constexpr int kFinishWaves = 8;
 template <int DT>
 __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishArgs a) {
     __shared__ float s_z[64];                              // K <= 64
+    __shared__ float4 s_parts[kStageParts];
     const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int waves = blockDim.x >> 6;                     // >= 2
     ChainLane c{};
     if (wave == 0) {
-        c = chain_prefix<DT>(a, b, lane);
+        c = chain_prefix<DT>(a, b, lane, s_parts, kStageParts);
     } else {
         for (int t = wave - 1; t < a.D; t += waves - 1) {
             const int pos = a.ws_listpos[static_cast<int64_t>(b) * a.D + t];   // wave-uniform
