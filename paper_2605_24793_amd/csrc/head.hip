@@ -229,14 +229,16 @@ __global__ __launch_bounds__(256) void k_arb_finish(ArbFinishArgs a) {
 
 }  // namespace
 
+// k-slices of d: one per XCD (each XCD's L2 then holds one slice of the hidden rows
+// and of W1), more, in multiples of the XCD count, while the tiles times slices stay
+// below one workgroup per CU; never more than there are stages of d.
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes) {
     const int64_t mt = (m_cap + kHeadTileM - 1) / kHeadTileM;
     const int64_t nt = (h + kHeadTileN - 1) / kHeadTileN;
     if (mt * nt <= 0) return 1;                        // no rows: nothing to split
     const int64_t stages = (static_cast<int64_t>(d) * elem_bytes + kStageBytes - 1) / kStageBytes;
-    int64_t ks = (kHeadTargetBlocks + mt * nt - 1) / (mt * nt);
-    if (ks < kXcds) ks = kXcds;                         // one k-slice per XCD (L2 locality)
-    if (ks > kHeadMaxSplit) ks = kHeadMaxSplit;
+    int64_t ks = kXcds;
+    while (ks + kXcds <= kHeadMaxSplit && mt * nt * (ks + kXcds) <= kHeadTargetBlocks) ks += kXcds;
     if (ks > stages) ks = stages;
     if (ks < 1) ks = 1;
     return static_cast<int32_t>(ks);

@@ -29,38 +29,51 @@ __device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
     return id;
 }
 
-constexpr int kEpiCols = 8;   // columns per lane per pass: every partial a lane needs is
-                              // loaded before any is summed (h <= 64 * kEpiCols per pass)
-
-// z of list entry m, in every lane of the calling wave; NaN when its hidden row is
-// outside [0, n_rows).
-template <int DT>
-__device__ inline float head_z(const HeadArgs &a, int64_t m, int lane) {
+// One pass of a lane covers CPL columns (lane, lane + 64, ...) and loads SPL k-slice
+// partials of each together, CPL * SPL = 64 loads in flight; narrow heads take fewer
+// columns and more slices per pass.
+template <int DT, int CPL>
+__device__ inline float head_z_cols(const HeadArgs &a, int64_t m, int lane) {
+    constexpr int SPL = 64 / CPL;
     float acc = 0.f;
-    for (int n0 = 0; n0 < a.h; n0 += 64 * kEpiCols) {
-        float u[kEpiCols][kHeadMaxSplit];
+    for (int n0 = 0; n0 < a.h; n0 += 64 * CPL) {
+        float v[CPL];
 #pragma unroll
-        for (int i = 0; i < kEpiCols; ++i)
+        for (int i = 0; i < CPL; ++i) v[i] = 0.f;
+        for (int k0 = 0; k0 < a.ksplit; k0 += SPL) {
+            float u[CPL][SPL];
 #pragma unroll
-            for (int ks = 0; ks < kHeadMaxSplit; ++ks) {
-                const int n = n0 + i * 64 + lane;
-                u[i][ks] = (ks < a.ksplit && n < a.h)
-                               ? a.upart[(static_cast<int64_t>(ks) * a.m_cap + m) * a.h + n] : 0.f;
-            }
+            for (int i = 0; i < CPL; ++i)
 #pragma unroll
-        for (int i = 0; i < kEpiCols; ++i) {
+                for (int k = 0; k < SPL; ++k) {
+                    const int n = n0 + i * 64 + lane;
+                    u[i][k] = (k0 + k < a.ksplit && n < a.h)
+                                  ? a.upart[(static_cast<int64_t>(k0 + k) * a.m_cap + m) * a.h + n] : 0.f;
+                }
+#pragma unroll
+            for (int i = 0; i < CPL; ++i)
+#pragma unroll
+                for (int k = 0; k < SPL; ++k) v[i] += u[i][k];
+        }
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
             const int n = n0 + i * 64 + lane;
             if (n < a.h) {
-                float v = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < kHeadMaxSplit; ++ks) v += u[i][ks];
                 const float bias = a.b1 ? scalar_at<DT>(a.b1, n) : 0.f;
-                acc += fmaxf(v + bias, 0.f) * scalar_at<DT>(a.w2, n);
+                acc = fmaf(fmaxf(v[i] + bias, 0.f), scalar_at<DT>(a.w2, n), acc);
             }
         }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+// z of list entry m, in every lane of the calling wave; NaN when its hidden row is
+// outside [0, n_rows).  Each column's k-slices are summed in slice order.
+template <int DT>
+__device__ inline float head_z(const HeadArgs &a, int64_t m, int lane) {
+    const float acc = a.h <= 256 ? head_z_cols<DT, 4>(a, m, lane) : head_z_cols<DT, 8>(a, m, lane);
     const int64_t id = hidden_row(a, m);
     return id >= 0 && id < a.n_rows ? acc + a.b2 : NAN;
 }

@@ -11,8 +11,9 @@ constexpr int kReduceThreads = 256;   // vocabulary-reduction workgroup
 constexpr int kDecideThreads = 256;   // one workgroup per sequence / tree
 constexpr int kHeadTileM = 128;       // head GEMM workgroup tile: rows
 constexpr int kHeadTileN = 128;       //                            columns of W1
-constexpr int kHeadTargetBlocks = 512; // k-splits are added until the grid reaches this
-constexpr int kHeadMaxSplit = 8;
+constexpr int kHeadTargetBlocks = 64;  // small heads: k-slices are added (in steps of the
+                                       // XCD count) until the active grid reaches this
+constexpr int kHeadMaxSplit = 32;
 constexpr int kXcds = 8;             // MI355X: 8 XCDs, each with its own L2
 constexpr int kMaxSeqRows = 256;      // rows per sequence / nodes per tree held in LDS
 constexpr int kSegVecs = 64;          // 16-byte vectors per probability-mass segment (one wave load)

@@ -63,72 +63,37 @@ struct RowStat {
 // Fixed-order merge of one row's split partials.  Every operation is rounded as
 // written (fma only where written, no contraction by the compiler), so that the
 // kernels that inline it (decide, finish, sampling) give bit-identical statistics for
-// the same partials.  The partials are loaded kMergeChunk at a time with every load of
-// a chunk in flight together (a row split many ways costs a few memory round trips,
-// not one per split); the arithmetic runs over s = 0, 1, ... in order either way.
-constexpr int kMergeChunk = 16;
-
-struct MergeAcc {
-    float M = -INFINITY;
-    int arg = INT_MAX;
-    float R = 0.f, S = 0.f, T = 0.f;
-};
-
-__device__ inline void merge_max(MergeAcc &m, float4 q) {
-    if (q.z > 0.f && q.x > m.M) { m.M = q.x; m.arg = __float_as_int(q.y); }   // earlier split wins ties
-}
-
-__device__ inline void merge_sum(MergeAcc &m, float4 q) {
-#pragma clang fp contract(off)
-    if (q.z > 0.f) {
-        const float dr = __fmul_rn(q.x, kLog2e) - m.R;   // the split's reference, as
-                                                         // k_vocab_reduce rounded it
-        const float f = __builtin_amdgcn_exp2f(dr);
-        m.S = fmaf(f, q.z, m.S);
-        m.T = fmaf(f, fmaf(dr, q.z, q.w), m.T);
-    }
-}
-
-__device__ inline void load_chunk(const float4 *p, int s0, int splits, float4 (&q)[kMergeChunk]) {
-#pragma unroll
-    for (int i = 0; i < kMergeChunk; ++i)
-        q[i] = s0 + i < splits ? p[s0 + i] : make_float4(-INFINITY, 0.f, 0.f, 0.f);
-}
-
+// the same partials.  p may point to global memory or to LDS (stage_partials).
 __device__ inline RowStat merge_row(const float4 *p, int splits) {
 #pragma clang fp contract(off)
-    MergeAcc m;
-    float4 q[kMergeChunk];
-    if (splits <= kMergeChunk) {                   // one round trip: both passes from registers
-        load_chunk(p, 0, splits, q);
-#pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) merge_max(m, q[i]);
-        m.R = __fmul_rn(m.M, kLog2e);
-#pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) merge_sum(m, q[i]);
-    } else {
-        for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-            load_chunk(p, s0, splits, q);
-#pragma unroll
-            for (int i = 0; i < kMergeChunk; ++i) merge_max(m, q[i]);
-        }
-        m.R = __fmul_rn(m.M, kLog2e);
-        for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-            load_chunk(p, s0, splits, q);
-#pragma unroll
-            for (int i = 0; i < kMergeChunk; ++i) merge_sum(m, q[i]);
+    float M = -INFINITY;
+    int arg = INT_MAX;
+    for (int s = 0; s < splits; ++s) {
+        const float4 q = p[s];
+        if (q.z > 0.f && q.x > M) { M = q.x; arg = __float_as_int(q.y); }   // earlier split wins ties
+    }
+    const float R = __fmul_rn(M, kLog2e);
+    float S = 0.f, T = 0.f;
+    for (int s = 0; s < splits; ++s) {
+        const float4 q = p[s];
+        if (q.z > 0.f) {
+            const float dr = __fmul_rn(q.x, kLog2e) - R;   // the split's reference, as
+                                                           // k_vocab_reduce rounded it
+            const float f = __builtin_amdgcn_exp2f(dr);
+            S = fmaf(f, q.z, S);
+            T = fmaf(f, fmaf(dr, q.z, q.w), T);
         }
     }
     // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
     // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
-    const float delta = fmaf(m.M, kLog2e, -m.R);
-    const float l2s = __log2f(m.S);
+    const float delta = fmaf(M, kLog2e, -R);
+    const float l2s = __log2f(S);
     RowStat r;
-    r.max = m.M;
-    r.arg = m.arg;
+    r.max = M;
+    r.arg = arg;
     r.log_s = (l2s - delta) * kLn2;
-    r.lse = m.M + r.log_s;
-    r.ent = (l2s - m.T / m.S) * kLn2;
+    r.lse = M + r.log_s;
+    r.ent = (l2s - T / S) * kLn2;
     return r;
 }
 
