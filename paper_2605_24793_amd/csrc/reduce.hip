@@ -25,6 +25,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "launch.h"
 #include "rowstat.h"
 
@@ -137,22 +139,35 @@ __device__ inline float transpose_sum8(const float (&m)[8], int lane) {
 }
 
 // Plain streaming of vectors [v0, v1) of a row: lane `tid` takes v0 + tid, then
-// every kReduceThreads-th vector.
+// every kReduceThreads-th vector.  Loads roll: while whole batches remain, each
+// register slot is refilled with the vector kUnroll steps ahead as soon as it is
+// unpacked, so a lane keeps kUnroll loads in flight through the row.
 template <int DT>
 __device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, Lane &st) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
+    constexpr int kStep = kUnroll * kReduceThreads;
     int v = v0 + tid;
-    for (; v + (kUnroll - 1) * kReduceThreads < v1; v += kUnroll * kReduceThreads) {
+    if (v + (kUnroll - 1) * kReduceThreads < v1) {
         u32x4 q[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
+        for (; v + kStep + (kUnroll - 1) * kReduceThreads < v1; v += kStep) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                float x[NV];
+                E::unpack(q[u], x);
+                q[u] = __builtin_nontemporal_load(rv + v + kStep + u * kReduceThreads);
+                consume<NV>(x, v + u * kReduceThreads, st);
+            }
+        }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
             consume<NV>(x, v + u * kReduceThreads, st);
         }
+        v += kStep;
     }
     // the rest: at most kUnroll - 1 vectors per lane, every load issued before the
     // first is used (one memory round trip, not one per vector)
@@ -194,17 +209,19 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     static_assert(kUnroll == 8 && kReduceThreads % kSegVecs == 0, "segment sums assume 8 loads per lane");
+    constexpr int kStep = kUnroll * kReduceThreads;
     const int lane = tid & 63;
     int w = v0 + (tid & ~63);                      // this wave's first vector
-    for (; w + (kUnroll - 1) * kReduceThreads + 63 < v1; w += kUnroll * kReduceThreads) {
-        u32x4 q[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+    // one batch: kUnroll whole segments of this wave; with RELOAD each slot is refilled
+    // from the next batch as soon as it is unpacked (loads roll, as in stream_plain)
+    auto batch = [&](u32x4 (&q)[kUnroll], auto reload) {
         float m[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
+            if constexpr (decltype(reload)::value)
+                q[u] = __builtin_nontemporal_load(rv + w + kStep + u * kReduceThreads + lane);
             float cm = -INFINITY;
 #pragma unroll
             for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
@@ -228,6 +245,15 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
         }
         const float tot = transpose_sum8(m, lane);
         if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, st.ref);
+    };
+    if (w + (kUnroll - 1) * kReduceThreads + 63 < v1) {   // wave-uniform: a whole batch
+        u32x4 q[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+        for (; w + kStep + (kUnroll - 1) * kReduceThreads + 63 < v1; w += kStep)
+            batch(q, std::true_type{});
+        batch(q, std::false_type{});
+        w += kStep;
     }
     // the rest: fewer than kUnroll segments of this wave, the last one possibly
     // partial; every load is issued before the first is used
