@@ -61,7 +61,8 @@ extern "C" {
 typedef enum {
     COSPEC_OK = 0,
     COSPEC_ERR_INVALID_ARG = -1,  /* null/misaligned pointer, bad size, NaN lambda ... */
-    COSPEC_ERR_UNSUPPORTED = -2,  /* K, N or split count above the documented maximum   */
+    COSPEC_ERR_UNSUPPORTED = -2,  /* K, N or split count above the documented maximum,
+                                     or a logit row (V * element bytes) over 2^31 - 1 B */
     COSPEC_ERR_WORKSPACE = -3,    /* workspace missing, misaligned or too small         */
     COSPEC_ERR_HIP = -4           /* a HIP call or kernel launch failed                 */
 } cospec_status;

@@ -35,6 +35,7 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
 constexpr int64_t kAutoBlocks = 2048;         // aim: 8 workgroups per CU on 256 CUs
 constexpr int kOverlapBlocksPerCU = 3;        // draft-row reduction beside the aux stream
+constexpr int64_t kMaxRowBytes = INT32_MAX;    // V * element bytes of one logit row
 
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -409,6 +410,8 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
 cospec_status check_logits(const void *p, cospec_dtype dt, int64_t ld, int32_t V) {
     if (!p || !aligned(p, 16)) return COSPEC_ERR_INVALID_ARG;
     if (ld < V || (ld * elem_bytes(dt)) % 16 != 0) return COSPEC_ERR_INVALID_ARG;
+    // a row is read through a buffer resource with 32-bit byte offsets
+    if (static_cast<int64_t>(V) * elem_bytes(dt) > kMaxRowBytes) return COSPEC_ERR_UNSUPPORTED;
     return COSPEC_OK;
 }
 

@@ -42,20 +42,37 @@ constexpr float kRescaleMargin = 32.0f;   // log2 units of headroom above the re
 constexpr float kFarBelow = -1.0e30f;     // initial reference: any finite logit rescales
 constexpr int kUnroll = 8;                // 16-byte loads in flight per lane
 
+// Word 3 of a raw (unswizzled, stride 0) buffer resource: 32-bit data format.
+constexpr int kRawBuffer = 0x00020000;
+constexpr int kNontemporal = 2;           // cache policy of the loads: streamed once
+
+// The whole 16-byte vectors of one logit row, read through a raw buffer resource: a
+// load takes the lane's byte offset in a VGPR and a per-load constant in the scalar
+// offset, so it costs no vector address arithmetic.
+struct RowReader {
+    __amdgpu_buffer_rsrc_t rs;
+    __device__ RowReader(const void *row, int bytes)
+        : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(row), 0, bytes, kRawBuffer)) {}
+    __device__ u32x4 load(int voff, int soff) const {
+        return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, kNontemporal));
+    }
+};
+
 struct Lane {
     float best;      // largest logit seen
     int chunk;       // first chunk (16-byte vector index) holding `best`, -1 if none
-    float ref;       // reference of S and T, in log2 units
+    float nref;      // minus the reference of S and T (log2 units): the exponent of a
+                     // logit x is fma(x, log2e, nref)
     float thresh;    // logits above this need a larger reference: (ref + margin) / log2e
     float S, T;
 };
 
 __device__ inline void rescale(Lane &st, float new_ref) {
-    const float dr = st.ref - new_ref;            // <= 0, finite
+    const float dr = -st.nref - new_ref;          // <= 0, finite
     const float f = __builtin_amdgcn_exp2f(dr);
     st.T = f * fmaf(dr, st.S, st.T);
     st.S = f * st.S;
-    st.ref = new_ref;
+    st.nref = -new_ref;
     st.thresh = (new_ref + kRescaleMargin) * kLn2;
 }
 
@@ -72,10 +89,9 @@ __device__ inline void consume(const float *x, int chunk, Lane &st) {
     if (__builtin_expect(__ballot(up) != 0, 0)) {
         if (up) rescale(st, __fmul_rn(cm, kLog2e));
     }
-    const float nref = -st.ref;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
-        const float t = fmaf(x[k], kLog2e, nref);
+        const float t = fmaf(x[k], kLog2e, st.nref);
         const float e = __builtin_amdgcn_exp2f(t);
         st.S += e;
         st.T = fmaf(e, t, st.T);
@@ -143,29 +159,30 @@ __device__ inline float transpose_sum8(const float (&m)[8], int lane) {
 // register slot is refilled with the vector kUnroll steps ahead as soon as it is
 // unpacked, so a lane keeps kUnroll loads in flight through the row.
 template <int DT>
-__device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, Lane &st) {
+__device__ inline void stream_plain(const RowReader &rr, int v0, int v1, int tid, Lane &st) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
-    constexpr int kStep = kUnroll * kReduceThreads;
+    constexpr int T = kReduceThreads;
+    constexpr int kStep = kUnroll * T;
     int v = v0 + tid;
-    if (v + (kUnroll - 1) * kReduceThreads < v1) {
+    if (v + (kUnroll - 1) * T < v1) {
         u32x4 q[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
-        for (; v + kStep + (kUnroll - 1) * kReduceThreads < v1; v += kStep) {
+        for (int u = 0; u < kUnroll; ++u) q[u] = rr.load(v * 16, u * T * 16);
+        for (; v + kStep + (kUnroll - 1) * T < v1; v += kStep) {
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 float x[NV];
                 E::unpack(q[u], x);
-                q[u] = __builtin_nontemporal_load(rv + v + kStep + u * kReduceThreads);
-                consume<NV>(x, v + u * kReduceThreads, st);
+                q[u] = rr.load(v * 16, (kStep + u * T) * 16);
+                consume<NV>(x, v + u * T, st);
             }
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
-            consume<NV>(x, v + u * kReduceThreads, st);
+            consume<NV>(x, v + u * T, st);
         }
         v += kStep;
     }
@@ -174,13 +191,13 @@ __device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, La
     u32x4 q[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u)
-        if (v + u * kReduceThreads < v1) q[u] = __builtin_nontemporal_load(rv + v + u * kReduceThreads);
+        if (v + u * T < v1) q[u] = rr.load(v * 16, u * T * 16);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-        if (v + u * kReduceThreads < v1) {
+        if (v + u * T < v1) {
             float x[NV];
             E::unpack(q[u], x);
-            consume<NV>(x, v + u * kReduceThreads, st);
+            consume<NV>(x, v + u * T, st);
         }
     }
 }
@@ -189,11 +206,11 @@ __device__ inline void stream_plain(const u32x4 *rv, int v0, int v1, int tid, La
 // factor applied to S.
 __device__ inline float rescale_wave(Lane &st, float cm) {
     const float nr = __fmul_rn(wave_max_valu(cm), kLog2e);
-    const float dr = st.ref - nr;
+    const float dr = -st.nref - nr;
     const float f = __builtin_amdgcn_exp2f(dr);
     st.T = f * fmaf(dr, st.S, st.T);
     st.S = f * st.S;
-    st.ref = nr;
+    st.nref = -nr;
     st.thresh = (nr + kRescaleMargin) * kLn2;
     return f;
 }
@@ -205,7 +222,7 @@ __device__ inline float rescale_wave(Lane &st, float cm) {
 // wave when any lane needs it, so a segment's mass is one wave sum.  Requires v0 to
 // be a multiple of kSegVecs.
 template <int DT>
-__device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid, Lane &st, float2 *seg) {
+__device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int tid, Lane &st, float2 *seg) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     static_assert(kUnroll == 8 && kReduceThreads % kSegVecs == 0, "segment sums assume 8 loads per lane");
@@ -220,8 +237,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
         for (int u = 0; u < kUnroll; ++u) {
             float x[NV];
             E::unpack(q[u], x);
-            if constexpr (decltype(reload)::value)
-                q[u] = __builtin_nontemporal_load(rv + w + kStep + u * kReduceThreads + lane);
+            if constexpr (decltype(reload)::value) q[u] = rr.load((w + lane) * 16, (kStep + u * kReduceThreads) * 16);
             float cm = -INFINITY;
 #pragma unroll
             for (int k = 0; k < NV; ++k) cm = fmaxf(cm, x[k]);
@@ -231,7 +247,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
 #pragma unroll
                 for (int j = 0; j < u; ++j) m[j] *= f;
             }
-            const float nref = -st.ref;
+            const float nref = st.nref;
             float mu = 0.f;
 #pragma unroll
             for (int k = 0; k < NV; ++k) {
@@ -244,12 +260,12 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
             st.S += mu;
         }
         const float tot = transpose_sum8(m, lane);
-        if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, st.ref);
+        if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, -st.nref);
     };
     if (w + (kUnroll - 1) * kReduceThreads + 63 < v1) {   // wave-uniform: a whole batch
         u32x4 q[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+        for (int u = 0; u < kUnroll; ++u) q[u] = rr.load((w + lane) * 16, u * kReduceThreads * 16);
         for (; w + kStep + (kUnroll - 1) * kReduceThreads + 63 < v1; w += kStep)
             batch(q, std::true_type{});
         batch(q, std::false_type{});
@@ -261,7 +277,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
         u32x4 q[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            if (w + u * kReduceThreads + lane < v1) q[u] = __builtin_nontemporal_load(rv + w + u * kReduceThreads + lane);
+            if (w + u * kReduceThreads + lane < v1) q[u] = rr.load((w + lane) * 16, u * kReduceThreads * 16);
         float m[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
@@ -285,7 +301,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
 #pragma unroll
                 for (int j = 0; j < u; ++j) m[j] *= f;
             }
-            const float nref = -st.ref;
+            const float nref = st.nref;
             float mu = 0.f;
 #pragma unroll
             for (int k = 0; k < NV; ++k) {
@@ -300,7 +316,7 @@ __device__ inline void stream_segmented(const u32x4 *rv, int v0, int v1, int tid
         }
         const float tot = transpose_sum8(m, lane);
         const int ws = w + (lane >> 3) * kReduceThreads;           // segment of value lane >> 3
-        if ((lane & 7) == 0 && ws < v1) seg[ws / kSegVecs] = make_float2(tot, st.ref);
+        if ((lane & 7) == 0 && ws < v1) seg[ws / kSegVecs] = make_float2(tot, -st.nref);
     }
 }
 
@@ -331,11 +347,12 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
     const int v1 = min(v0 + a.vec_per_split, nvec);
     const u32x4 *rv = reinterpret_cast<const u32x4 *>(rp);
 
-    Lane st{-INFINITY, -1, kFarBelow, -INFINITY, 0.f, 0.f};   // the first chunk always rescales
+    Lane st{-INFINITY, -1, -kFarBelow, -INFINITY, 0.f, 0.f};   // the first chunk always rescales
     float2 *seg = nullptr;
     if (SEG && row < a.n_tgt_rows) seg = a.seg + static_cast<int64_t>(row) * a.nseg;
-    if (SEG && seg) stream_segmented<DT>(rv, v0, v1, tid, st, seg);
-    else stream_plain<DT>(rv, v0, v1, tid, st);
+    const RowReader rr(rp, nvec * 16);
+    if (SEG && seg) stream_segmented<DT>(rr, v0, v1, tid, st, seg);
+    else stream_plain<DT>(rr, v0, v1, tid, st);
     // elements past the last whole vector: the last split's first lane (their own
     // segment, the row's last, when segments are written)
     if (tail > 0 && split == a.splits - 1 && tid == 0) {
@@ -346,13 +363,13 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
         if (cm > st.thresh) rescale(st, __fmul_rn(cm, kLog2e));
         float mu = 0.f;
         for (int k = 0; k < tail; ++k) {
-            const float t = fmaf(E::at(rp, e0 + k), kLog2e, -st.ref);
+            const float t = fmaf(E::at(rp, e0 + k), kLog2e, st.nref);
             const float e = __builtin_amdgcn_exp2f(t);
             mu += e;
             st.T = fmaf(e, t, st.T);
         }
         st.S += mu;
-        if (SEG && seg) seg[a.nseg - 1] = make_float2(mu, st.ref);
+        if (SEG && seg) seg[a.nseg - 1] = make_float2(mu, -st.nref);
     }
 
     __shared__ float s_best[kReduceThreads / 64];
@@ -401,7 +418,7 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
     const float R = __fmul_rn(M, kLog2e);   // the partial's reference: rounded, never contracted
     float S = 0.f, T = 0.f;
     if (st.S > 0.f) {
-        const float dr = st.ref - R;
+        const float dr = -st.nref - R;
         const float f = __builtin_amdgcn_exp2f(dr);
         S = f * st.S;
         T = f * fmaf(dr, st.S, st.T);

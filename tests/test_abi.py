@@ -92,6 +92,7 @@ def _block(L, **kw):
     (dict(K=-1), INVALID),
     (dict(K=65), UNSUPPORTED),
     (dict(V=0), INVALID),
+    (dict(dt=0, V=1 << 29, ld=1 << 29), UNSUPPORTED),   # an fp32 row of 2^31 bytes
     (dict(lam=math.nan), INVALID),
     (dict(head=_head(d=0)), INVALID),
     (dict(head=_head(h=0)), INVALID),
