@@ -492,7 +492,8 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     }
     for (int j = t; j < a.RT; j += kDecideThreads) {
         const int64_t r = static_cast<int64_t>(b) * a.RT + j;
-        const RowStat rs = merge_row((staged ? s_parts : seq_parts) + static_cast<int64_t>(j) * a.splits, a.splits);
+        const RowStat rs = staged ? merge_row_lds(s_parts + j * a.splits, a.splits)
+                                  : merge_row(seq_parts + static_cast<int64_t>(j) * a.splits, a.splits);
         // the verification candidate: the argmax, or the temperature-1 sample
         // k_sample left in ws_tgt_arg
         const int cand = a.sampled ? a.ws_tgt_arg[r] : rs.arg;

@@ -63,25 +63,47 @@ struct RowStat {
 // Fixed-order merge of one row's split partials.  Every operation is rounded as
 // written (fma only where written, no contraction by the compiler), so that the
 // kernels that inline it (decide, finish, sampling) give bit-identical statistics for
-// the same partials.  p may point to global memory or to LDS (stage_partials).
-__device__ inline RowStat merge_row(const float4 *p, int splits) {
+// the same partials, whether they read them from global memory or LDS.  The
+// partials are read kMergeChunk at a time, every read of a chunk issued before the
+// first is used; the arithmetic runs over s = 0, 1, ... in order.
+constexpr int kMergeChunk = 8;
+
+typedef __attribute__((address_space(3))) const float lds_float;
+
+// ld(s) returns partial s, read from global memory or from LDS through a pointer of
+// that address space: a global and an LDS pointer are never merged into one, so
+// every access is a global or an LDS instruction, never a flat one.
+template <typename Ld>
+__device__ inline RowStat merge_row_t(Ld ld, int splits) {
 #pragma clang fp contract(off)
     float M = -INFINITY;
     int arg = INT_MAX;
-    for (int s = 0; s < splits; ++s) {
-        const float4 q = p[s];
-        if (q.z > 0.f && q.x > M) { M = q.x; arg = __float_as_int(q.y); }   // earlier split wins ties
+    float4 q[kMergeChunk];
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i)
+            if (s0 + i < splits) q[i] = ld(s0 + i);
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i)   // earlier split wins ties
+            if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
     }
     const float R = __fmul_rn(M, kLog2e);
     float S = 0.f, T = 0.f;
-    for (int s = 0; s < splits; ++s) {
-        const float4 q = p[s];
-        if (q.z > 0.f) {
-            const float dr = __fmul_rn(q.x, kLog2e) - R;   // the split's reference, as
-                                                           // k_vocab_reduce rounded it
-            const float f = __builtin_amdgcn_exp2f(dr);
-            S = fmaf(f, q.z, S);
-            T = fmaf(f, fmaf(dr, q.z, q.w), T);
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+        if (splits > kMergeChunk) {              // else the chunk is still in registers
+#pragma unroll
+            for (int i = 0; i < kMergeChunk; ++i)
+                if (s0 + i < splits) q[i] = ld(s0 + i);
+        }
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i) {
+            if (s0 + i < splits && q[i].z > 0.f) {
+                const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
+                                                                  // k_vocab_reduce rounded it
+                const float f = __builtin_amdgcn_exp2f(dr);
+                S = fmaf(f, q[i].z, S);
+                T = fmaf(f, fmaf(dr, q[i].z, q[i].w), T);
+            }
         }
     }
     // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
@@ -95,6 +117,18 @@ __device__ inline RowStat merge_row(const float4 *p, int splits) {
     r.lse = M + r.log_s;
     r.ent = (l2s - T / S) * kLn2;
     return r;
+}
+
+// A row's partials in global memory.
+__device__ inline RowStat merge_row(const float4 *p, int splits) {
+    return merge_row_t([p](int s) { return p[s]; }, splits);
+}
+
+// A row's partials staged in LDS (p points into a __shared__ array).
+__device__ inline RowStat merge_row_lds(const float4 *p, int splits) {
+    const lds_float *f = (const lds_float *)p;   // address-space cast to LDS
+    return merge_row_t([f](int s) { return make_float4(f[4 * s], f[4 * s + 1], f[4 * s + 2], f[4 * s + 3]); },
+                       splits);
 }
 
 // A sequence's partials, when a row is split many ways, are first copied into LDS by

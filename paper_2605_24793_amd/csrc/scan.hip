@@ -101,8 +101,8 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, f
         const bool valid = c.st != kStateReject;
         c.tok_d = a.tokens[di];
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
-        const RowStat rs =
-            merge_row((staged ? stage : seq_parts) + static_cast<int64_t>(lane) * a.drf_splits, a.drf_splits);
+        const RowStat rs = staged ? merge_row_lds(stage + lane * a.drf_splits, a.drf_splits)
+                                  : merge_row(seq_parts + static_cast<int64_t>(lane) * a.drf_splits, a.drf_splits);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
         c.pos = a.ws_listpos[di];
