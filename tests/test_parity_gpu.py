@@ -173,6 +173,10 @@ FUZZ = [
     (3, 64, 2053, "bf16", 0, 2, 0.5, 4.0, 0.3),
     (300, 3, 513, "bf16", 0, 0, 0.5, 4.0, 1.0),
     (9, 7, 20000, "f32", 0, 64, 0.2, 2.0, 2.0),
+    # merges across a chunk boundary (9 splits), and rows split so many ways that a
+    # sequence's partials do not fit the LDS stage (41 x 30 > 1024): merged from memory
+    (4, 5, 30011, "f32", 0, 9, 0.5, 4.0, 1.0),
+    (2, 40, 60001, "bf16", 0, 30, 0.5, 4.0, 0.8),
 ]
 
 
@@ -231,9 +235,13 @@ def test_fuzz_tree(shape, N):
     tr = workloads.make_random_tree(B=5, N=N, V=3001, d=64, h=48, shape=shape, seed=N, bias=True,
                                     noise=0.5)
     for lam in (0.3, 0.5):
-        gpu = _gpu_tree(tr, lam, pad=8)
-        stats = parity.check_tree(gpu, _ref_tree(tr, lam))
-        _report(f"tree {shape} N={N} lambda {lam}", stats, gpu)
+        ref = _ref_tree(tr, lam)
+        # rows split 5 ways too: a tree's partials staged in LDS (N x 5 <= 1024) or,
+        # for 256 nodes, merged from memory
+        for splits in (0, 5):
+            gpu = _gpu_tree(tr, lam, pad=8, splits=splits)
+            stats = parity.check_tree(gpu, ref)
+            _report(f"tree {shape} N={N} lambda {lam} splits {splits}", stats, gpu)
 
 
 def test_path_tree_equals_chain_on_gpu():
