@@ -78,31 +78,40 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
 #pragma clang fp contract(off)
     float M = -INFINITY;
     int arg = INT_MAX;
-    float4 q[kMergeChunk];
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-#pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i)
-            if (s0 + i < splits) q[i] = ld(s0 + i);
-#pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i)   // earlier split wins ties
-            if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
-    }
-    const float R = __fmul_rn(M, kLog2e);
     float S = 0.f, T = 0.f;
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-        if (splits > kMergeChunk) {              // else the chunk is still in registers
+    float R;
+    if (splits == 1) {
+        // one partial: what the loops below compute for it (its reference is R itself,
+        // so dr = 0 and the factor exp2(0) = 1), without them
+        const float4 q0 = ld(0);
+        if (q0.z > 0.f) { M = q0.x; arg = __float_as_int(q0.y); S = q0.z; T = q0.w; }
+        R = __fmul_rn(M, kLog2e);
+    } else {
+        float4 q[kMergeChunk];
+        for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
 #pragma unroll
             for (int i = 0; i < kMergeChunk; ++i)
                 if (s0 + i < splits) q[i] = ld(s0 + i);
-        }
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) {
-            if (s0 + i < splits && q[i].z > 0.f) {
-                const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
-                                                                  // k_vocab_reduce rounded it
-                const float f = __builtin_amdgcn_exp2f(dr);
-                S = fmaf(f, q[i].z, S);
-                T = fmaf(f, fmaf(dr, q[i].z, q[i].w), T);
+            for (int i = 0; i < kMergeChunk; ++i)   // earlier split wins ties
+                if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
+        }
+        R = __fmul_rn(M, kLog2e);
+        for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+            if (splits > kMergeChunk) {              // else the chunk is still in registers
+#pragma unroll
+                for (int i = 0; i < kMergeChunk; ++i)
+                    if (s0 + i < splits) q[i] = ld(s0 + i);
+            }
+#pragma unroll
+            for (int i = 0; i < kMergeChunk; ++i) {
+                if (s0 + i < splits && q[i].z > 0.f) {
+                    const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
+                                                                      // k_vocab_reduce rounded it
+                    const float f = __builtin_amdgcn_exp2f(dr);
+                    S = fmaf(f, q[i].z, S);
+                    T = fmaf(f, fmaf(dr, q[i].z, q[i].w), T);
+                }
             }
         }
     }

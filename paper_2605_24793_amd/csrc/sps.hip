@@ -70,18 +70,28 @@ struct LastRows {
     RowStat ts, ds;
 };
 
-__device__ inline LastRows last_rows(const SpsArgs &a, int b) {
+// The rows alone (no statistics yet), so that a caller can issue its loads of them
+// before the merges' own loads and arithmetic.
+__device__ inline LastRows last_row_ptrs(const SpsArgs &a, int b) {
     LastRows r;
     const int s = a.accept_len[b];
     const int64_t trow = static_cast<int64_t>(b) * (a.K + 1) + (s - 1);
     r.t = a.tgt + trow * a.ld_bytes;
-    r.ts = merge_row(a.partials + trow * a.splits, a.splits);
     r.d = nullptr;
-    if (s <= a.K) {
-        const int64_t drow = static_cast<int64_t>(b) * a.K + (s - 1);
-        r.d = a.drf + drow * a.ld_bytes;
-        r.ds = merge_row(a.partials + (a.drf_row0 + drow) * a.splits, a.splits);
-    }
+    if (s <= a.K) r.d = a.drf + (static_cast<int64_t>(b) * a.K + (s - 1)) * a.ld_bytes;
+    return r;
+}
+
+__device__ inline void last_row_stats(const SpsArgs &a, int b, LastRows &r) {
+    const int s = a.accept_len[b];
+    const int64_t trow = static_cast<int64_t>(b) * (a.K + 1) + (s - 1);
+    r.ts = merge_row(a.partials + trow * a.splits, a.splits);
+    if (r.d) r.ds = merge_row(a.partials + (a.drf_row0 + static_cast<int64_t>(b) * a.K + (s - 1)) * a.splits, a.splits);
+}
+
+__device__ inline LastRows last_rows(const SpsArgs &a, int b) {
+    LastRows r = last_row_ptrs(a, b);
+    last_row_stats(a, b, r);
     return r;
 }
 
@@ -118,7 +128,7 @@ __global__ __launch_bounds__(256) void k_sps_mass(SpsArgs a) {
     const int b = blockIdx.x / per_seq;
     const int seg0 = (blockIdx.x % per_seq) * kMassSegsPerBlock + (threadIdx.x >> 6) * kMassSegsPerWave;
     if (seg0 >= a.nseg) return;                            // whole wave leaves
-    const LastRows r = last_rows(a, b);
+    LastRows r = last_row_ptrs(a, b);
     const int nvec = static_cast<int>((static_cast<int64_t>(a.V) * E::kBytes) / 16);
     const int nmain = (nvec + kSegVecs - 1) / kSegVecs;
     // all of this wave's loads first (kMassSegsPerWave segments of both rows), then
@@ -134,6 +144,7 @@ __global__ __launch_bounds__(256) void k_sps_mass(SpsArgs a) {
             if (r.d) dq[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(r.d) + v);
         }
     }
+    last_row_stats(a, b, r);                               // while the segments are in flight
 #pragma unroll
     for (int j = 0; j < kMassSegsPerWave; ++j) {
         const int seg = seg0 + j;
