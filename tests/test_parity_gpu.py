@@ -317,6 +317,50 @@ def test_overlap_stream_gives_the_same_results():
     parity.check_tree(b, _ref_tree(tr, 0.5))
 
 
+def _replays_match_eager(p, perturb):
+    """Capture p.launch() in a HIP graph; every replay, with its outputs poisoned first
+    and another eager step (perturb) run in between, must give the eager results."""
+    p.launch()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in p.result().items()}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        p.launch()                                       # warm-up off the default stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        p.launch()
+    for i in range(4):
+        for v in p.result().values():
+            v.fill_(7)
+        perturb()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in p.result().items():
+            a, b = ref[k], v
+            same = torch.equal(a.view(torch.uint8), b.view(torch.uint8)) if a.dtype == torch.float32 else torch.equal(a, b)
+            assert same, f"replay {i}: {k}"
+
+
+def test_step_replays_from_a_hip_graph():
+    # the step enqueues kernels only (no allocation, copy or memset node): a captured
+    # step replays bit for bit, chains and trees, also with split rows
+    wl = workloads.make_chain(B=32, K=7, V=30001, d=256, h=128, seed=21, bias=True, noise=1.0)
+    other = workloads.make_chain(B=32, K=7, V=30001, d=256, h=128, seed=22, bias=True, noise=1.5)
+    dev = lambda w: (_padded(w.target, 0), _padded(w.draft, 0), w.draft_tokens.to(DEV), w.hidden.to(DEV))
+    q = cs.prepare_block(*dev(other), _head_dev(other.head), 0.5)
+    for splits in (0, 3):
+        p = cs.prepare_block(*dev(wl), _head_dev(wl.head), 0.5, splits=splits)
+        _replays_match_eager(p, q.launch)
+    tr = workloads.make_random_tree(B=6, N=40, V=3001, d=64, h=32, seed=23, bias=True)
+    pt = cs.prepare_tree(_padded(tr.target, 0), _padded(tr.draft, 0), tr.parent.to(DEV), tr.node_tokens.to(DEV),
+                         tr.hidden.to(DEV), _head_dev(tr.head), 0.5)
+    _replays_match_eager(pt, q.launch)
+
+
 @pytest.mark.parametrize("logit_dtype,head_dtype", [("bf16", "f32"), ("f32", "bf16")])
 def test_mixed_logit_and_head_dtypes(logit_dtype, head_dtype):
     wl = workloads.make_chain(B=9, K=6, V=5003, d=128, h=96, dtype=logit_dtype, seed=31, bias=True)
