@@ -64,6 +64,9 @@ def parse():
                     help="time the arbitrator's hybrid attention over the region queries "
                          "(B=64 sequences, 2048 context tokens, K=7, 32 query / 8 key-value heads, "
                          "D=128) instead of the verify step")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured in a HIP graph (no per-launch host "
+                         "work: what a serving loop that captures its step sees)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     return ap.parse_args()
@@ -198,13 +201,31 @@ def main():
     torch.cuda.synchronize()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
+    step = p.launch
+    if args.graph:
+        if args.overlap:
+            print(json.dumps({"error": "--graph does not capture the aux stream"}))
+            sys.exit(2)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            p.launch()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            p.launch()
+        step = graph.replay
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+
     # timed region 1: the whole step, back to back, nothing else on the stream
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record()
     for _ in range(args.steps):
-        p.launch()
+        step()
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -306,6 +327,7 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
                    "splits": args.splits or "auto", "head_overlap": args.overlap,
+                   "hip_graph": args.graph,
                    "temperature": 1 if args.sample or args.sps else 0,
                    "rule": "speculative sampling" if args.sps else "cospec",
                    "rows_per_step": rows,
