@@ -343,6 +343,11 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2; ha.b2 = c.head->b2;
         ha.d = c.head->d; ha.h = c.head->h;
         ha.ksplit = ksplit_for(m_cap, c.head);
+        // Trees mismatch most of their slots (about 60% on the 64-tree batch: 304
+        // workgroups at 8 k-slices), more than one workgroup per CU: the shallow ring
+        // lets two share a CU and finish in one round (19.9 -> 13.8 us there).  The
+        // chain batches measured fill the CUs once, where the deep ring is 0.9 us faster.
+        ha.two_per_cu = c.is_tree;
         ha.upart = upart;
         ha.z = zlog;
         const Dtype hdt = static_cast<Dtype>(c.head->dtype);
@@ -690,6 +695,10 @@ cospec_status cospec_arbitrate(const void *hidden, int64_t n_rows, const int32_t
     ha.count_dev = nullptr; ha.count_host = n_sel; ha.m_cap = n_sel;
     ha.w1 = head->w1; ha.b1 = head->b1; ha.w2 = head->w2; ha.b2 = head->b2; ha.d = head->d; ha.h = head->h;
     ha.ksplit = ks;
+    // the row count is known here: the shallow ring when the grid has more workgroups
+    // than there are CUs
+    ha.two_per_cu = ((n_sel + kHeadTileM - 1) / kHeadTileM) * ((head->h + kHeadTileN - 1) / kHeadTileN) * ks >
+                    cu_count();
     ha.upart = upart;
     ha.z = zlog;
     if (launch_head(static_cast<Dtype>(head->dtype), ha, stream) != hipSuccess) return COSPEC_ERR_HIP;

@@ -35,7 +35,11 @@ typedef __attribute__((ext_vector_type(4))) float floatx4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStageBytes = 128;                  // bytes of k per row per stage
-constexpr int kRing = 4;                          // LDS stages: three in flight while one is used
+// LDS ring depth: four stages (three in flight while one is used, 128 KiB: one
+// workgroup per CU), or two (64 KiB: two workgroups per CU) when the grid has more
+// workgroups than there are CUs.
+constexpr int kRingDeep = 4;
+constexpr int kRingShallow = 2;
 constexpr int kWaveTile = 64;                    // rows of a wave's sub-tile
 constexpr int kWaveCols = 32;                    // columns of a wave's sub-tile
 constexpr int kGemmWaves = 8;                    // 2 x 4 waves per workgroup: two per SIMD
@@ -79,7 +83,7 @@ __device__ inline void lds_barrier() {
 
 using headz::hidden_row;
 
-template <int DT>
+template <int DT, int kRing>
 __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
     constexpr int BK = kStageBytes / EB;          // elements of k per stage
@@ -251,8 +255,13 @@ hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(tiles * a.ksplit));
     if (grid.x == 0) return hipSuccess;
     const dim3 block(64 * kGemmWaves);
-    if (dt == kBF16) hipLaunchKernelGGL(k_head_gemm<kBF16>, grid, block, 0, s, a);
-    else hipLaunchKernelGGL(k_head_gemm<kF32>, grid, block, 0, s, a);
+    if (a.two_per_cu) {
+        if (dt == kBF16) hipLaunchKernelGGL((k_head_gemm<kBF16, kRingShallow>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_head_gemm<kF32, kRingShallow>), grid, block, 0, s, a);
+    } else {
+        if (dt == kBF16) hipLaunchKernelGGL((k_head_gemm<kBF16, kRingDeep>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_head_gemm<kF32, kRingDeep>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 

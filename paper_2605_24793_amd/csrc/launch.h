@@ -100,6 +100,7 @@ struct HeadArgs {
     float b2;
     int32_t d, h;
     int32_t ksplit;            // slices of d, one workgroup each (head_ksplit)
+    int32_t two_per_cu;        // use the shallow LDS ring: two workgroups fit on a CU
     float *upart;              // [ksplit][m_cap][h] partial pre-activations
     float *z;                  // [m_cap] head logits of the selected rows
 };
