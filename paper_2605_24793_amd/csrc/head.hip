@@ -81,7 +81,7 @@ __device__ inline void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
-using headz::hidden_row;
+using headz::mapped_row;
 
 template <int DT, int kRing>
 __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
@@ -93,8 +93,21 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
     const int ks = blockIdx.x % a.ksplit;
     const int tile = blockIdx.x / a.ksplit;
     const int mtiles = static_cast<int>((a.m_cap + kHeadTileM - 1) / kHeadTileM);
-    const int64_t M = a.count_dev ? static_cast<int64_t>(*a.count_dev) : a.count_host;
     const int64_t m_base = static_cast<int64_t>(tile % mtiles) * kHeadTileM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lrow = lane >> 3, lslot = lane & 7;
+    // the list entries of this lane's two loader rows are read together with M (not
+    // after it): entries past M are stale and replaced below, so the first operand
+    // loads wait for one memory round trip instead of two
+    int32_t lid[2] = {0, 0};
+    if (a.list) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int64_t m = min(m_base + 8 * (wave * 2 + i) + lrow, a.m_cap - 1);
+            lid[i] = a.list[m];
+        }
+    }
+    const int64_t M = a.count_dev ? static_cast<int64_t>(*a.count_dev) : a.count_host;
     if (m_base >= M) return;
     const int n_base = (tile / mtiles) * kHeadTileN;
     const int kchunk = ((a.d + a.ksplit - 1) / a.ksplit + BK - 1) / BK * BK;
@@ -102,7 +115,6 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
     const int k1 = min(a.d, k0 + kchunk);
     const int nst = k1 > k0 ? (k1 - k0 + BK - 1) / BK : 0;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 2, wc = wave & 3;
     const int g = lane >> 4, l16 = lane & 15;
 
@@ -112,7 +124,6 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
 
     // async loader: per stage, wave w fills 1 KB blocks w*2+i of A and of B (8 rows each);
     // lane l brings row 8*(w*2+i) + l/8, k-vector (l%8) ^ (row%8)
-    const int lrow = lane >> 3, lslot = lane & 7;
     const char *ga[2];
     const char *gb[2];
     int lvec[2];
@@ -120,10 +131,11 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm(HeadArgs a) {
     for (int i = 0; i < 2; ++i) {
         const int row = 8 * (wave * 2 + i) + lrow;
         lvec[i] = lslot ^ (row & 7);
-        int64_t m = m_base + row;
-        if (m >= M) m = M - 1;                     // garbage rows are computed, never stored
-        int64_t id = hidden_row(a, m);
-        if (id < 0 || id >= a.n_rows) id = 0;     // its logit is set to NaN by the epilogue
+        const int64_t m = m_base + row;
+        // rows past M are computed from row 0 and never stored; an invalid id's logit
+        // is set to NaN by the epilogue
+        int64_t id = m >= M ? 0 : a.list ? mapped_row(a, lid[i]) : mapped_row(a, m);
+        if (id < 0 || id >= a.n_rows) id = 0;
         ga[i] = static_cast<const char *>(a.hidden) + id * static_cast<int64_t>(a.d) * EB;
         int n = n_base + row;
         if (n >= a.h) n = a.h - 1;

@@ -22,11 +22,15 @@ template <> __device__ inline float scalar_at<kF32>(const void *p, int64_t i) {
     return static_cast<const float *>(p)[i];
 }
 
-// Hidden row of list entry m (see HeadArgs::row0).
-__device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
-    int64_t id = a.list ? static_cast<int64_t>(a.list[m]) : m;
+// Hidden row of decision slot id (see HeadArgs::row0).
+__device__ inline int64_t mapped_row(const HeadArgs &a, int64_t id) {
     if (a.row0 && id >= 0) id = a.row0[id / a.slots] + id % a.slots;
     return id;
+}
+
+// Hidden row of list entry m.
+__device__ inline int64_t hidden_row(const HeadArgs &a, int64_t m) {
+    return mapped_row(a, a.list ? static_cast<int64_t>(a.list[m]) : m);
 }
 
 // One pass of a lane covers CPL columns (lane, lane + 64, ...) and loads SPL k-slice
