@@ -44,6 +44,64 @@ def measured_traffic(kernel_source: str):
     return rec.get("traffic_bytes_per_launch")
 
 
+def host_info():
+    """ROCm release, the GPU clocks rocm-smi reports before this process touches the GPU
+    (idle clocks, not the clocks under load) and the host's CPU model; fields that
+    cannot be read are left out."""
+    import subprocess
+    info = {}
+    try:
+        info["rocm"] = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        pass
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=20)
+        card = next(iter(json.loads(r.stdout).values()))
+        for k, v in card.items():        # e.g. "sclk clock speed:": "(107Mhz)"
+            if "clock speed" in k and "Mhz" in v:
+                info[k.split()[0] + "_mhz_idle_at_start"] = int(v.strip("()").replace("Mhz", ""))
+    except Exception:
+        pass
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                info["cpu_model"] = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return info
+
+
+def device_info(torch):
+    prop = torch.cuda.get_device_properties(0)
+    return {"name": prop.name, "arch": getattr(prop, "gcnArchName", None),
+            "compute_units": prop.multi_processor_count, "hip": torch.version.hip}
+
+
+def step_percentiles(torch, np, step, steps, flush=None):
+    """Per-step HIP-event times (ms) of `steps` calls: p10, median, p90.  With `flush`,
+    that callable runs before every step, outside the step's events."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        if flush is not None:
+            flush()
+        a.record()
+        step()
+        b.record()
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    return {"p10": float(np.percentile(ms, 10)), "p50": float(np.median(ms)), "p90": float(np.percentile(ms, 90))}
+
+
+def oracle_threads():
+    """Threads for the parallel oracle run: the CPUs this process may use, at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -76,6 +134,7 @@ def bench_attention(args):
     """The arbitrator's hybrid attention for one round's region queries: each sequence's
     2K+3 new positions attend to its cached context and the region (bf16, fp32
     accumulation).  Roofline: the key/value bytes every launch must read."""
+    hinfo = host_info()
     import numpy as np
     import torch
 
@@ -131,7 +190,8 @@ def bench_attention(args):
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                          "kernel": "k_hybrid_attention", "kernel_ms": ms,
                          "algorithmic_bytes_per_launch": kv_bytes},
-            "tflops": flops / (ms * 1e-3) / 1e12, "cpu_baseline": cpu}
+            "tflops": flops / (ms * 1e-3) / 1e12, "device": dict(device_info(torch), **hinfo),
+            "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 
 
@@ -144,6 +204,7 @@ def main():
     if args.attention:
         bench_attention(args)
         return
+    hinfo = host_info()
     import numpy as np
     import torch
 
@@ -242,6 +303,14 @@ def main():
     for i in range(args.steps):
         p.launch(timing=ev[i])
     torch.cuda.synchronize()
+    # per-step distribution: back to back, and with the 256 MB last-level cache (MALL)
+    # flushed before every step by writing a 512 MB buffer outside the step's events
+    print(f"[bench] per-step times, warm and with the cache flushed, {args.steps} steps each",
+          file=sys.stderr, flush=True)
+    warm_pct = step_percentiles(torch, np, step, args.steps)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold_pct = step_percentiles(torch, np, step, args.steps, flush=lambda: scratch.fill_(0x5A))
+    del scratch
     launches = 2 if args.overlap else 1             # the draft rows get their own launch
     k_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev]
     k_raw = float(np.mean(k_ms)) / launches         # event interval per launch
@@ -259,7 +328,7 @@ def main():
 
     # CPU oracle on a bounded sample (first sequences of the same workload), also a
     # parity re-check of the timed outputs on those sequences
-    cpu = None
+    cpu = cpu_par = None
     if args.cpu_seconds > 0:
         import oracle
         from oracle import parity
@@ -311,6 +380,32 @@ def main():
                          f"workload, fp64 oracle, single thread, {spent:.1f} s",
                "parity_checked_sequences": checked}
 
+        # the same sequences again, one chunk per task on a thread pool: the oracle's C
+        # loops release the interpreter lock, so its row reductions run in parallel
+        from concurrent.futures import ThreadPoolExecutor
+        nth = oracle_threads()
+
+        def run_chunk(seqs):
+            sub = wl.take(seqs)
+            us = None if u_host is None else u_host[seqs].double().numpy()
+            if args.sps:
+                oracle.sps_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                 sps_u[seqs].double().numpy())
+            elif tree:
+                oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(), sub.node_tokens.numpy(),
+                                   conv(sub.hidden), head_np, lam, sample_u=us)
+            else:
+                oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                    conv(sub.hidden), head_np, lam, sample_u=us)
+        chunks = [list(range(s, min(done, s + chunk))) for s in range(0, done, chunk)]
+        c0 = time.perf_counter()
+        with ThreadPoolExecutor(max_workers=nth) as pool:
+            list(pool.map(run_chunk, chunks))
+        par_spent = time.perf_counter() - c0
+        cpu_par = {"value": cpu_rows / par_spent, "unit": "rows/s", "cores": nth, "kind": "oracle",
+                   "sample": f"the same {done} sequences, {len(chunks)} chunks of up to {chunk} on "
+                             f"{nth} threads, {par_spent:.1f} s"}
+
     line = {
         "metric": METRIC,
         "value": value,
@@ -343,7 +438,11 @@ def main():
         "step_hbm_gbps": logit_bytes / (ms_per_step * 1e-3) / 1e9,
         "wall_s": wall,
         "mean_accept_len": float(out["accept_len"].float().mean()),
+        "step_ms_warm": warm_pct,
+        "step_ms_cache_flushed": cold_pct,
+        "device": dict(device_info(torch), **hinfo),
         "cpu_baseline": cpu,
+        "cpu_baseline_threads": cpu_par,
     }
     print(json.dumps(line), flush=True)
 
