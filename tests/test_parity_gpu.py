@@ -746,6 +746,21 @@ def test_sps_configs(cfg):
     _report(f"SpS config {cfg}", stats, gpu)
 
 
+def test_sps_config4_full_size_sampled():
+    # the launch configuration bench.py --sps times (256 sequences, automatic splits),
+    # checked on a sample of the sequences
+    wl = workloads.make_config(4)
+    u = _uniforms((wl.B, wl.K + 1), 404)
+    gpu = cs.sps_block(wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV), u.to(DEV))
+    torch.cuda.synchronize()
+    seqs = _sample(wl.B, 16, 41)
+    sub = wl.take(seqs)
+    gsub = {k: v.cpu()[seqs] for k, v in gpu.items()}
+    t, d, us = _conv(sub.target), _conv(sub.draft), u[seqs].double().numpy()
+    ref = oracle.sps_block(t, d, sub.draft_tokens.numpy(), us)
+    _report("SpS config 4 (16 sampled sequences of 256)", parity.check_sps(gsub, ref, t, d, us), gsub)
+
+
 @pytest.mark.parametrize("B,K,V,dtype,pad,splits", [(3, 1, 7, "f32", 1, 0), (4, 4, 9, "bf16", 0, 2),
                                                      (5, 6, 4097, "bf16", 8, 3), (3, 5, 32001, "f32", 3, 0),
                                                      (2, 0, 3000, "bf16", 0, 0), (6, 9, 151936, "bf16", 0, 5)])
@@ -808,6 +823,31 @@ def _attn_case(B, nq, Hq, Hkv, D, L, ctx, qs, K, seed):
     print(f"[hybrid attention B={B} n_q={nq} Hq={Hq} Hkv={Hkv} D={D} L={L}] max err {err:.2e} (tol {tol:.2e})",
           flush=True)
     assert err <= tol
+
+
+def test_hybrid_attention_bench_shape_sampled():
+    # the shape bench.py --attention times: 64 sequences x 2048 context tokens, K = 7
+    # (17 region queries each), 32 query / 8 key-value heads, D = 128; the oracle checks
+    # four sampled sequences
+    B, ctx_len, K, Hq, Hkv, D = 64, 2048, 7, 32, 8, 128
+    nq = 2 * K + 3
+    L = (ctx_len + nq + 15) // 16 * 16
+    g = torch.Generator().manual_seed(12)
+    q = torch.randn(B, nq, Hq, D, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, L, Hkv, D, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, L, Hkv, D, generator=g).to(torch.bfloat16)
+    ctx = torch.full((B,), ctx_len, dtype=torch.int32)
+    scale = 1.0 / np.sqrt(D)
+    out = cs.hybrid_attention(q.to(DEV), k.to(DEV), v.to(DEV), ctx.to(DEV), ctx.to(DEV), K, scale)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    for b in _sample(B, 4, 13):
+        ref = oracle.hybrid_attention(bf16_bits(q[b:b + 1]), bf16_bits(k[b:b + 1]), bf16_bits(v[b:b + 1]),
+                                      [ctx_len], [ctx_len], K, scale)
+        tol = 6e-3 * float(v[b].float().abs().max())
+        err = np.abs(got[b:b + 1] - ref).max()
+        print(f"[hybrid attention bench shape, sequence {b}] max err {err:.2e} (tol {tol:.2e})", flush=True)
+        assert err <= tol
 
 
 @pytest.mark.parametrize("D", [128, 64])
