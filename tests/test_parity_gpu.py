@@ -177,6 +177,9 @@ FUZZ = [
     # sequence's partials do not fit the LDS stage (41 x 30 > 1024): merged from memory
     (4, 5, 30011, "f32", 0, 9, 0.5, 4.0, 1.0),
     (2, 40, 60001, "bf16", 0, 30, 0.5, 4.0, 0.8),
+    # vocabularies far past the workloads' (2 MiB and 4 MiB rows, ragged tails)
+    (2, 3, 1048583, "bf16", 0, 0, 0.5, 4.0, 1.0),
+    (1, 2, 1048577, "f32", 3, 0, 0.5, 4.0, 1.0),
 ]
 
 
