@@ -198,7 +198,7 @@ def bench_attention(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+        print(json.dumps({"error": "bench.py measures one GPU (sequences shard across GPUs with no exchange); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     if args.attention:
