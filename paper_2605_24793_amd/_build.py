@@ -11,7 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libcospec.so")
 SOURCES = ["cospec_api.hip", "reduce.hip", "sample.hip", "head.hip", "scan.hip", "sps.hip", "attention.hip"]
-HEADERS = [os.path.join(CSRC, "launch.h"), os.path.join(INCLUDE, "cospec.h")]
+HEADERS = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")) + \
+    [os.path.join(INCLUDE, "cospec.h")]
 
 
 def hipcc() -> str:
