@@ -44,24 +44,37 @@ def measured_traffic(kernel_source: str):
     return rec.get("traffic_bytes_per_launch")
 
 
-def host_info():
-    """ROCm release, the GPU clocks rocm-smi reports before this process touches the GPU
-    (idle clocks, not the clocks under load) and the host's CPU model; fields that
-    cannot be read are left out."""
+def gpu_state(tag):
+    """GPU clocks (MHz) and power (W) as rocm-smi reports them, run as a child process;
+    {} when it cannot be read."""
+    import re
     import subprocess
+    out = {}
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--showpower", "--json"], capture_output=True,
+                           text=True, timeout=20)
+        card = next(iter(json.loads(r.stdout).values()))
+        for k, v in card.items():        # e.g. "sclk clock speed:": "(107Mhz)"
+            num = re.search(r"[-+]?\d+(\.\d+)?", str(v))
+            if "clock speed" in k and num:
+                out[f"{k.split()[0]}_mhz_{tag}"] = float(num.group())
+            elif "Power" in k and num:
+                out[f"power_w_{tag}"] = float(num.group())
+    except Exception:
+        pass
+    return out
+
+
+def host_info():
+    """ROCm release, the GPU state before this process touches the GPU (idle clocks, not
+    the clocks under load) and the host's CPU model; fields that cannot be read are left
+    out."""
     info = {}
     try:
         info["rocm"] = open("/opt/rocm/.info/version").read().strip()
     except OSError:
         pass
-    try:
-        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=20)
-        card = next(iter(json.loads(r.stdout).values()))
-        for k, v in card.items():        # e.g. "sclk clock speed:": "(107Mhz)"
-            if "clock speed" in k and "Mhz" in v:
-                info[k.split()[0] + "_mhz_idle_at_start"] = int(v.strip("()").replace("Mhz", ""))
-    except Exception:
-        pass
+    info.update(gpu_state("idle_at_start"))
     try:
         for ln in open("/proc/cpuinfo"):
             if ln.startswith("model name"):
@@ -310,6 +323,7 @@ def main():
     warm_pct = step_percentiles(torch, np, step, args.steps)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     cold_pct = step_percentiles(torch, np, step, args.steps, flush=lambda: scratch.fill_(0x5A))
+    hinfo.update(gpu_state("right_after_timing"))
     del scratch
     launches = 2 if args.overlap else 1             # the draft rows get their own launch
     k_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev]
