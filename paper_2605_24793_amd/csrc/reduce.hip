@@ -320,6 +320,8 @@ __device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int
     }
 }
 
+static_assert(kReduceThreads >= kMaxSeqRows, "a tree node's children are found by one thread each");
+
 // One unit of work: split `split` of row `row`, whose partial goes to slot `slot`.
 template <int DT, bool SEG>
 __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int split, int64_t slot) {
@@ -335,7 +337,7 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
         rp = a.drf + static_cast<int64_t>(r) * a.ld_bytes;
         if (a.parent) {   // tree: only nodes with a child need their draft row
             const int b = r / a.N, n = r - b * a.N;
-            const int m = n + 1 + tid;
+            const int m = n + 1 + tid;   // every later node: N <= kMaxSeqRows <= kReduceThreads
             const bool child = m < a.N && a.parent[static_cast<int64_t>(b) * a.N + m] == n;
             if (!__syncthreads_or(child)) return;
         }
