@@ -44,22 +44,30 @@ def measured_traffic(kernel_source: str):
     return rec.get("traffic_bytes_per_launch")
 
 
-def gpu_state(tag):
-    """GPU clocks (MHz) and power (W) as rocm-smi reports them, run as a child process;
-    {} when it cannot be read."""
-    import re
-    import subprocess
+def gpu_state(tag, torch=None):
+    """Current shader and memory clocks (MHz) and average power (W) of the benchmarked GPU,
+    read from its sysfs files (no other program is started: this process may already
+    have initialised the GPU); {} when the device cannot be identified or read."""
+    import glob
     out = {}
     try:
-        r = subprocess.run(["rocm-smi", "--showclocks", "--showpower", "--json"], capture_output=True,
-                           text=True, timeout=20)
-        card = next(iter(json.loads(r.stdout).values()))
-        for k, v in card.items():        # e.g. "sclk clock speed:": "(107Mhz)"
-            num = re.search(r"[-+]?\d+(\.\d+)?", str(v))
-            if "clock speed" in k and num:
-                out[f"{k.split()[0]}_mhz_{tag}"] = float(num.group())
-            elif "Power" in k and num:
-                out[f"power_w_{tag}"] = float(num.group())
+        dev = None
+        if torch is not None:
+            prop = torch.cuda.get_device_properties(0)
+            dev = "/sys/bus/pci/devices/%04x:%02x:%02x.0" % (prop.pci_domain_id, prop.pci_bus_id,
+                                                            prop.pci_device_id)
+        else:
+            cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+            if len(cards) == 1:                  # only when the device is unambiguous
+                dev = os.path.dirname(cards[0])
+        if dev is None or not os.path.isdir(dev):
+            return out
+        for clk in ("sclk", "mclk"):
+            for ln in open(os.path.join(dev, "pp_dpm_" + clk)):
+                if ln.rstrip().endswith("*"):    # e.g. "1: 2100Mhz *"
+                    out[f"{clk}_mhz_{tag}"] = float(ln.split(":")[1].split("Mhz")[0])
+        for pw in glob.glob(os.path.join(dev, "hwmon", "hwmon*", "power1_average")):
+            out[f"power_w_{tag}"] = int(open(pw).read()) / 1e6
     except Exception:
         pass
     return out
@@ -323,7 +331,7 @@ def main():
     warm_pct = step_percentiles(torch, np, step, args.steps)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     cold_pct = step_percentiles(torch, np, step, args.steps, flush=lambda: scratch.fill_(0x5A))
-    hinfo.update(gpu_state("right_after_timing"))
+    hinfo.update(gpu_state("right_after_timing", torch))
     del scratch
     launches = 2 if args.overlap else 1             # the draft rows get their own launch
     k_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev]
