@@ -58,6 +58,9 @@ struct RowReader {
     }
 };
 
+typedef __attribute__((address_space(3))) float lds_fw;
+constexpr int kSegStage = 1024;           // segments of one split staged in LDS
+
 struct Lane {
     float best;      // largest logit seen
     int chunk;       // first chunk (16-byte vector index) holding `best`, -1 if none
@@ -222,9 +225,21 @@ __device__ inline float rescale_wave(Lane &st, float cm) {
 // wave when any lane needs it, so a segment's mass is one wave sum.  Requires v0 to
 // be a multiple of kSegVecs.
 template <int DT>
-__device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int tid, Lane &st, float2 *seg) {
+__device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int tid, Lane &st, float2 *seg,
+                                        lds_fw *sst, int sbase, bool staged) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
+    // a segment's (mass, reference): into the workgroup's LDS stage when the split's
+    // segments fit it (LDS writes do not share the vector-memory counter with the
+    // rolling loads, so the loads never wait behind a store), else straight to memory
+    auto put = [&](int i, float mass) {
+        if (staged) {
+            sst[2 * (i - sbase)] = mass;
+            sst[2 * (i - sbase) + 1] = -st.nref;
+        } else {
+            seg[i] = make_float2(mass, -st.nref);
+        }
+    };
     static_assert(kUnroll == 8 && kReduceThreads % kSegVecs == 0, "segment sums assume 8 loads per lane");
     constexpr int kStep = kUnroll * kReduceThreads;
     const int lane = tid & 63;
@@ -260,7 +275,7 @@ __device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int
             st.S += mu;
         }
         const float tot = transpose_sum8(m, lane);
-        if ((lane & 7) == 0) seg[(w + (lane >> 3) * kReduceThreads) / kSegVecs] = make_float2(tot, -st.nref);
+        if ((lane & 7) == 0) put((w + (lane >> 3) * kReduceThreads) / kSegVecs, tot);
     };
     if (w + (kUnroll - 1) * kReduceThreads + 63 < v1) {   // wave-uniform: a whole batch
         u32x4 q[kUnroll];
@@ -316,7 +331,7 @@ __device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int
         }
         const float tot = transpose_sum8(m, lane);
         const int ws = w + (lane >> 3) * kReduceThreads;           // segment of value lane >> 3
-        if ((lane & 7) == 0 && ws < v1) seg[ws / kSegVecs] = make_float2(tot, -st.nref);
+        if ((lane & 7) == 0 && ws < v1) put(ws / kSegVecs, tot);
     }
 }
 
@@ -353,7 +368,11 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
     float2 *seg = nullptr;
     if (SEG && row < a.n_tgt_rows) seg = a.seg + static_cast<int64_t>(row) * a.nseg;
     const RowReader rr(rp, nvec * 16);
-    if (SEG && seg) stream_segmented<DT>(rr, v0, v1, tid, st, seg);
+    __shared__ float s_seg[SEG ? 2 * kSegStage : 1];
+    const int sbase = v0 / kSegVecs;
+    const int nsg = v1 > v0 ? (v1 - v0 + kSegVecs - 1) / kSegVecs : 0;
+    const bool staged = nsg <= kSegStage;
+    if (SEG && seg) stream_segmented<DT>(rr, v0, v1, tid, st, seg, (lds_fw *)s_seg, sbase, staged);
     else stream_plain<DT>(rr, v0, v1, tid, st);
     // elements past the last whole vector: the last split's first lane (their own
     // segment, the row's last, when segments are written)
@@ -437,6 +456,9 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
         for (int w = 1; w < kReduceThreads / 64; ++w) { SS += s_S[w]; TT += s_T[w]; }
         a.partials[slot] = make_float4(M, __int_as_float(s_idx[0]), SS, TT);
     }
+    // the staged segment masses, complete since every wave passed the barriers above
+    if (SEG && seg && staged)
+        for (int i = tid; i < nsg; i += kReduceThreads) seg[sbase + i] = make_float2(s_seg[2 * i], s_seg[2 * i + 1]);
 }
 
 // Units are (row, split) pairs of the launch's rows, split fastest.  Normally there is
