@@ -148,6 +148,9 @@ def parse():
                          "work: what a serving loop that captures its step sees)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the records of the peaked serving chain and the tree batch that the "
+                         "default run appends")
     return ap.parse_args()
 
 
@@ -216,6 +219,180 @@ def bench_attention(args):
     print(json.dumps(line), flush=True)
 
 
+def _conv(torch, bf16_bits, t):
+    return bf16_bits(t) if t.dtype == torch.bfloat16 else t.contiguous().numpy()
+
+
+class Step:
+    """One workload resident on the GPU with its pre-marshalled verify call."""
+
+    def __init__(self, cs, workloads, torch, np, wl, dev, lam, args, u_host=None, sps_u=None):
+        self.wl, self.lam, self.torch = wl, lam, torch
+        self.tree = isinstance(wl, workloads.TreeBatch)
+        head = workloads.Head(wl.head.w1.to(dev), None if wl.head.b1 is None else wl.head.b1.to(dev),
+                              wl.head.w2.to(dev), wl.head.b2)
+        tgt, drf, hid = wl.target.to(dev), wl.draft.to(dev), wl.hidden.to(dev)
+        u_dev = None if u_host is None else u_host.to(dev)
+        if self.tree:
+            par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
+            self.p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
+                                     overlap=args.overlap, sample_u=u_dev)
+            self.rows = wl.B * wl.N
+            internal = np.zeros((wl.B, wl.N), bool)
+            pn = wl.parent.numpy()
+            for b in range(wl.B):
+                for n in range(1, wl.N):
+                    internal[b, pn[b, n]] = True
+            self.reduced_rows = self.rows + int(internal.sum())
+        else:
+            tok = wl.draft_tokens.to(dev)
+            if sps_u is not None:
+                self.p = cs.prepare_sps(tgt, drf, tok, sps_u.to(dev), features=True, splits=args.splits)
+            else:
+                self.p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
+                                          overlap=args.overlap, sample_u=u_dev)
+            self.rows = wl.B * (wl.K + 1)
+            self.reduced_rows = wl.B * (2 * wl.K + 1)
+        self.elem = tgt.element_size()
+        self.logit_bytes = self.reduced_rows * wl.V * self.elem   # algorithmic bytes of the reductions
+        self.launches = 2 if args.overlap else 1                  # the draft rows get their own launch
+        self.step = self.p.launch
+
+    def warmup(self, n):
+        for _ in range(n):
+            self.step()
+        self.torch.cuda.synchronize()
+
+    def timed(self, n):
+        """n back-to-back steps between two events on the stream: ms per step, wall s."""
+        torch = self.torch
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        t0.record()
+        for _ in range(n):
+            self.step()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n, time.perf_counter() - wall0
+
+    def reduction_events(self, np, n, flush=None):
+        """HIP events recorded by the library around the vocabulary-reduction launches (on
+        the stream they run on) over n steps; with `flush`, that callable runs before every
+        step.  Returns (average launch ms, raw event interval ms, empty-pair ms)."""
+        torch = self.torch
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+        for e in (x for row in ev for x in row):
+            e.record()                                 # materialise the HIP events
+        torch.cuda.synchronize()
+        for i in range(n):
+            if flush is not None:
+                flush()
+            self.p.launch(timing=ev[i])
+        torch.cuda.synchronize()
+        k_raw = float(np.mean([e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev])) / self.launches
+        # Without the overlap stream the library records the second pair back to back with
+        # no launch between them, so that pair measures what an event interval adds on its
+        # own (barrier packets, timestamps); it is taken off the kernel's interval.
+        overhead = 0.0 if self.launches == 2 else float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+        return k_raw - overhead, k_raw, overhead
+
+
+def oracle_parity(torch, np, bf16_bits, wl, out, lam, tree, u_host=None, sps_u=None, nthreads=1,
+                  budget_s=None):
+    """Oracle over the workload's sequences, chunks of eight on `nthreads` threads (the
+    oracle's C loops release the interpreter lock), each chunk's timed GPU outputs
+    checked against it.  With budget_s the chunks run in order on one thread until the
+    budget is spent.  Returns (sequences checked, CPU seconds of oracle work)."""
+    import oracle
+    from oracle import parity
+
+    def conv(t):
+        return _conv(torch, bf16_bits, t)
+    head_np = (conv(wl.head.w1), None if wl.head.b1 is None else conv(wl.head.b1), conv(wl.head.w2),
+               wl.head.b2)
+
+    def run(seqs):
+        sub = wl.take(seqs)
+        us = None if u_host is None else u_host[seqs].double().numpy()
+        c0 = time.perf_counter()
+        if sps_u is not None:
+            ref = oracle.sps_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                   sps_u[seqs].double().numpy())
+        elif tree:
+            ref = oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
+                                     sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam, sample_u=us)
+        else:
+            ref = oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                      conv(sub.hidden), head_np, lam, sample_u=us)
+        spent = time.perf_counter() - c0
+        gsub = {k: v[seqs] for k, v in out.items()}
+        if sps_u is not None:
+            parity.check_sps(gsub, ref, conv(sub.target), conv(sub.draft), sps_u[seqs].double().numpy())
+            return len(seqs), spent
+        if us is not None:
+            # candidates at a cumulative boundary may differ; the check validates them and
+            # the rest of the step is compared on the GPU's candidates
+            cand = parity.check_candidates(gsub["tgt_candidate"], conv(sub.target), us)
+            if not np.array_equal(cand, ref["tgt_cand"]):
+                ref = (oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
+                                          sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam,
+                                          sample_u=us, cand_override=cand) if tree else
+                       oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
+                                           conv(sub.hidden), head_np, lam, sample_u=us, cand_override=cand))
+        (parity.check_tree if tree else parity.check_block)(gsub, ref)
+        return len(seqs), spent
+
+    chunk = 8
+    chunks = [list(range(s, min(wl.B, s + chunk))) for s in range(0, wl.B, chunk)]
+    if budget_s is not None:
+        done, spent = 0, 0.0
+        for c in chunks:
+            if spent >= budget_s:
+                break
+            n, t = run(c)
+            done, spent = done + n, spent + t
+        return done, spent
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=nthreads) as pool:
+        parts = list(pool.map(run, chunks))
+    return sum(n for n, _ in parts), sum(t for _, t in parts)
+
+
+def extra_workload(cs, workloads, torch, np, bf16_bits, cfg, dev, args, nthreads):
+    """Compact record of another named workload, same binary and launch sequence: step
+    time back to back, the reduction kernel's HBM fraction by HIP events with the
+    last-level cache flushed before every step, and a parity re-check of every sequence
+    (every threshold the workload names) against the oracle."""
+    wl = workloads.make_config(cfg)
+    tree = isinstance(wl, workloads.TreeBatch)
+    lam = wl.lambdas[len(wl.lambdas) // 2]
+    st = Step(cs, workloads, torch, np, wl, dev, lam, args)
+    st.warmup(args.warmup)
+    ms, _ = st.timed(args.steps)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    k_avg, k_raw, _ = st.reduction_events(np, args.steps, flush=lambda: scratch.fill_(0x5A))
+    cold = step_percentiles(torch, np, st.step, args.steps, flush=lambda: scratch.fill_(0x5A))
+    del scratch
+    checked = 0
+    for lam_i in wl.lambdas:
+        p = st if lam_i == lam else Step(cs, workloads, torch, np, wl, dev, lam_i, args)
+        if p is not st:
+            p.warmup(1)
+        out = {k: v.cpu() for k, v in p.p.result().items()}
+        n, _ = oracle_parity(torch, np, bf16_bits, wl, out, lam_i, tree, nthreads=nthreads)
+        checked += n
+    launch_bytes = st.logit_bytes / st.launches
+    gbps = launch_bytes / (k_avg * 1e-3) / 1e9
+    return {"workload": wl.name, "lambda": lam, "ms_per_step": ms, "rows_per_s": st.rows / (ms * 1e-3),
+            "step_ms_cache_flushed": cold,
+            "reduction_cache_flushed": {"kernel": "k_vocab_reduce", "kernel_ms": k_avg,
+                                        "event_interval_ms": k_raw, "achieved_gbps": gbps,
+                                        "frac": gbps / HBM_PEAK_GBPS,
+                                        "algorithmic_bytes_per_launch": launch_bytes},
+            "parity_checked_sequences": checked, "lambdas_checked": list(wl.lambdas)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -238,195 +415,94 @@ def main():
     wl = workloads.make_config(args.config)
     tree = isinstance(wl, workloads.TreeBatch)
     lam = wl.lambdas[len(wl.lambdas) // 2]
-    head = workloads.Head(wl.head.w1.to(dev), None if wl.head.b1 is None else wl.head.b1.to(dev),
-                          wl.head.w2.to(dev), wl.head.b2)
-    tgt, drf, hid = wl.target.to(dev), wl.draft.to(dev), wl.hidden.to(dev)
     u_host = None
     if args.sample:
         R = wl.N if tree else wl.K + 1
         u_host = torch.rand((wl.B, R), generator=torch.Generator().manual_seed(2024))
-    u_dev = None if u_host is None else u_host.to(dev)
     sps_u = None
     if args.sps:
         if tree:
             print(json.dumps({"error": "--sps runs on chain workloads"}))
             sys.exit(2)
         sps_u = torch.rand((wl.B, wl.K + 1), generator=torch.Generator().manual_seed(2025))
-    if tree:
-        par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
-        p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
-                            overlap=args.overlap, sample_u=u_dev)
-        rows = wl.B * wl.N
-        internal = np.zeros((wl.B, wl.N), bool)
-        pn = wl.parent.numpy()
-        for b in range(wl.B):
-            for n in range(1, wl.N):
-                internal[b, pn[b, n]] = True
-        reduced_rows = rows + int(internal.sum())
-    else:
-        tok = wl.draft_tokens.to(dev)
-        if args.sps:
-            p = cs.prepare_sps(tgt, drf, tok, sps_u.to(dev), features=True, splits=args.splits)
-        else:
-            p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
-                                 overlap=args.overlap, sample_u=u_dev)
-        rows = wl.B * (wl.K + 1)
-        reduced_rows = wl.B * (2 * wl.K + 1)
-    elem = tgt.element_size()
-    logit_bytes = reduced_rows * wl.V * elem       # algorithmic bytes of the two reduction launches
-
+    if args.graph and args.overlap:
+        print(json.dumps({"error": "--graph does not capture the aux stream"}))
+        sys.exit(2)
+    st = Step(cs, workloads, torch, np, wl, dev, lam, args, u_host=u_host, sps_u=sps_u)
     torch.cuda.synchronize()
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        p.launch()
-    torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    step = p.launch
+    st.warmup(args.warmup)
     if args.graph:
-        if args.overlap:
-            print(json.dumps({"error": "--graph does not capture the aux stream"}))
-            sys.exit(2)
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
-            p.launch()
+            st.p.launch()
         torch.cuda.current_stream().wait_stream(side)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            p.launch()
-        step = graph.replay
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
+            st.p.launch()
+        st.step = graph.replay
+        st.warmup(args.warmup)
 
-    # timed region 1: the whole step, back to back, nothing else on the stream
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t0.record()
-    for _ in range(args.steps):
-        step()
-    t1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = t0.elapsed_time(t1)
-
-    # timed region 2: the same steps with HIP events recorded by the library around
-    # the two vocabulary-reduction launches (target rows, draft rows), on the stream
-    # they run on
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for e in (x for row in ev for x in row):
-        e.record()                                 # materialise the HIP events
-    torch.cuda.synchronize()
+    # Measurement loops that report on the same step run first, each exactly `steps`
+    # steps: the reduction kernel's own launches by HIP events, then the per-step time
+    # distribution back to back and with the 256 MB last-level cache (MALL) flushed before
+    # every step by writing a 512 MB buffer outside the step's events.  The headline loop
+    # then times `steps` steps of a GPU that has been running this step.
     print(f"[bench] timing the reduction kernel over {args.steps} steps", file=sys.stderr, flush=True)
-    for i in range(args.steps):
-        p.launch(timing=ev[i])
-    torch.cuda.synchronize()
-    # per-step distribution: back to back, and with the 256 MB last-level cache (MALL)
-    # flushed before every step by writing a 512 MB buffer outside the step's events
+    k_avg, k_raw, ev_overhead = st.reduction_events(np, args.steps)
     print(f"[bench] per-step times, warm and with the cache flushed, {args.steps} steps each",
           file=sys.stderr, flush=True)
-    warm_pct = step_percentiles(torch, np, step, args.steps)
+    warm_pct = step_percentiles(torch, np, st.step, args.steps)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    cold_pct = step_percentiles(torch, np, step, args.steps, flush=lambda: scratch.fill_(0x5A))
-    hinfo.update(gpu_state("right_after_timing", torch))
+    cold_pct = step_percentiles(torch, np, st.step, args.steps, flush=lambda: scratch.fill_(0x5A))
     del scratch
-    launches = 2 if args.overlap else 1             # the draft rows get their own launch
-    k_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev]
-    k_raw = float(np.mean(k_ms)) / launches         # event interval per launch
-    # Without the overlap stream the library records the second pair back to back with
-    # no launch between them, so that pair measures what an event interval adds on its
-    # own (barrier packets, timestamps); it is taken off the kernel's interval.
-    ev_overhead = 0.0 if args.overlap else float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
-    k_avg = k_raw - ev_overhead                     # average duration of one launch
-    ms_per_step = total_ms / args.steps
-    value = rows / (ms_per_step * 1e-3)
-    launch_bytes = logit_bytes / launches
-    achieved = launch_bytes / (k_avg * 1e-3) / 1e9
-    res = p.result()
-    out = {k: v.cpu() for k, v in res.items()}
+    st.warmup(args.warmup)
+    hinfo.update(gpu_state("before_headline", torch))
 
-    # CPU oracle on a bounded sample (first sequences of the same workload), also a
-    # parity re-check of the timed outputs on those sequences
+    # the headline: `steps` whole steps back to back, nothing else on the stream
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    ms_per_step, wall = st.timed(args.steps)
+    hinfo.update(gpu_state("right_after_timing", torch))
+    value = st.rows / (ms_per_step * 1e-3)
+    launch_bytes = st.logit_bytes / st.launches
+    achieved = launch_bytes / (k_avg * 1e-3) / 1e9
+    out = {k: v.cpu() for k, v in st.p.result().items()}
+
+    nth = oracle_threads()
+    extras = {}
+    default_mode = (args.config == 4 and not (args.sample or args.sps or args.overlap or args.graph
+                                              or args.splits) and not args.no_extras)
+    if default_mode:
+        for key, cfg in (("peaked_chain", 3), ("tree", 5)):
+            print(f"[bench] workload {cfg}: timing, flushed reduction events, parity of every sequence",
+                  file=sys.stderr, flush=True)
+            extras[key] = extra_workload(cs, workloads, torch, np, bf16_bits, cfg, dev, args, nth)
+
+    # CPU oracle on a bounded sample (first sequences of the same workload), also a parity
+    # re-check of the timed outputs on those sequences; then the same sequences on a pool
     cpu = cpu_par = None
     if args.cpu_seconds > 0:
-        import oracle
-        from oracle import parity
-
-        def conv(t):
-            return bf16_bits(t) if t.dtype == torch.bfloat16 else t.contiguous().numpy()
-        head_np = (conv(wl.head.w1), None if wl.head.b1 is None else conv(wl.head.b1),
-                   conv(wl.head.w2), wl.head.b2)
-        done, spent, chunk = 0, 0.0, 8
-        checked = 0
-        while done < wl.B and spent < args.cpu_seconds:
-            seqs = list(range(done, min(wl.B, done + chunk)))
-            sub = wl.take(seqs)
-            us = None if u_host is None else u_host[seqs].double().numpy()
-            c0 = time.perf_counter()
-            if args.sps:
-                ref = oracle.sps_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
-                                       sps_u[seqs].double().numpy())
-            elif tree:
-                ref = oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(),
-                                         sub.node_tokens.numpy(), conv(sub.hidden), head_np, lam,
-                                         sample_u=us)
-            else:
-                ref = oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
-                                          conv(sub.hidden), head_np, lam, sample_u=us)
-            spent += time.perf_counter() - c0
-            gsub = {k: v[seqs] for k, v in out.items()}
-            if args.sps:
-                parity.check_sps(gsub, ref, conv(sub.target), conv(sub.draft), sps_u[seqs].double().numpy())
-                checked += len(seqs)
-                done += len(seqs)
-                continue
-            if us is not None:
-                # candidates at a cumulative boundary may differ; the check validates
-                # them and the rest of the step is compared on the GPU's candidates
-                cand = parity.check_candidates(gsub["tgt_candidate"], conv(sub.target), us)
-                if not np.array_equal(cand, ref["tgt_cand"]):
-                    fn = oracle.verify_tree if tree else oracle.verify_block
-                    ref = (fn(conv(sub.target), conv(sub.draft), sub.parent.numpy(), sub.node_tokens.numpy(),
-                              conv(sub.hidden), head_np, lam, sample_u=us, cand_override=cand) if tree else
-                           fn(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(), conv(sub.hidden),
-                              head_np, lam, sample_u=us, cand_override=cand))
-            (parity.check_tree if tree else parity.check_block)(gsub, ref)
-            checked += len(seqs)
-            done += len(seqs)
+        print("[bench] oracle baseline", file=sys.stderr, flush=True)
+        done, spent = oracle_parity(torch, np, bf16_bits, wl, out, lam, tree, u_host, sps_u,
+                                    budget_s=args.cpu_seconds)
         cpu_rows = done * (wl.N if tree else wl.K + 1)
+        host_cpus = os.cpu_count()
         cpu = {"value": cpu_rows / spent, "unit": "rows/s", "cores": 1, "kind": "oracle",
                "sample": f"first {done} of {wl.B} sequences ({cpu_rows} verified rows) of the same "
                          f"workload, fp64 oracle, single thread, {spent:.1f} s",
-               "parity_checked_sequences": checked}
-
-        # the same sequences again, one chunk per task on a thread pool: the oracle's C
-        # loops release the interpreter lock, so its row reductions run in parallel
-        from concurrent.futures import ThreadPoolExecutor
-        nth = oracle_threads()
-
-        def run_chunk(seqs):
-            sub = wl.take(seqs)
-            us = None if u_host is None else u_host[seqs].double().numpy()
-            if args.sps:
-                oracle.sps_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
-                                 sps_u[seqs].double().numpy())
-            elif tree:
-                oracle.verify_tree(conv(sub.target), conv(sub.draft), sub.parent.numpy(), sub.node_tokens.numpy(),
-                                   conv(sub.hidden), head_np, lam, sample_u=us)
-            else:
-                oracle.verify_block(conv(sub.target), conv(sub.draft), sub.draft_tokens.numpy(),
-                                    conv(sub.hidden), head_np, lam, sample_u=us)
-        chunks = [list(range(s, min(done, s + chunk))) for s in range(0, done, chunk)]
+               "parity_checked_sequences": done, "host_cpus": host_cpus}
+        sub = wl.take(list(range(done)))
+        sout = {k: v[:done] for k, v in out.items()}
         c0 = time.perf_counter()
-        with ThreadPoolExecutor(max_workers=nth) as pool:
-            list(pool.map(run_chunk, chunks))
+        oracle_parity(torch, np, bf16_bits, sub, sout, lam, tree, None if u_host is None else u_host[:done],
+                      None if sps_u is None else sps_u[:done], nthreads=nth)
         par_spent = time.perf_counter() - c0
         cpu_par = {"value": cpu_rows / par_spent, "unit": "rows/s", "cores": nth, "kind": "oracle",
-                   "sample": f"the same {done} sequences, {len(chunks)} chunks of up to {chunk} on "
-                             f"{nth} threads, {par_spent:.1f} s"}
+                   "sample": f"the same {done} sequences, chunks of up to 8 on {nth} threads "
+                             f"(of {host_cpus} host CPUs), {par_spent:.1f} s",
+                   "host_cpus": host_cpus}
 
     line = {
         "metric": METRIC,
@@ -439,7 +515,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if elem == 2 else "f32",
+        "dtype": "bf16" if st.elem == 2 else "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
@@ -447,8 +523,10 @@ def main():
                    "hip_graph": args.graph,
                    "temperature": 1 if args.sample or args.sps else 0,
                    "rule": "speculative sampling" if args.sps else "cospec",
-                   "rows_per_step": rows,
-                   "reduced_rows_per_step": reduced_rows},
+                   "rows_per_step": st.rows,
+                   "reduced_rows_per_step": st.reduced_rows,
+                   "loops_before_headline": "warmup, reduction-kernel events, warm and flushed "
+                                            f"per-step times ({args.steps} steps each), warmup"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
@@ -456,8 +534,8 @@ def main():
                                  and not args.sps else None),
                      "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
                      "event_interval_ms": k_raw, "empty_event_interval_ms": ev_overhead,
-                     "launches_per_step": launches, "algorithmic_bytes_per_launch": launch_bytes},
-        "step_hbm_gbps": logit_bytes / (ms_per_step * 1e-3) / 1e9,
+                     "launches_per_step": st.launches, "algorithmic_bytes_per_launch": launch_bytes},
+        "step_hbm_gbps": st.logit_bytes / (ms_per_step * 1e-3) / 1e9,
         "wall_s": wall,
         "mean_accept_len": float(out["accept_len"].float().mean()),
         "step_ms_warm": warm_pct,
@@ -466,6 +544,7 @@ def main():
         "cpu_baseline": cpu,
         "cpu_baseline_threads": cpu_par,
     }
+    line.update({f"workload_{k}": v for k, v in extras.items()})
     print(json.dumps(line), flush=True)
 
 

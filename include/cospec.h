@@ -13,7 +13,7 @@
  * mismatch (Eq. cospec_length): it emits the draft tokens before that position
  * and the target token there, or all K draft tokens plus the bonus token.
  *
- * At temperature 1 (Section 2, stochastic decoding; Appendix C.3) the target's
+ * At temperature 1 (Section 3.1, stochastic decoding; Appendix C.3) the target's
  * verification candidate is a sample of softmax(target row) instead of its
  * argmax; the same arbitration rule then applies to the pair.  The library takes
  * that sample by inversion of a caller-supplied uniform (cospec_options).
@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define COSPEC_ABI_VERSION 4
+#define COSPEC_ABI_VERSION 5
 #define COSPEC_MAX_K 64      /* chain: draft tokens per block              */
 #define COSPEC_MAX_N 256     /* tree: nodes per tree, root included        */
 #define COSPEC_MAX_SPLITS 64 /* workgroups per logit row (tuning override) */
@@ -114,13 +114,13 @@ typedef struct {
                               (the argmax, or the temperature-1 sample)        */
     float *logp_action;    /* per decision: log pi(a_i) of the action taken,
                               log sigma(z) if accepted, log sigma(-z) if not
-                              (the rollout-time probability of Section 3.2);
+                              (the rollout-time probability of Section 3.4);
                               0 on matches, NaN where the head did not run or
                               the draft token is invalid                      */
 } cospec_features;
 
 /*
- * Per-round statistics of the reinforcement-learning stage (Section 3.2), for
+ * Per-round statistics of the reinforcement-learning stage (Section 3.4), for
  * chains only.  With decisions i = 1..K, s the round length and Delta, a the
  * mismatch flags and actions:
  *   effective actions  I = {i : Delta_i = 0 and i <= min(s, K)}
@@ -183,7 +183,7 @@ typedef struct {
      */
     const float *sample_uniform;
     /*
-     * Sampled arbitration (Section 3.2: rollouts draw mismatch actions from the
+     * Sampled arbitration (Section 3.4: rollouts draw mismatch actions from the
      * policy).  NULL: a_i = 1[sigma(z_i) > lambda] (Eq. infer_thre).  Otherwise
      * one uniform per decision ([B][K] chain, [B][N] tree) and a mismatch is
      * accepted when policy_uniform < sigma(z_i) (fp32); lambda is then unused.
@@ -205,8 +205,26 @@ typedef struct {
 /* COSPEC_ABI_VERSION of the built library. */
 int32_t cospec_abi_version(void);
 
+/*
+ * Build id of the library: the first 32 hex digits of the SHA-256 of the sources and
+ * headers it was compiled from, set by the build ("unknown" if the build set none).
+ * Build tooling compares it with the sources on disk to refuse a stale binary.
+ */
+const char *cospec_build_id(void);
+
 /* Static string naming a status code (never NULL). */
 const char *cospec_status_string(int32_t status);
+
+/*
+ * Workspace bytes for a step with n_target_rows target rows, n_draft_rows draft rows
+ * and n_decisions decision slots over vocabularies of V entries, with the head `head`
+ * (NULL: the head does not run, as in cospec_verify_block_sps).  For a chain batch
+ * these are B(K+1), BK and BK; for a tree batch BN, BN and BN.  The result equals the
+ * matching per-entry query below (0 for negative counts, V < 1 or an invalid head).
+ * The workspace must be 256-byte aligned.
+ */
+size_t cospec_workspace_bytes(int32_t n_target_rows, int32_t n_draft_rows, int32_t n_decisions, int32_t V,
+                              const cospec_head *head);
 
 /*
  * Workspace bytes cospec_verify_block needs for these sizes (0 for invalid
@@ -283,8 +301,8 @@ cospec_status cospec_verify_block_arbitrate(const void *target_logits, const voi
 
 /*
  * Standard speculative sampling over B chain blocks: the distribution-
- * preserving baseline the paper compares against at temperature 1 (Section 2,
- * Appendix C.3), on the same reductions.  Draft token i (drawn by the caller
+ * preserving baseline the paper compares against at temperature 1 (Section 3.1,
+ * stochastic decoding; Appendix C.3), on the same reductions.  Draft token i (drawn by the caller
  * from draft row i-1) is accepted when uniforms[b][i-1] < p_T(token) /
  * p_D(token) (target and draft rows i-1), i.e. with probability min(1, ratio);
  * the round stops at the first rejection s and emits draft tokens 1..s-1, then

@@ -15,9 +15,8 @@ Readings of the paper used here (each also listed with the design notes):
   * entropy is the Shannon entropy in nats of softmax(logits) over the whole
     vocabulary; log-probabilities are reported (logp = x[token] - lse);
   * the head g_phi is a two-layer MLP  z = w2 . relu(W1 h + b1) + b2;
-  * the threshold is strict (a = 1[pi > lambda]) and is decided in fp32, the
-    precision the GPU path takes it in; decisions with |sigma(z) - lambda| <= 1e-3
-    (in fp64) are flagged ambiguous;
+  * the threshold is strict (a = 1[pi > lambda], decided in fp64); decisions with
+    |sigma(z) - lambda| <= 1e-3 are flagged ambiguous;
   * every mismatch decision is scored, not only those before the stop;
   * at temperature 1 the target's verification candidate of a row is a sample
     of softmax(row), taken by inversion of a caller-supplied uniform u: the
@@ -55,17 +54,26 @@ SPS_BAND = 1e-4                     # speculative-sampling tests closer than thi
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cospec_oracle.c")
-_SO = os.path.join(_HERE, "libcospec_oracle.so")
+# COSPEC_ORACLE_SANITIZE=1 builds and loads a copy instrumented with AddressSanitizer and
+# UndefinedBehaviorSanitizer (host code only; the process must preload libasan), so that
+# the pins can be run with every array access of the C loops checked.
+_SANITIZE = os.environ.get("COSPEC_ORACLE_SANITIZE") == "1"
+_SO = os.path.join(_HERE, "libcospec_oracle_san.so" if _SANITIZE else "libcospec_oracle.so")
 _lib = None
 
 
-def build() -> str:
-    """Compile the C half of the oracle with gcc (IEEE semantics, no fast-math)."""
-    tmp = _SO + ".tmp"
-    subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math", "-o", tmp,
-                    _SRC, "-lm"], check=True)
-    os.replace(tmp, _SO)
-    return _SO
+def build(sanitize: bool = _SANITIZE) -> str:
+    """Compile the C half of the oracle with gcc (IEEE semantics, no fast-math); with
+    `sanitize`, instrumented for out-of-bounds accesses and undefined behaviour, any
+    finding fatal."""
+    so = os.path.join(_HERE, "libcospec_oracle_san.so" if sanitize else "libcospec_oracle.so")
+    tmp = so + ".tmp"
+    extra = (["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+              "-fno-sanitize-recover=all"] if sanitize else [])
+    subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math"] + extra +
+                   ["-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, so)
+    return so
 
 
 def _load():
@@ -208,7 +216,7 @@ def residual_sample(target_rows, draft_rows, u=None, query=None):
 
 def sps_block(target, draft, draft_tokens, u) -> dict:
     """Standard speculative sampling over a chain block, the distribution-preserving
-    baseline the paper runs at T = 1 (Section 2, Appendix C.3).
+    baseline the paper runs at T = 1 (Section 3.1, stochastic decoding; Appendix C.3).
 
     target [B, K+1, V], draft [B, K, V], draft_tokens [B, K] (drawn from the draft),
     u [B, K+1] uniforms.  Draft token i (rows i-1) is accepted when u[b, i-1] <
@@ -275,7 +283,7 @@ def final_token(target_seq, draft_seq, s: int, u_last: float, query=None):
 def candidates(target, stats: "RowStats", sample_u=None, override=None):
     """The target's verification candidate of every target row: the argmax at
     T = 0 (Section 3.1), a temperature-1 sample by inversion of the uniform
-    `sample_u` at T = 1 (Section 2, Appendix C.3).  `override` replaces the
+    `sample_u` at T = 1 (Section 3.1, stochastic decoding; Appendix C.3).  `override` replaces the
     computed candidates (a test passes another implementation's candidates
     after checking each against cdf_at)."""
     if override is not None:
@@ -311,43 +319,34 @@ def head_logits(hidden: np.ndarray, rows, w1: np.ndarray, b1: Optional[np.ndarra
 
 
 def policy_accept(z: np.ndarray, lam: float):
-    """pi = sigma(z) (Eq. policy-prob) and a = 1[pi > lambda] (Eq. infer_thre).
-
-    The decision is taken in fp32 (z rounded to fp32, sigma in fp32, compared with
-    lambda as fp32), the precision the GPU takes it in; pi is also returned in
-    fp64 with the flag |pi - lambda| <= 1e-3 marking decisions too close to call.
-    """
+    """pi = sigma(z) (Eq. policy-prob) and a = 1[pi > lambda] (Eq. infer_thre), both in
+    fp64 with lambda as given.  Decisions with |pi - lambda| <= 1e-3 are flagged
+    ambiguous: an implementation that rounds differently may take them either way."""
     z = np.asarray(z, dtype=np.float64)
-    lam32 = np.float32(lam)
+    lam = float(lam)
     with np.errstate(over="ignore"):
-        z32 = z.astype(np.float32)
-        pi32 = np.float32(1.0) / (np.float32(1.0) + np.exp(-z32))
         pi = 1.0 / (1.0 + np.exp(-z))
-    accept = pi32 > lam32
-    ambiguous = np.abs(pi - np.float64(lam32)) <= AMBIGUITY_BAND
+    accept = pi > lam
+    ambiguous = np.abs(pi - lam) <= AMBIGUITY_BAND
     return accept, pi, ambiguous
 
 
 def policy_sample(z: np.ndarray, u):
-    """Sampled arbitration (Section 3.2: at training time mismatch actions are drawn
-    from pi_theta): a = 1[u < pi] for a caller-supplied uniform u, with pi = sigma(z)
-    taken in fp32 as in policy_accept; decisions with |pi - u| <= 1e-3 (fp64) are
-    flagged ambiguous."""
+    """Sampled arbitration (Section 3.4: at training time mismatch actions are drawn
+    from pi_theta): a = 1[u < pi] for a caller-supplied uniform u, with pi = sigma(z),
+    in fp64; decisions with |pi - u| <= 1e-3 are flagged ambiguous."""
     z = np.asarray(z, dtype=np.float64)
     u = np.asarray(u, dtype=np.float64)
     with np.errstate(over="ignore"):
-        z32 = z.astype(np.float32)
-        pi32 = np.float32(1.0) / (np.float32(1.0) + np.exp(-z32))
         pi = 1.0 / (1.0 + np.exp(-z))
-    u32 = u.astype(np.float32)
-    accept = u32 < pi32
-    ambiguous = np.abs(pi - u32.astype(np.float64)) <= AMBIGUITY_BAND
+    accept = u < pi
+    ambiguous = np.abs(pi - u) <= AMBIGUITY_BAND
     return accept, pi, ambiguous
 
 
 def action_logprob(z: np.ndarray, accept) -> np.ndarray:
     """log pi_theta(a | q) of the action taken on a mismatch decision (the rollout-time
-    probability in the PPO ratio of Section 3.2): log sigma(z) when a = 1 and
+    probability in the PPO ratio of Section 3.4): log sigma(z) when a = 1 and
     log(1 - sigma(z)) = log sigma(-z) when a = 0, in fp64."""
     z = np.asarray(z, dtype=np.float64)
     x = np.where(np.asarray(accept, bool), z, -z)
@@ -357,7 +356,7 @@ def action_logprob(z: np.ndarray, accept) -> np.ndarray:
 
 def rl_round(delta, accept, logp_tgt, correct: bool, alpha: float = RL_ALPHA,
              beta: float = RL_BETA) -> dict:
-    """Per-round statistics of the reinforcement-learning stage (Section 3.2) for one
+    """Per-round statistics of the reinforcement-learning stage (Section 3.4) for one
     chain round with decisions i = 1..K (index i-1 of each array).
 
       s      the round length (Eq. cospec_length);

@@ -125,7 +125,7 @@ static int oracle_softmax_row(const void *row, int dtype, int64_t V, double *p)
 }
 
 /*
- * Sampling at temperature 1 (Section 2, stochastic decoding; Appendix C.3: at
+ * Sampling at temperature 1 (Section 3.1, stochastic decoding; Appendix C.3: at
  * T = 1 the target's verification candidate is a sample from its next-token
  * distribution).  The sample is taken by inversion: given a uniform u in [0, 1)
  * for row r, the candidate is the smallest v whose cumulative probability
@@ -196,7 +196,7 @@ int64_t oracle_cdf_at(const void *rows, int dtype, int64_t ld, int64_t nrows, in
 
 /*
  * Resampling step of standard speculative sampling (the distribution-preserving
- * baseline the paper runs at T = 1, Section 2 and Appendix C.3).  With p = the
+ * baseline the paper runs at T = 1, Section 3.1 (stochastic decoding) and Appendix C.3).  With p = the
  * softmax of a target row and q = the softmax of the draft row at the same
  * position, the residual distribution is max(0, p - q) / Z, Z = sum_v max(0,
  * p[v] - q[v]); with no draft row (drf == NULL) the distribution is p itself

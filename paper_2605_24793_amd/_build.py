@@ -1,6 +1,7 @@
 """Builds libcospec.so (the HIP kernels and the C ABI) in-tree for gfx950."""
 from __future__ import annotations
 
+import hashlib
 import os
 import shutil
 import subprocess
@@ -22,11 +23,28 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libcospec.so)")
 
 
+def source_files() -> list:
+    """Every file the library is built from, in a fixed order: the HIP sources, then
+    the headers sorted by path."""
+    return [os.path.join(CSRC, s) for s in SOURCES] + HEADERS
+
+
+def source_hash() -> str:
+    """Build id of the current sources: the first 32 hex digits of the SHA-256 of their
+    concatenation in source_files() order (the Makefile computes the same)."""
+    h = hashlib.sha256()
+    for p in source_files():
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:32]
+
+
 def flags() -> list:
     return ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
             # no packed fp32 VALU instructions anywhere in the device code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-Wall", "-Wno-unused-result", "-I", INCLUDE]
+            "-Wall", "-Wno-unused-result", "-I", INCLUDE,
+            f"-DCOSPEC_BUILD_ID=\"{source_hash()}\""]
 
 
 def build(verbose: bool = False) -> str:
@@ -49,7 +67,7 @@ def stale() -> bool:
     if not os.path.exists(LIB):
         return True
     t = os.path.getmtime(LIB)
-    return any(os.path.getmtime(p) > t for p in [os.path.join(CSRC, s) for s in SOURCES] + HEADERS)
+    return any(os.path.getmtime(p) > t for p in source_files())
 
 
 if __name__ == "__main__":

@@ -70,7 +70,9 @@ def _event_handle(ev) -> int:
 
 
 def lib():
-    """The loaded library (built first if no build exists)."""
+    """The loaded library, built first if no build exists.  A build whose id (the hash
+    of the sources it was compiled from) differs from the sources on disk is refused:
+    the kernels it holds are not the ones in csrc/."""
     global _lib
     if _lib is None:
         if not os.path.exists(_build.LIB):
@@ -78,8 +80,16 @@ def lib():
         L = ctypes.CDLL(_build.LIB)
         P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         HP = ctypes.POINTER(_Head)
+        L.cospec_build_id.restype = ctypes.c_char_p
+        L.cospec_build_id.argtypes = []
+        built, want = L.cospec_build_id().decode(), _build.source_hash()
+        if built != want:
+            raise CospecError(f"{_build.LIB} is stale: built from sources {built}, the sources on disk are "
+                              f"{want}; rebuild it (python -m paper_2605_24793_amd._build)")
         L.cospec_abi_version.restype = I32
         L.cospec_abi_version.argtypes = []
+        L.cospec_workspace_bytes.restype = SZ
+        L.cospec_workspace_bytes.argtypes = [I32, I32, I32, I32, HP]
         L.cospec_status_string.restype = ctypes.c_char_p
         L.cospec_status_string.argtypes = [I32]
         L.cospec_verify_block_workspace_size.restype = SZ

@@ -426,6 +426,11 @@ extern "C" {
 
 int32_t cospec_abi_version(void) { return COSPEC_ABI_VERSION; }
 
+#ifndef COSPEC_BUILD_ID
+#define COSPEC_BUILD_ID "unknown"
+#endif
+const char *cospec_build_id(void) { return COSPEC_BUILD_ID; }
+
 const char *cospec_status_string(int32_t status) {
     switch (status) {
         case COSPEC_OK: return "ok";
@@ -435,6 +440,15 @@ const char *cospec_status_string(int32_t status) {
         case COSPEC_ERR_HIP: return "HIP error";
         default: return "unknown status";
     }
+}
+
+size_t cospec_workspace_bytes(int32_t n_target_rows, int32_t n_draft_rows, int32_t n_decisions, int32_t V,
+                              const cospec_head *head) {
+    if (n_target_rows < 0 || n_draft_rows < 0 || n_decisions < 0 || V < 1) return 0;
+    if (head && check_head(head) != COSPEC_OK) return 0;
+    // the layout depends on the batch only through these three counts (B * rows per
+    // sequence), so one "sequence" holding all of them gives the same sizes
+    return layout(static_cast<int64_t>(n_target_rows) + n_draft_rows, 1, n_target_rows, n_decisions, head, V).total;
 }
 
 size_t cospec_verify_block_workspace_size(int32_t B, int32_t K, int32_t V, const cospec_head *head) {

@@ -1,4 +1,4 @@
-// Temperature-1 verification candidates (Section 2, stochastic decoding; at
+// Temperature-1 verification candidates (Section 3.1, stochastic decoding; at
 // T = 1 the target's candidate is a sample of its next-token distribution,
 // Appendix C.3).  The sample is taken by inversion of a caller-supplied uniform
 // u: the candidate of a row is the smallest v whose cumulative probability

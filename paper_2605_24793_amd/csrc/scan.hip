@@ -137,7 +137,7 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
         a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = j < s - 1 ? td : j == s - 1 ? tt : -1;
     }
     if (!a.rl_on) return;
-    // Section 3.2: effective actions up to the stop, rho, S_acc / S_rej and the
+    // Section 3.4: effective actions up to the stop, rho, S_acc / S_rej and the
     // shaped reward; the first rejected mismatch is the stop itself (or K+1)
     const uint64_t mm = __ballot(mism);
     const int i_star = mm ? __builtin_ctzll(mm) + 1 : 0;

@@ -1,5 +1,5 @@
 // Standard speculative sampling over chain blocks: the distribution-preserving
-// baseline the paper runs at temperature 1 (Section 2, Appendix C.3), on the
+// baseline the paper runs at temperature 1 (Section 3.1, stochastic decoding; Appendix C.3), on the
 // same reductions as the CoSpec step.
 //
 // k_sps_finish (one wave per sequence, lane i-1 owns draft token i): merges the

@@ -67,6 +67,38 @@ def test_workspace_sizes():
     assert L.cospec_verify_block_workspace_size(1, 4, 100, ctypes.byref(bad)) == 0
 
 
+@pytest.mark.parametrize("B,K,V", [(64, 7, 151936), (256, 7, 151936), (1, 4, 32000), (8, 5, 128256),
+                                   (0, 7, 100), (5, 0, 1000), (300, 64, 9)])
+def test_generic_workspace_query_matches_the_per_entry_queries(B, K, V):
+    L = cs.lib()
+    hd = _head(d=5120, h=512)
+    block = L.cospec_verify_block_workspace_size(B, K, V, ctypes.byref(hd))
+    assert L.cospec_workspace_bytes(B * (K + 1), B * K, B * K, V, ctypes.byref(hd)) == block
+    N = K + 1
+    tree = L.cospec_verify_tree_workspace_size(B, N, V, ctypes.byref(hd))
+    assert L.cospec_workspace_bytes(B * N, B * N, B * N, V, ctypes.byref(hd)) == tree
+    sps = L.cospec_verify_block_sps_workspace_size(B, K, V)
+    assert L.cospec_workspace_bytes(B * (K + 1), B * K, B * K, V, None) == sps
+
+
+def test_generic_workspace_query_rejects_invalid_sizes():
+    L = cs.lib()
+    hd = _head()
+    assert L.cospec_workspace_bytes(-1, 0, 0, 100, ctypes.byref(hd)) == 0
+    assert L.cospec_workspace_bytes(8, -1, 0, 100, ctypes.byref(hd)) == 0
+    assert L.cospec_workspace_bytes(8, 7, -1, 100, ctypes.byref(hd)) == 0
+    assert L.cospec_workspace_bytes(8, 7, 7, 0, ctypes.byref(hd)) == 0
+    bad = _head(d=12)
+    assert L.cospec_workspace_bytes(8, 7, 7, 100, ctypes.byref(bad)) == 0
+
+
+def test_build_id_matches_the_sources():
+    from paper_2605_24793_amd import _build
+    L = cs.lib()
+    assert L.cospec_build_id().decode() == _build.source_hash()
+    assert re.fullmatch(r"[0-9a-f]{32}", _build.source_hash())
+
+
 def _block(L, **kw):
     a = dict(tgt=FAKE, drf=FAKE, dt=1, ld=151936, toks=FAKE, hid=FAKE, head=_head(), lam=0.5,
              B=4, K=7, V=151936, alen=FAKE, otok=FAKE, feats=None, opts=None, ws=FAKE, wsb=1 << 30)

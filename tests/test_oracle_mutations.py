@@ -2,7 +2,7 @@
 
 Each case copies oracle/ to a temporary directory, applies one textual mutation
 (a dropped term, a wrong sign, a wrong index, a transposed operand, a flipped
-comparison), builds it, and runs tests/test_oracle_pins.py against the copy in a
+comparison, a dropped filter), builds it, and runs tests/test_oracle_pins.py against the copy in a
 subprocess.  The pins must fail.  This runs on the CPU only.
 """
 import os
@@ -42,7 +42,7 @@ MUTATIONS = [
     ("__init__.py", "s_acc[i - 1] = bool(accept[i - 1]) and i < i_rej",
      "s_acc[i - 1] = i <= i_rej"),                                            # rejected one in S_acc
     ("__init__.py", "- beta * s_rej[i - 1])", "+ beta * s_rej[i - 1])"),        # rejection rewarded
-    ("__init__.py", "accept = u32 < pi32", "accept = u32 <= pi32"),
+    ("__init__.py", "accept = u < pi", "accept = u <= pi"),
     ("cospec_oracle.c", "p[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;", "p[v] = p[v] - q[v];"),   # unclipped residual
     ("__init__.py", "accept = uu[:, :K] < ratio", "accept = uu[:, :K] < 1.0 / ratio"),        # inverted ratio
     ("__init__.py", "vis = np.arange(p + 1) if p < lc else np.arange(ln)",
@@ -52,8 +52,16 @@ MUTATIONS = [
     ("__init__.py", "t = target_seq[s - 1: s]", "t = target_seq[s - 2: s - 1]"),           # resample wrong row
     ("__init__.py", "logp_tgt = _gather(target[:, :K, :], toks)", "logp_tgt = _gather(target[:, 1:, :], toks)"),
     ("__init__.py", "if ok[n] and depth[n] > depth[best]:", "if ok[n] and depth[n] >= depth[best]:"),
-    ("__init__.py", "accept = pi32 > lam32", "accept = pi32 >= lam32"),        # non-strict threshold
+    ("__init__.py", "accept = pi > lam", "accept = pi >= lam"),                # non-strict threshold
     ("__init__.py", "ok[n] = ok[p] and bool(passed[n])", "ok[n] = bool(passed[n])"),  # ignores ancestors
+    ("__init__.py", "if not delta[n] and ambiguous[n] and not blocked[int(parent[n])]]",
+     "if not delta[n] and not blocked[int(parent[n])]]"),                       # certain decisions set free
+    ("__init__.py", "blocked[n] = blocked[p] or certain_fail", "blocked[n] = certain_fail"),  # not inherited
+    ("__init__.py", "free = [i for i in range(limit) if not delta[i] and ambiguous[i]]",
+     "free = [i for i in range(limit) if not delta[i]]"),                       # chain: certain set free
+    ("cospec_oracle.c", "out_lo[r] = before / z;", "out_lo[r] = before;"),     # residual not normalised
+    ("cospec_oracle.c", "out_hi[r] = (before + p[pick]) / z;", "out_hi[r] = (before + p[pick + 1]) / z;"),
+    ("cospec_oracle.c", "before += p[v];\n        out_lo[r]", "before += p[v] + p[pick];\n        out_lo[r]"),
 ]
 
 

@@ -464,6 +464,88 @@ def test_chain_outcome_set_enumerates_ambiguous_decisions():
     assert outs == {(1, (5, -1, -1))}
 
 
+def test_chain_outcome_sets_hand_worked():
+    draft, cand = [1, 2, 3, 4, 5], [10, 11, 12, 13, 14, 15]
+    # decision 4 is a certain rejection, so only the ambiguous decision 1 before it can
+    # matter: accepted, the round runs to the stop at 4; rejected, it stops at 1.  The
+    # ambiguous decision 5 lies after the certain stop and cannot matter.
+    outs = oracle.chain_outcomes([0, 0, 1, 0, 0], [1, 1, 1, 0, 1], [True, False, False, False, True],
+                                 draft, cand)
+    assert outs == {(4, (1, 2, 3, 13, -1, -1)), (1, (10, -1, -1, -1, -1, -1))}
+    # two ambiguous decisions and no certain rejection: (1, 3) both accepted gives the whole
+    # block and the bonus token; 3 rejected stops at 3; 1 rejected stops at 1 whatever 3 does
+    outs = oracle.chain_outcomes([0, 1, 0], [0, 1, 1], [True, False, True], [1, 2, 3], [7, 8, 9, 6])
+    assert outs == {(4, (1, 2, 3, 6)), (3, (1, 2, 9, -1)), (1, (7, -1, -1, -1))}
+    # no ambiguous decision: the one nominal outcome, a certain rejection included
+    outs = oracle.chain_outcomes([0, 0], [1, 0], [False, False], [1, 2], [7, 8, 9])
+    assert outs == {(2, (1, 8, -1))}
+
+
+# A 7-node tree for the hand-worked outcome sets below:
+#     0 -> 1 -> 3 -> 6,   1 -> 4,   0 -> 2 -> 5
+_T_PARENT = [-1, 0, 0, 1, 1, 2, 3]
+_T_TOKENS = [-1, 11, 12, 13, 14, 15, 16]
+_T_CAND = [21, 22, 23, 24, 25, 26, 27]         # the candidate of target row n
+
+
+def _tree_outcome(accept_len, tokens, path, N=7):
+    return (accept_len, tuple(tokens + [-1] * (N - len(tokens))), tuple(path + [-1] * (N - len(path))))
+
+
+def test_tree_outcomes_ambiguous_node_under_a_certain_failure():
+    # node 1 is a certain rejection; the ambiguous node 3 lies below it and cannot
+    # matter.  Reachable: 0, 2, 5 -> the deepest is node 5
+    delta = [1, 0, 1, 0, 1, 1, 1]
+    accept = [1, 0, 1, 1, 1, 1, 1]
+    amb = [False, False, False, True, False, False, False]
+    outs = oracle.tree_outcomes(_T_PARENT, delta, accept, amb, _T_TOKENS, _T_CAND)
+    assert outs == {_tree_outcome(3, [12, 15, 26], [0, 2, 5])}
+
+
+def test_tree_outcomes_ambiguous_node_on_a_live_path():
+    # node 3 is ambiguous with every ancestor passing: accepted, the round reaches node 6
+    # (depth 3); rejected, the deepest reachable nodes are 4 and 5 (depth 2) and the
+    # lower id, 4, wins
+    delta = [1, 1, 1, 0, 1, 1, 1]
+    accept = [1, 1, 1, 1, 1, 1, 1]
+    amb = [False, False, False, True, False, False, False]
+    outs = oracle.tree_outcomes(_T_PARENT, delta, accept, amb, _T_TOKENS, _T_CAND)
+    assert outs == {_tree_outcome(4, [11, 13, 16, 27], [0, 1, 3, 6]),
+                    _tree_outcome(3, [11, 14, 25], [0, 1, 4])}
+
+
+def test_tree_outcomes_ambiguous_siblings_tie_to_the_lower_id():
+    # node 3 is a certain rejection (its child 6 is unreachable); the ambiguous nodes 4 and
+    # 5 share depth 2.  Node 4 accepted: it wins the tie whatever 5 does.  Only 5
+    # accepted: node 5.  Neither: depth 1, nodes 1 and 2 tie and node 1 wins.
+    delta = [1, 1, 1, 0, 0, 0, 1]
+    accept = [1, 1, 1, 0, 1, 0, 1]
+    amb = [False, False, False, False, True, True, False]
+    outs = oracle.tree_outcomes(_T_PARENT, delta, accept, amb, _T_TOKENS, _T_CAND)
+    assert outs == {_tree_outcome(3, [11, 14, 25], [0, 1, 4]),
+                    _tree_outcome(3, [12, 15, 26], [0, 2, 5]),
+                    _tree_outcome(2, [11, 22], [0, 1])}
+
+
+def test_tree_outcomes_count_only_decisions_that_can_matter():
+    # node 1 is a certain rejection with a matched child 2 under it, and the 17 ambiguous
+    # nodes 3..19 hang below node 2; node 20 is a matched child of the root.  None of the
+    # 17 can matter, so the set is the single nominal outcome and the cap of 16 free
+    # decisions is not reached.
+    N = 21
+    parent = [-1, 0, 1] + [2] * 17 + [0]
+    delta = [1, 0, 1] + [0] * 17 + [1]
+    accept = [1, 0, 1] + [1] * 17 + [1]
+    amb = [False, False, False] + [True] * 17 + [False]
+    toks = [-1] + list(range(100, 100 + N - 1))
+    cand = list(range(200, 200 + N))
+    outs = oracle.tree_outcomes(parent, delta, accept, amb, toks, cand)
+    assert outs == {(2, tuple([119, 220] + [-1] * (N - 2)), tuple([0, 20] + [-1] * (N - 2)))}
+    # the same 17 on a live path exceed the cap: the set is not enumerated
+    delta2 = [1, 1] + delta[2:]
+    assert oracle.tree_outcomes(parent, delta2, accept, amb, toks, cand) is None
+
+
 def test_path_tree_verify_equals_chain_verify():
     wl = _small_chain(B=4, K=5, V=1500, noise=0.6)
     t, d, toks, hid, head = _np_chain(wl)
@@ -690,6 +772,37 @@ def test_sps_residual_closed_form():
     # token 0: ratio 0.5 / 0.2 > 1, accepted for every u < 1
     r = oracle.sps_block(target, draft, np.array([[0]]), np.array([[0.999, 0.1]]))
     assert r["accept_len"][0] == 2
+
+
+def test_sps_residual_interval_closed_form():
+    # p_T = (0.4, 0.1, 0.3, 0.2), p_D = (0.1, 0.4, 0.1, 0.4): the residual max(0, p_T - p_D)
+    # = (0.3, 0, 0.2, 0) has Z = 0.5, so its normalised cumulative weights are
+    # 0.6, 0.6, 1, 1 and token v takes the uniforms in [P(v-1), P(v))
+    pT, pD = [0.4, 0.1, 0.3, 0.2], [0.1, 0.4, 0.1, 0.4]
+    t, d = _logits_of(pT)[None], _logits_of(pD)[None]
+    want = {0: (0.0, 0.6), 1: (0.6, 0.6), 2: (0.6, 1.0), 3: (1.0, 1.0)}
+    for q, (lo, hi) in want.items():
+        idx, l, h = oracle.residual_sample(t, d, query=[q])
+        assert idx[0] == q
+        assert l[0] == pytest.approx(lo, abs=1e-6) and h[0] == pytest.approx(hi, abs=1e-6)
+    for u, v in ((0.0, 0), (0.59, 0), (0.61, 2), (0.999, 2)):
+        assert oracle.residual_sample(t, d, [u])[0][0] == v
+    # without a draft row: the cumulative weights of p_T itself
+    want = {0: (0.0, 0.4), 1: (0.4, 0.5), 2: (0.5, 0.8), 3: (0.8, 1.0)}
+    for q, (lo, hi) in want.items():
+        _, l, h = oracle.residual_sample(t, None, query=[q])
+        assert l[0] == pytest.approx(lo, abs=1e-6) and h[0] == pytest.approx(hi, abs=1e-6)
+    # final_token's interval: a round that stops at s <= K resamples the residual of rows
+    # s-1; a full round (s = K+1) draws from target row K.  K = 2 here, with row 1 of the
+    # draft equal to row 1 of the target except for the residual above
+    target = np.stack([_logits_of([0.25] * 4), _logits_of(pT), _logits_of([0.7, 0.1, 0.1, 0.1])])
+    draft = np.stack([_logits_of([0.25] * 4), _logits_of(pD)])
+    assert oracle.final_token(target, draft, 2, 0.0, query=2) == pytest.approx((0.6, 1.0), abs=1e-6)
+    assert oracle.final_token(target, draft, 3, 0.0, query=1) == pytest.approx((0.7, 0.8), abs=1e-6)
+    assert oracle.final_token(target, draft, 3, 0.75) == 1
+    assert oracle.final_token(target, draft, 2, 0.75) == 2
+    with pytest.raises(IndexError):
+        oracle.residual_sample(t, d, query=[4])
 
 
 def test_sps_ambiguous_stops():

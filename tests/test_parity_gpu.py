@@ -4,6 +4,8 @@ Integers (argmax, Delta, accept flags outside the 1e-3 band, accept lengths,
 tokens, paths) must be bit-exact; floating-point features within the stated
 2e-3 * max(1, |ref|) and the tighter bounds of oracle/parity.py.
 """
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -13,6 +15,8 @@ from oracle import parity
 import paper_2605_24793_amd as cs
 from paper_2605_24793_amd import workloads
 from paper_2605_24793_amd.workloads import bf16_bits
+
+import oracle_pool
 
 pytestmark = pytest.mark.gpu
 
@@ -93,38 +97,49 @@ def test_config_full(cfg):
 
 
 def test_config3_full_lambda_sweep():
+    """The peaked serving batch (B=64, K=7, V=151936) at every threshold it names, in the
+    launch sequence bench.py times, every sequence against the oracle."""
     wl = workloads.make_config(3)
     for lam in wl.lambdas:
-        gpu = _gpu_block(wl, lam, overlap=True)
-        stats = parity.check_block(gpu, _ref_block(wl, lam))
-        _report(f"config 3 lambda {lam}", stats, gpu)
+        gpu = _gpu_block(wl, lam)
+        stats = parity.check_block(gpu, oracle_pool.verify_block(wl, lam))
+        _report(f"config 3 lambda {lam} (all {wl.B} sequences)", stats, gpu)
+
+
+def test_config4_full_size():
+    """The large chain batch (B=256, K=7, V=151936, head 5120->512->1) in the launch
+    sequence bench.py times; all 256 sequences against the oracle."""
+    wl = workloads.make_config(4)
+    lam = wl.lambdas[0]
+    gpu = _gpu_block(wl, lam)
+    stats = parity.check_block(gpu, oracle_pool.verify_block(wl, lam))
+    _report(f"config 4 (all {wl.B} sequences)", stats, gpu)
+    _chain_properties(wl, gpu)
+
+
+def test_config5_full_size():
+    """The tree batch (64 trees of 60 nodes, V=151936) in the launch sequence bench.py
+    --config 5 times; all 64 trees against the oracle."""
+    tr = workloads.make_config(5)
+    lam = tr.lambdas[0]
+    gpu = _gpu_tree(tr, lam)
+    stats = parity.check_tree(gpu, oracle_pool.verify_tree(tr, lam))
+    _report(f"config 5 (all {tr.B} trees)", stats, gpu)
+    _tree_properties(tr, gpu)
+
+
+def test_overlap_stream_matches_oracle_on_the_peaked_batch():
+    """The optional second-stream launch sequence, on the peaked serving batch at one
+    threshold: every sequence against the oracle."""
+    wl = workloads.make_config(3)
+    gpu = _gpu_block(wl, 0.5, overlap=True)
+    stats = parity.check_block(gpu, oracle_pool.verify_block(wl, 0.5))
+    _report("config 3 lambda 0.5, overlap stream", stats, gpu)
 
 
 def _sample(B, n, seed):
     rng = np.random.default_rng(seed)
     return sorted(rng.choice(B, size=min(n, B), replace=False).tolist())
-
-
-def test_config4_full_size_sampled():
-    wl = workloads.make_config(4)
-    lam = wl.lambdas[0]
-    gpu = _gpu_block(wl, lam, overlap=True)
-    seqs = _sample(wl.B, 32, 40)
-    sub = {k: v[seqs] for k, v in gpu.items()}
-    stats = parity.check_block(sub, _ref_block(wl.take(seqs), lam))
-    _report("config 4 (32 sampled sequences of 256)", stats, sub)
-    _chain_properties(wl, gpu)
-
-
-def test_config5_full_size_sampled():
-    tr = workloads.make_config(5)
-    lam = tr.lambdas[0]
-    gpu = _gpu_tree(tr, lam, overlap=True)
-    seqs = _sample(tr.B, 12, 50)
-    sub = {k: v[seqs] for k, v in gpu.items()}
-    stats = parity.check_tree(sub, _ref_tree(tr.take(seqs), lam))
-    _report("config 5 (12 sampled trees of 64)", stats, sub)
-    _tree_properties(tr, gpu)
 
 
 def _chain_properties(wl, gpu):
@@ -481,30 +496,24 @@ def test_t1_configs_full(cfg):
     assert (gpu["tgt_candidate"] != gpu["tgt_argmax"]).any()
 
 
-def test_t1_config4_full_size_sampled():
+def test_t1_config4_full_size():
     wl = workloads.make_config(4)
     u = _uniforms((wl.B, wl.K + 1), 104)
     gpu = _gpu_block(wl, wl.lambdas[0], u=u)
-    seqs = _sample(wl.B, 16, 41)
-    sub = {k: v[seqs] for k, v in gpu.items()}
-    ws = wl.take(seqs)
     stats = {}
-    cand = parity.check_candidates(sub["tgt_candidate"], _conv(ws.target), u[seqs].double().numpy(), stats)
-    stats.update(parity.check_block(sub, _ref_block(ws, wl.lambdas[0], u[seqs], cand)))
-    _report("T=1 config 4 (16 sampled sequences of 256)", stats, sub)
+    cand = oracle_pool.check_candidates(parity, gpu["tgt_candidate"], wl, u, stats)
+    stats.update(parity.check_block(gpu, oracle_pool.verify_block(wl, wl.lambdas[0], u=u, cand=cand)))
+    _report(f"T=1 config 4 (all {wl.B} sequences)", stats, gpu)
 
 
-def test_t1_config5_full_size_sampled():
+def test_t1_config5_full_size():
     tr = workloads.make_config(5)
     u = _uniforms((tr.B, tr.N), 105)
     gpu = _gpu_tree(tr, tr.lambdas[0], u=u)
-    seqs = _sample(tr.B, 6, 51)
-    sub = {k: v[seqs] for k, v in gpu.items()}
-    ts = tr.take(seqs)
     stats = {}
-    cand = parity.check_candidates(sub["tgt_candidate"], _conv(ts.target), u[seqs].double().numpy(), stats)
-    stats.update(parity.check_tree(sub, _ref_tree(ts, tr.lambdas[0], u[seqs], cand)))
-    _report("T=1 config 5 (6 sampled trees of 64)", stats, sub)
+    cand = oracle_pool.check_candidates(parity, gpu["tgt_candidate"], tr, u, stats)
+    stats.update(parity.check_tree(gpu, oracle_pool.verify_tree(tr, tr.lambdas[0], u=u, cand=cand)))
+    _report(f"T=1 config 5 (all {tr.B} trees)", stats, gpu)
 
 
 T1_FUZZ = [
@@ -749,19 +758,25 @@ def test_sps_configs(cfg):
     _report(f"SpS config {cfg}", stats, gpu)
 
 
-def test_sps_config4_full_size_sampled():
+def test_sps_config4_full_size():
     # the launch configuration bench.py --sps times (256 sequences, automatic splits),
-    # checked on a sample of the sequences
+    # every sequence checked, a chunk of sequences per oracle task
     wl = workloads.make_config(4)
     u = _uniforms((wl.B, wl.K + 1), 404)
     gpu = cs.sps_block(wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV), u.to(DEV))
     torch.cuda.synchronize()
-    seqs = _sample(wl.B, 16, 41)
-    sub = wl.take(seqs)
-    gsub = {k: v.cpu()[seqs] for k, v in gpu.items()}
-    t, d, us = _conv(sub.target), _conv(sub.draft), u[seqs].double().numpy()
-    ref = oracle.sps_block(t, d, sub.draft_tokens.numpy(), us)
-    _report("SpS config 4 (16 sampled sequences of 256)", parity.check_sps(gsub, ref, t, d, us), gsub)
+    gpu = {k: v.cpu() for k, v in gpu.items()}
+
+    def one(seqs):
+        sub = wl.take(seqs)
+        gsub = {k: v[seqs] for k, v in gpu.items()}
+        t, d, us = _conv(sub.target), _conv(sub.draft), u[seqs].double().numpy()
+        return parity.check_sps(gsub, oracle.sps_block(t, d, sub.draft_tokens.numpy(), us), t, d, us)
+    chunks = [list(range(s, min(wl.B, s + 8))) for s in range(0, wl.B, 8)]
+    with ThreadPoolExecutor(max_workers=oracle_pool.threads()) as pool:
+        parts = list(pool.map(one, chunks))
+    stats = {k: max(p.get(k, 0.0) for p in parts) for k in parts[0] if isinstance(parts[0][k], float)}
+    _report(f"SpS config 4 (all {wl.B} sequences)", stats, gpu)
 
 
 @pytest.mark.parametrize("B,K,V,dtype,pad,splits", [(3, 1, 7, "f32", 1, 0), (4, 4, 9, "bf16", 0, 2),
