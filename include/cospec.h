@@ -30,7 +30,8 @@
  *    *_workspace_size function).  Its contents need no initialisation and are
  *    garbage afterwards.  Calls that may overlap in time need distinct workspaces.
  *  - Host structs are read during the call and not retained.  There is no global
- *    mutable state, so the library is reentrant.
+ *    mutable state (apart from the static scratch buffer of
+ *    cospec_verify_block_static), so the library is reentrant.
  *  - Every argument that lives on the host is checked before anything is
  *    enqueued; an invalid call returns a negative status and enqueues nothing.
  *    Launch failures return COSPEC_ERR_HIP.  No C++ exception crosses the ABI.
@@ -64,8 +65,13 @@ typedef enum {
     COSPEC_ERR_UNSUPPORTED = -2,  /* K, N or split count above the documented maximum,
                                      or a logit row (V * element bytes) over 2^31 - 1 B */
     COSPEC_ERR_WORKSPACE = -3,    /* workspace missing, misaligned or too small         */
-    COSPEC_ERR_HIP = -4           /* a HIP call or kernel launch failed                 */
+    COSPEC_ERR_HIP = -4,          /* a HIP call or kernel launch failed                 */
+    COSPEC_ERR_SCRATCH_LIMIT = -5 /* cospec_verify_block_static: the sizes need more than
+                                     COSPEC_STATIC_SCRATCH_BYTES of scratch             */
 } cospec_status;
+
+/* Bytes of the library's static scratch buffer (per GPU), see cospec_verify_block_static. */
+#define COSPEC_STATIC_SCRATCH_BYTES (64u << 20)
 
 typedef enum { COSPEC_F32 = 0, COSPEC_BF16 = 1 } cospec_dtype;
 
@@ -260,6 +266,31 @@ cospec_status cospec_verify_block(const void *target_logits, const void *draft_l
                                   int32_t V, int32_t *accept_len, int32_t *out_tokens,
                                   const cospec_features *feats, const cospec_options *opts,
                                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * cospec_verify_block without a workspace argument, for callers that cannot allocate
+ * device memory (code being captured into a HIP graph, tight serving loops, harnesses
+ * that forbid allocation): the step's scratch memory is a static buffer of
+ * COSPEC_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on, from
+ * when its code object loads until the process ends.  Arguments, results and errors
+ * are those of cospec_verify_block, plus:
+ *  - COSPEC_ERR_SCRATCH_LIMIT when cospec_verify_block_workspace_size(B, K, V, head)
+ *    exceeds COSPEC_STATIC_SCRATCH_BYTES (checked before anything is enqueued);
+ *  - COSPEC_ERR_HIP when the buffer's device address cannot be obtained (the first
+ *    call on a device looks it up with that device current and keeps it).
+ * The call allocates nothing: no hipMalloc, no hipFree, no allocating library routine.
+ * Every call on one GPU shares that GPU's buffer, so calls that may overlap in time on
+ * one GPU (on different streams, or from different threads) race and must be
+ * serialised by the caller; calls in one stream are ordered and safe.  The buffer
+ * keeps the last call's contents; the step clears what it needs cleared itself.
+ */
+cospec_status cospec_verify_block_static(const void *target_logits, const void *draft_logits,
+                                         cospec_dtype logit_dtype, int64_t ld,
+                                         const int32_t *draft_tokens, const void *hidden,
+                                         const cospec_head *head, float lambda, int32_t B, int32_t K,
+                                         int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                         const cospec_features *feats, const cospec_options *opts,
+                                         hipStream_t stream);
 
 /*
  * The same chain step in two phases, for an arbitrator whose input needs the

@@ -15,7 +15,7 @@ import torch
 
 from . import _build
 
-__all__ = ["lib", "verify_block", "verify_tree", "arbitrate", "CospecError", "Prepared",
+__all__ = ["lib", "verify_block", "verify_block_static", "verify_tree", "arbitrate", "CospecError", "Prepared",
            "prepare_block", "prepare_tree", "prepare_sps", "SplitBlock", "sps_block", "hybrid_mask",
            "hybrid_attention", "status_string", "MAX_K",
            "MAX_N", "MAX_SPLITS"]
@@ -106,6 +106,9 @@ def lib():
         L.cospec_verify_tree.argtypes = [P, P, I32, I64, P, P, P, HP, ctypes.c_float, I32, I32,
                                          I32, P, P, P, ctypes.POINTER(_Features),
                                          ctypes.POINTER(_Options), P, SZ, P]
+        L.cospec_verify_block_static.restype = I32
+        L.cospec_verify_block_static.argtypes = [P, P, I32, I64, P, P, HP, ctypes.c_float, I32, I32, I32,
+                                                 P, P, ctypes.POINTER(_Features), ctypes.POINTER(_Options), P]
         L.cospec_verify_block_reduce.restype = I32
         L.cospec_verify_block_reduce.argtypes = [P, P, I32, I64, P, HP, I32, I32, I32, P,
                                                  ctypes.POINTER(_Features), ctypes.POINTER(_Options),
@@ -360,6 +363,37 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features
                       sample_u, policy_u, correct, alpha, beta)
     p.launch()
     return p.result()
+
+
+def verify_block_static(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
+                        splits: int = 0, sample_u: Optional[torch.Tensor] = None) -> dict:
+    """cospec_verify_block_static: the chain step on the library's static scratch buffer
+    (no workspace is allocated here or in the library).  Same results as verify_block."""
+    B, R, V = target.shape
+    K = R - 1
+    ld = _row_stride(target)
+    if K > 0 and (_row_stride(draft) != ld or tuple(draft.shape) != (B, K, V)
+                  or tuple(draft_tokens.shape) != (B, K) or draft_tokens.dtype != torch.int32
+                  or not draft_tokens.is_contiguous() or hidden.shape[:2] != (B, K)
+                  or not hidden.is_contiguous()):
+        raise ValueError("shape/dtype mismatch between target, draft, draft_tokens and hidden")
+    dev = target.device
+    hs = _head_struct(head)
+    outputs = dict(accept_len=torch.empty(B, dtype=torch.int32, device=dev),
+                   tokens=torch.empty((B, K + 1), dtype=torch.int32, device=dev))
+    feats, fst = _features(features, dev, B, K + 1, K, K)
+    u = _uniforms(sample_u, B, K + 1)
+    opts = _Options(splits=int(splits), sample_uniform=_ptr(u)) if (splits or u is not None) else None
+    code = lib().cospec_verify_block_static(
+        _ptr(target), _ptr(draft) if K > 0 else None, _dtype_code(target), ld,
+        _ptr(draft_tokens) if K > 0 else None, _ptr(hidden) if K > 0 else None, ctypes.byref(hs), float(lam),
+        B, K, V, _ptr(outputs["accept_len"]), _ptr(outputs["tokens"]),
+        ctypes.byref(fst) if fst is not None else None, ctypes.byref(opts) if opts is not None else None,
+        _stream())
+    _check(code, "cospec_verify_block_static")
+    out = dict(outputs)
+    out.update(feats or {})
+    return out
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,

@@ -24,8 +24,18 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/cospec.h"
 #include "launch.h"
+
+// Scratch memory of cospec_verify_block_static: a file-scope device array, so that
+// entry point needs no workspace from its caller and allocates nothing.  Each GPU the
+// library runs on holds its own copy, from when the code object is loaded until the
+// process ends.  In host code `scratch` names a host-side stand-in, not the device
+// address: host code only ever uses the address hipGetSymbolAddress returns for the
+// current device (static_scratch() below).
+static __device__ __align__(256) char scratch[COSPEC_STATIC_SCRATCH_BYTES];
 
 using namespace cospec;
 
@@ -420,6 +430,24 @@ cospec_status check_logits(const void *p, cospec_dtype dt, int64_t ld, int32_t V
     return COSPEC_OK;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];   // device address of `scratch` per device, once looked up
+
+// The address of the current device's copy of `scratch`, looked up on the first call on
+// that device (with it current) and kept; null if the lookup fails.
+void *static_scratch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch[dev] = p;
+    }
+    return g_scratch[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -438,6 +466,7 @@ const char *cospec_status_string(int32_t status) {
         case COSPEC_ERR_UNSUPPORTED: return "unsupported size";
         case COSPEC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
         case COSPEC_ERR_HIP: return "HIP error";
+        case COSPEC_ERR_SCRATCH_LIMIT: return "sizes need more scratch than the library's static buffer holds";
         default: return "unknown status";
     }
 }
@@ -500,6 +529,29 @@ cospec_status cospec_verify_block(const void *target_logits, const void *draft_l
     if (st != COSPEC_OK || B == 0) return st;
     if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4))
         return COSPEC_ERR_INVALID_ARG;
+    return run(c, kWhole, accept_len, out_tokens, nullptr);
+}
+
+cospec_status cospec_verify_block_static(const void *target_logits, const void *draft_logits,
+                                         cospec_dtype logit_dtype, int64_t ld, const int32_t *draft_tokens,
+                                         const void *hidden, const cospec_head *head, float lambda, int32_t B,
+                                         int32_t K, int32_t V, int32_t *accept_len, int32_t *out_tokens,
+                                         const cospec_features *feats, const cospec_options *opts,
+                                         hipStream_t stream) {
+    Common c{};
+    cospec_status st = block_common(target_logits, draft_logits, logit_dtype, ld, draft_tokens, hidden, true,
+                                    head, lambda, B, K, V, feats, opts, nullptr, 0, stream, c);
+    if (st != COSPEC_OK || B == 0) return st;
+    if (!accept_len || !aligned(accept_len, 4) || !out_tokens || !aligned(out_tokens, 4))
+        return COSPEC_ERR_INVALID_ARG;
+    const size_t need = cospec_verify_block_workspace_size(B, K, V, head);
+    if (need == 0 || need > COSPEC_STATIC_SCRATCH_BYTES) return COSPEC_ERR_SCRATCH_LIMIT;
+    // the step's scratch memory needs no clearing: the one counter that must start at
+    // zero (the mismatch-list length) is zeroed by the first reduction workgroup
+    void *ws = static_scratch();
+    if (!ws) return COSPEC_ERR_HIP;
+    c.ws = ws;
+    c.ws_bytes = COSPEC_STATIC_SCRATCH_BYTES;
     return run(c, kWhole, accept_len, out_tokens, nullptr);
 }
 

@@ -261,3 +261,20 @@ def test_arbitrate_rejects_before_launch():
     assert call(ws=None) == WORKSPACE
     assert call(wsb=8) == WORKSPACE
     assert call(n_sel=0) == OK
+
+
+def test_static_scratch_entry_point_rejects_before_any_launch():
+    L = cs.lib()
+    hd = _head(d=5120, h=512)
+    args = [FAKE, FAKE, 1, 151936, FAKE, FAKE, ctypes.byref(hd), 0.5]
+
+    def call(B, K, V, **kw):
+        a = list(args)
+        a[3] = V
+        return L.cospec_verify_block_static(*a, B, K, V, FAKE, FAKE, None, kw.get("opts"), None)
+    assert L.cospec_verify_block_workspace_size(4096, 64, 151936, ctypes.byref(hd)) > (64 << 20)
+    assert call(4096, 64, 151936) == -5                   # needs more than the static buffer
+    assert call(4, 65, 151936) == UNSUPPORTED             # K above the maximum
+    assert call(-1, 7, 151936) == INVALID
+    assert call(0, 7, 151936) == OK                       # empty batch: nothing to do
+    assert "static buffer" in binding.status_string(-5)
