@@ -130,9 +130,6 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (default 4)")
     ap.add_argument("--splits", type=int, default=0, help="workgroups per row (0 = automatic)")
-    ap.add_argument("--overlap", action="store_true",
-                    help="run the head on a second stream, overlapping the draft-row reduction "
-                         "(slower on the large chain batch: the reduction fills every CU)")
     ap.add_argument("--sample", action="store_true",
                     help="temperature-1 target candidates (inversion of seeded uniforms) instead "
                          "of the greedy argmax")
@@ -236,7 +233,7 @@ class Step:
         if self.tree:
             par, tok = wl.parent.to(dev), wl.node_tokens.to(dev)
             self.p = cs.prepare_tree(tgt, drf, par, tok, hid, head, lam, features=True, splits=args.splits,
-                                     overlap=args.overlap, sample_u=u_dev)
+                                     sample_u=u_dev)
             self.rows = wl.B * wl.N
             internal = np.zeros((wl.B, wl.N), bool)
             pn = wl.parent.numpy()
@@ -250,12 +247,12 @@ class Step:
                 self.p = cs.prepare_sps(tgt, drf, tok, sps_u.to(dev), features=True, splits=args.splits)
             else:
                 self.p = cs.prepare_block(tgt, drf, tok, hid, head, lam, features=True, splits=args.splits,
-                                          overlap=args.overlap, sample_u=u_dev)
+                                          sample_u=u_dev)
             self.rows = wl.B * (wl.K + 1)
             self.reduced_rows = wl.B * (2 * wl.K + 1)
         self.elem = tgt.element_size()
+        self.kernel = "k_vocab_reduce"
         self.logit_bytes = self.reduced_rows * wl.V * self.elem   # algorithmic bytes of the reductions
-        self.launches = 2 if args.overlap else 1                  # the draft rows get their own launch
         self.step = self.p.launch
 
     def warmup(self, n):
@@ -290,11 +287,11 @@ class Step:
                 flush()
             self.p.launch(timing=ev[i])
         torch.cuda.synchronize()
-        k_raw = float(np.mean([e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev])) / self.launches
-        # Without the overlap stream the library records the second pair back to back with
-        # no launch between them, so that pair measures what an event interval adds on its
-        # own (barrier packets, timestamps); it is taken off the kernel's interval.
-        overhead = 0.0 if self.launches == 2 else float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+        k_raw = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        # The library records the second pair back to back with no launch between them, so
+        # that pair measures what an event interval adds on its own (barrier packets,
+        # timestamps); it is taken off the kernel's interval.
+        overhead = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
         return k_raw - overhead, k_raw, overhead
 
 
@@ -382,11 +379,11 @@ def extra_workload(cs, workloads, torch, np, bf16_bits, cfg, dev, args, nthreads
         out = {k: v.cpu() for k, v in p.p.result().items()}
         n, _ = oracle_parity(torch, np, bf16_bits, wl, out, lam_i, tree, nthreads=nthreads)
         checked += n
-    launch_bytes = st.logit_bytes / st.launches
+    launch_bytes = st.logit_bytes
     gbps = launch_bytes / (k_avg * 1e-3) / 1e9
     return {"workload": wl.name, "lambda": lam, "ms_per_step": ms, "rows_per_s": st.rows / (ms * 1e-3),
             "step_ms_cache_flushed": cold,
-            "reduction_cache_flushed": {"kernel": "k_vocab_reduce", "kernel_ms": k_avg,
+            "reduction_cache_flushed": {"kernel": st.kernel, "kernel_ms": k_avg,
                                         "event_interval_ms": k_raw, "achieved_gbps": gbps,
                                         "frac": gbps / HBM_PEAK_GBPS,
                                         "algorithmic_bytes_per_launch": launch_bytes},
@@ -425,9 +422,6 @@ def main():
             print(json.dumps({"error": "--sps runs on chain workloads"}))
             sys.exit(2)
         sps_u = torch.rand((wl.B, wl.K + 1), generator=torch.Generator().manual_seed(2025))
-    if args.graph and args.overlap:
-        print(json.dumps({"error": "--graph does not capture the aux stream"}))
-        sys.exit(2)
     st = Step(cs, workloads, torch, np, wl, dev, lam, args, u_host=u_host, sps_u=sps_u)
     torch.cuda.synchronize()
 
@@ -466,14 +460,14 @@ def main():
     ms_per_step, wall = st.timed(args.steps)
     hinfo.update(gpu_state("right_after_timing", torch))
     value = st.rows / (ms_per_step * 1e-3)
-    launch_bytes = st.logit_bytes / st.launches
+    launch_bytes = st.logit_bytes
     achieved = launch_bytes / (k_avg * 1e-3) / 1e9
     out = {k: v.cpu() for k, v in st.p.result().items()}
 
     nth = oracle_threads()
     extras = {}
-    default_mode = (args.config == 4 and not (args.sample or args.sps or args.overlap or args.graph
-                                              or args.splits) and not args.no_extras)
+    default_mode = (args.config == 4 and not (args.sample or args.sps or args.graph or args.splits)
+                    and not args.no_extras)
     if default_mode:
         for key, cfg in (("peaked_chain", 3), ("tree", 5)):
             print(f"[bench] workload {cfg}: timing, flushed reduction events, parity of every sequence",
@@ -519,7 +513,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, ("N" if tree else "K"): (wl.N if tree else wl.K),
                    "V": wl.V, "d": wl.head.d, "h": wl.head.h, "lambda": lam,
-                   "splits": args.splits or "auto", "head_overlap": args.overlap,
+                   "splits": args.splits or "auto",
                    "hip_graph": args.graph,
                    "temperature": 1 if args.sample or args.sps else 0,
                    "rule": "speculative sampling" if args.sps else "cospec",
@@ -532,9 +526,9 @@ def main():
                      "traffic": (measured_traffic("paper_2605_24793_amd/csrc/reduce.hip")
                                  if args.config == 4 and not args.splits and not args.sample
                                  and not args.sps else None),
-                     "kernel": "k_vocab_reduce", "kernel_ms": k_avg,
+                     "kernel": st.kernel, "kernel_ms": k_avg,
                      "event_interval_ms": k_raw, "empty_event_interval_ms": ev_overhead,
-                     "launches_per_step": st.launches, "algorithmic_bytes_per_launch": launch_bytes},
+                     "launches_per_step": 1, "algorithmic_bytes_per_launch": launch_bytes},
         "step_hbm_gbps": st.logit_bytes / (ms_per_step * 1e-3) / 1e9,
         "wall_s": wall,
         "mean_accept_len": float(out["accept_len"].float().mean()),

@@ -159,24 +159,16 @@ typedef struct {
  * Order of work inside a verify call: (1) reduce the logit rows, (2) decide
  * (verification tokens, Delta, mismatch list), (3) the head on the mismatch
  * rows, (4) finish (draft statistics, log p_D, verdicts, first stop, emission).
- * The draft rows only feed features, so the decision needs the target rows
- * alone.  When `aux_stream` is given, step 1 reduces only the target rows and
- * the draft rows are reduced on `stream` while step 3 runs on `aux_stream`;
- * `aux_ready` and `aux_done` must then be events created
- * by the caller on the same device (timing may be disabled); the library
- * records and waits on them and creates nothing itself.  The call still
- * completes in `stream` order: work enqueued on `stream` afterwards sees every
- * output.  Two calls that overlap in time must not share these events.
  */
 typedef struct {
     hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ...        */
-    hipEvent_t reduce_end;    /* ... and just after the first reduction launch            */
-    hipEvent_t reduce2_begin; /* if non-NULL, recorded on `stream` just before ...        */
-    hipEvent_t reduce2_end;   /* ... and after the draft-row launch (back to back if none) */
-    int32_t splits;           /* workgroups per logit row, 1..COSPEC_MAX_SPLITS; 0 = auto */
-    hipStream_t aux_stream;   /* second stream for the head, or NULL (all on `stream`)  */
-    hipEvent_t aux_ready;     /* required with aux_stream                               */
-    hipEvent_t aux_done;      /* required with aux_stream                               */
+    hipEvent_t reduce_end;    /* ... and just after the reduction launch                  */
+    hipEvent_t reduce2_begin; /* if non-NULL, recorded on `stream` right after reduce_end, */
+    hipEvent_t reduce2_end;   /* and this one right after it: an empty interval that
+                                 measures what an event pair adds by itself              */
+    int32_t splits;           /* workgroups per logit row, 1..COSPEC_MAX_SPLITS; 0 = auto
+                                 (one per row for large batches, more for small ones so
+                                 that every CU stays busy)                                */
     /*
      * Temperature-1 target candidates.  NULL: the candidate of every target row
      * is its argmax (greedy decoding).  Otherwise a device array with one
@@ -312,7 +304,7 @@ cospec_status cospec_verify_block_static(const void *target_logits, const void *
  * workspace must not be touched between them and phase 2 must be enqueued on a
  * stream ordered after phase 1.  Of the options, phase 1 reads splits (which
  * phase 2 must repeat) and sample_uniform; phase 2 reads policy_uniform, rl and
- * the hidden-row map; aux_stream is not supported.  The two phases together
+ * the hidden-row map.  The two phases together
  * give exactly the results of one cospec_verify_block call.
  */
 cospec_status cospec_verify_block_reduce(const void *target_logits, const void *draft_logits,

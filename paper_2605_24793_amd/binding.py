@@ -55,8 +55,7 @@ class _RL(ctypes.Structure):
 class _Options(ctypes.Structure):
     _fields_ = [("reduce_begin", ctypes.c_void_p), ("reduce_end", ctypes.c_void_p),
                 ("reduce2_begin", ctypes.c_void_p), ("reduce2_end", ctypes.c_void_p),
-                ("splits", ctypes.c_int32), ("aux_stream", ctypes.c_void_p),
-                ("aux_ready", ctypes.c_void_p), ("aux_done", ctypes.c_void_p),
+                ("splits", ctypes.c_int32),
                 ("sample_uniform", ctypes.c_void_p), ("policy_uniform", ctypes.c_void_p),
                 ("rl", ctypes.POINTER(_RL)), ("hidden_row0", ctypes.c_void_p),
                 ("hidden_rows", ctypes.c_int64)]
@@ -177,11 +176,11 @@ def _stream() -> int:
 
 class Prepared:
     """Pre-marshalled arguments of one verify call: outputs, features, workspace and
-    (with overlap) the auxiliary stream and its two events are allocated once, so
+    are allocated once, so
     `launch()` enqueues the step with no allocation."""
 
     def __init__(self, fn, args_before_feats, outputs, feats, feats_struct, workspace, splits,
-                 overlap, uniform=None, policy_u=None, rl=None):
+                 uniform=None, policy_u=None, rl=None):
         self._fn = fn
         self._args = args_before_feats
         self.outputs = outputs
@@ -192,21 +191,15 @@ class Prepared:
         self.uniform = uniform
         self.policy_u = policy_u
         self.rl = rl                    # (struct, output tensors, correct tensor) or None
-        self.aux = None
-        if overlap:
-            dev = workspace.device
-            self.aux = (torch.cuda.Stream(device=dev), torch.cuda.Event(), torch.cuda.Event())
         self._keep = []
 
     def _options(self, timing):
-        if (timing is None and not self.splits and self.aux is None and self.uniform is None
+        if (timing is None and not self.splits and self.uniform is None
                 and self.policy_u is None and self.rl is None):
             return None
         ev = [None] * 4 if timing is None else [None if e is None else _event_handle(e) for e in timing]
-        aux = (None, None, None) if self.aux is None else (
-            self.aux[0].cuda_stream, _event_handle(self.aux[1]), _event_handle(self.aux[2]))
         rl = None if self.rl is None else ctypes.pointer(self.rl[0])
-        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, *aux, _ptr(self.uniform),
+        return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, _ptr(self.uniform),
                         _ptr(self.policy_u), rl)
 
     def launch(self, timing=None):
@@ -276,7 +269,7 @@ def _rl(correct: Optional[torch.Tensor], alpha: float, beta: float, B: int, K: i
 
 
 def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                  splits: int = 0, overlap: bool = False,
+                  splits: int = 0,
                   sample_u: Optional[torch.Tensor] = None,
                   policy_u: Optional[torch.Tensor] = None,
                   correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
@@ -309,7 +302,7 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
             _ptr(draft_tokens) if K > 0 else None, _ptr(hidden) if K > 0 else None,
             ctypes.byref(hs), float(lam), B, K, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]))
-    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits, overlap,
+    p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits,
                  _uniforms(sample_u, B, K + 1), _policy_uniforms(policy_u, B, K),
                  _rl(correct, alpha, beta, B, K, dev))
     p._keep = [hs, target, draft, draft_tokens, hidden, head]
@@ -317,7 +310,7 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
 
 
 def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                 features: bool = True, splits: int = 0, overlap: bool = False,
+                 features: bool = True, splits: int = 0,
                  sample_u: Optional[torch.Tensor] = None,
                  policy_u: Optional[torch.Tensor] = None) -> Prepared:
     """sample_u: one uniform per target row [B, N] for temperature-1 candidates;
@@ -345,21 +338,21 @@ def prepare_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
     args = (_ptr(target), _ptr(draft), _dtype_code(target), ld, _ptr(parent), _ptr(node_tokens),
             _ptr(hidden), ctypes.byref(hs), float(lam), B, N, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]), _ptr(outputs["path"]))
-    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits, overlap,
+    p = Prepared(L.cospec_verify_tree, args, outputs, feats, fst, workspace, splits,
                  _uniforms(sample_u, B, N), _policy_uniforms(policy_u, B, N))
     p._keep = [hs, target, draft, parent, node_tokens, hidden, head]
     return p
 
 
 def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features: bool = True,
-                 splits: int = 0, overlap: bool = False,
+                 splits: int = 0,
                  sample_u: Optional[torch.Tensor] = None,
                  policy_u: Optional[torch.Tensor] = None,
                  correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
                  beta: float = 0.25) -> dict:
     """cospec_verify_block on device tensors; returns accept_len, tokens (+ features,
     + rl_* statistics when `correct` is given)."""
-    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits, overlap,
+    p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits,
                       sample_u, policy_u, correct, alpha, beta)
     p.launch()
     return p.result()
@@ -397,12 +390,12 @@ def verify_block_static(target, draft, draft_tokens, hidden, head, lam: float, f
 
 
 def verify_tree(target, draft, parent, node_tokens, hidden, head, lam: float,
-                features: bool = True, splits: int = 0, overlap: bool = False,
+                features: bool = True, splits: int = 0,
                 sample_u: Optional[torch.Tensor] = None,
                 policy_u: Optional[torch.Tensor] = None) -> dict:
     """cospec_verify_tree on device tensors; returns accept_len, tokens, path (+ features)."""
     p = prepare_tree(target, draft, parent, node_tokens, hidden, head, lam, features, splits,
-                     overlap, sample_u, policy_u)
+                     sample_u, policy_u)
     p.launch()
     return p.result()
 
@@ -535,7 +528,7 @@ def prepare_sps(target, draft, draft_tokens, uniforms, features: bool = True,
     args = (_ptr(target), _ptr(draft) if K > 0 else None, _dtype_code(target), ld,
             _ptr(draft_tokens) if K > 0 else None, _ptr(u), B, K, V, _ptr(outputs["accept_len"]),
             _ptr(outputs["tokens"]))
-    p = Prepared(L.cospec_verify_block_sps, args, outputs, feats, fst, ws, splits, False)
+    p = Prepared(L.cospec_verify_block_sps, args, outputs, feats, fst, ws, splits)
     p._keep = [target, draft, draft_tokens, u, unwritten]
     return p
 

@@ -2,32 +2,30 @@
 // carving and the launch sequence.  Declared in include/cospec.h.
 //
 // verify_block / verify_tree enqueue, on the caller's stream:
-//   1. k_vocab_reduce   the target and draft rows (only the target rows when the
-//                       decision work overlaps step 4 on the aux stream), split
-//                       over `splits` workgroups per row -> partial (max, argmax,
-//                       S, T); zeroes the list counter
+//   1. k_vocab_reduce   every target and draft row (tree: draft rows of nodes with
+//                       a child), one workgroup per (row, split) -> split partials
+//                       (max, argmax, S, T); zeroes the list counter
 //   1b. k_sample        temperature 1 only: one wave per target row samples the
 //                       candidate by inversion of its uniform (segment masses
 //                       written by step 1, then one segment re-read)
 //   2. k_decide         one workgroup per sequence: target statistics, Delta,
 //                       log p_T, mismatch compaction (device-side count M)
-//   3. k_head_gemm + k_head_epilogue   MFMA head over the M compacted rows
-//                       (on the aux stream when given; skipped when the
-//                       threshold decides every mismatch by itself and no
-//                       score is requested)
-//   4. k_vocab_reduce   with the aux stream only: the draft rows (tree: nodes with
-//                       a child)
-//   5. k_chain_finish / k_tree_finish   draft statistics, log p_D, verdicts
-//                       (threshold or sampled), first stop, emission, and for
-//                       chains the optional per-round RL statistics
+//   3. k_head_gemm (+ k_head_epilogue for trees)   MFMA head over the M compacted
+//                       rows (skipped when the threshold decides every mismatch by
+//                       itself and no score is requested)
+//   4. k_chain_finish(_head) / k_tree_finish   draft statistics, log p_D, the head's
+//                       second layer (chains), verdicts (threshold or sampled), first
+//                       stop, emission, and for chains the optional per-round RL
+//                       statistics
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
 
 #include <mutex>
 
-#include "../../include/cospec.h"
+#include "cospec.h"
 #include "launch.h"
+
 
 // Scratch memory of cospec_verify_block_static: a file-scope device array, so that
 // entry point needs no workspace from its caller and allocates nothing.  Each GPU the
@@ -43,8 +41,6 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
-constexpr int64_t kAutoBlocks = 2048;         // aim: 8 workgroups per CU on 256 CUs
-constexpr int kOverlapBlocksPerCU = 3;        // draft-row reduction beside the aux stream
 constexpr int64_t kMaxRowBytes = INT32_MAX;    // V * element bytes of one logit row
 
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -96,9 +92,15 @@ inline int64_t n_segments_any(int32_t V) {
     return a > b ? a : b;
 }
 
+// rows = all logit rows; B*RT target rows; B*D decision slots (the sizes depend on
+// these three counts alone, which cospec_workspace_bytes relies on).  The partial slots
+// hold what the automatic split rule can ask for (rows * splits <= 4 * slots + rows / 2
+// when it splits at all, slots <= kMaxReduceSlots) and, on small batches, a split
+// override.
 Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head *hd, int32_t V) {
     Layout L{};
-    L.partial_slots = rows > kMinPartialSlots ? rows : kMinPartialSlots;
+    const int64_t auto_slots = rows + 4 * static_cast<int64_t>(kMaxReduceSlots);
+    L.partial_slots = auto_slots > kMinPartialSlots ? auto_slots : kMinPartialSlots;
     size_t off = 0;
     L.partials = off; off += round_up(static_cast<size_t>(L.partial_slots) * 16);
     L.seg = off;      off += round_up(static_cast<size_t>(B * RT) * static_cast<size_t>(n_segments_any(V)) * 8);
@@ -116,15 +118,6 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     return L;
 }
 
-// The draft-row reduction beside the aux stream's kernels (decide, head GEMM): a grid of
-// kOverlapBlocksPerCU workgroups per CU, so that each SIMD keeps three reduction waves
-// (measured: the same bandwidth as a full grid) and has wave slots, registers and LDS
-// left for a head GEMM workgroup.  The split count, among those whose partials fit,
-// minimises the longest workgroup's work: rounds over the grid times vectors per unit.
-struct DraftPlan {
-    int32_t splits, blocks;
-};
-
 // Compute units of the current device (MI355X: 256).
 int32_t cu_count() {
     int dev = 0, cus = 0;
@@ -134,30 +127,34 @@ int32_t cu_count() {
     return cus;
 }
 
-DraftPlan draft_plan(int64_t rows, int64_t nvec, int64_t free_slots) {
-    const int64_t cap = static_cast<int64_t>(kOverlapBlocksPerCU) * cu_count();
-    DraftPlan best{1, static_cast<int32_t>(rows < cap ? rows : cap)};
-    int64_t best_cost = INT64_MAX;
-    for (int64_t sp = 1; sp <= COSPEC_MAX_SPLITS; ++sp) {
-        const int64_t units = rows * sp;
-        if (units > free_slots || units > INT32_MAX || (sp > 1 && nvec / sp < kReduceThreads)) break;
-        const int64_t blocks = units < cap ? units : cap;
-        const int64_t cost = (units + blocks - 1) / blocks * ((nvec + sp - 1) / sp);
-        if (cost < best_cost) {
-            best_cost = cost;
-            best = DraftPlan{static_cast<int32_t>(sp), static_cast<int32_t>(blocks)};
-        }
-    }
-    return best;
-}
-
-int32_t auto_splits(int64_t rows, int64_t nvec) {
-    int64_t s = (kAutoBlocks + rows - 1) / rows;
-    const int64_t by_len = nvec / kReduceThreads;    // at least one vector per lane
+// Splits per row when the caller gives none, from the rows of the launch, the 16-byte
+// vectors of a row and the reduction workgroups the device holds at once (`slots`):
+//  - at least 1.5 rounds of whole rows (the large batches): one workgroup per row, the
+//    cheapest merge and the fewest partials (the large chain batch: 3840 rows on 2048
+//    slots, one split 85.6% of the HBM peak, two 84.9%, three 83.8%);
+//  - fewer rows: about four rounds of pieces, so that every slot stays busy and the
+//    last round is short (the peaked chain batch, 960 rows: one split 82%, nine 86%),
+//    but at least four vectors per lane, so every lane keeps its loads in flight (the
+//    small chain batch's reduction 4.8 us at 15 splits against 9.9 us at 62; the tiny
+//    chain's 1.2 against 2.4 us at 8 and 4 splits).
+int32_t auto_splits(int64_t rows, int64_t nvec, int64_t slots) {
+    if (rows <= 0) return 1;
+    if (2 * rows >= 3 * slots) return 1;
+    int64_t s = (4 * slots + rows / 2) / rows;
+    const int64_t by_len = nvec / (4 * kReduceThreads);
     if (s > by_len) s = by_len;
     if (s > COSPEC_MAX_SPLITS) s = COSPEC_MAX_SPLITS;
     if (s < 1) s = 1;
     return static_cast<int32_t>(s);
+}
+
+// The partial layout of a step: the caller's split count, or the rule above.  Both
+// phases of a split step derive it from the same arguments.
+PartPlan make_plan(int64_t n_tgt_rows, int64_t n_drf_rows, int64_t nvec, int32_t override_splits, Dtype dt) {
+    PartPlan p{};
+    p.n_tgt_rows = n_tgt_rows;
+    p.splits = override_splits > 0 ? override_splits : auto_splits(n_tgt_rows + n_drf_rows, nvec, reduce_slots(dt));
+    return p;
 }
 
 bool feats_aligned(const cospec_features *f) {
@@ -195,15 +192,17 @@ enum Phase { kWhole, kReducePhase, kArbitratePhase };
 cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *out_tokens,
                   int32_t *out_path) {
     const int eb = elem_bytes(c.dt);
-    const int64_t rows = static_cast<int64_t>(c.B) * (c.RT + c.RD);
+    const int64_t n_tgt = static_cast<int64_t>(c.B) * c.RT, n_drf = static_cast<int64_t>(c.B) * c.RD;
+    const int64_t rows = n_tgt + n_drf;
     const int64_t nvec = static_cast<int64_t>(c.V) * eb / 16;
-    int32_t splits = auto_splits(rows, nvec);
+    int32_t override_splits = 0;
     if (c.opts && c.opts->splits) {
         if (c.opts->splits < 0 || c.opts->splits > COSPEC_MAX_SPLITS) return COSPEC_ERR_UNSUPPORTED;
-        splits = c.opts->splits;
+        override_splits = c.opts->splits;
     }
     const Layout L = layout(rows, c.B, c.RT, c.D, c.head, c.V);
     const float *uniform = c.opts ? c.opts->sample_uniform : nullptr;
+    const PartPlan plan = make_plan(n_tgt, n_drf, nvec, override_splits, static_cast<Dtype>(c.dt));
     if (uniform && !aligned(uniform, 4)) return COSPEC_ERR_INVALID_ARG;
     const float *policy_u = c.opts ? c.opts->policy_uniform : nullptr;
     if (policy_u && !aligned(policy_u, 4)) return COSPEC_ERR_INVALID_ARG;
@@ -215,8 +214,11 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         for (const void *p : p4)
             if (p && !aligned(p, 4)) return COSPEC_ERR_INVALID_ARG;
     }
-    if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    if (rows * plan.splits > L.partial_slots || rows * plan.splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
     if (!c.ws || !aligned(c.ws, kAlign) || c.ws_bytes < L.total) return COSPEC_ERR_WORKSPACE;
+    const int64_t *hidden_row0 = c.opts ? c.opts->hidden_row0 : nullptr;
+    const int64_t hidden_rows = hidden_row0 ? c.opts->hidden_rows : static_cast<int64_t>(c.B) * c.D;
+    if (hidden_row0 && (!aligned(hidden_row0, 8) || hidden_rows < 0)) return COSPEC_ERR_INVALID_ARG;
 
     char *ws = static_cast<char *>(c.ws);
     float4 *partials = reinterpret_cast<float4 *>(ws + L.partials);
@@ -235,109 +237,82 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     const bool lambda_decides = !(c.lambda >= 0.0f && c.lambda < 1.0f);
     const bool want_scores = F.z_tilde || F.policy || F.logp_action;
     const bool head = decisions && (!lambda_decides || want_scores || policy_u);
-
-    const bool aux = c.opts && c.opts->aux_stream;
-    if (aux && (phase != kWhole || !c.opts->aux_ready || !c.opts->aux_done || c.opts->aux_stream == c.stream))
-        return COSPEC_ERR_INVALID_ARG;
-    const int64_t *hidden_row0 = c.opts ? c.opts->hidden_row0 : nullptr;
-    const int64_t hidden_rows = hidden_row0 ? c.opts->hidden_rows : static_cast<int64_t>(c.B) * c.D;
-    if (hidden_row0 && (!aligned(hidden_row0, 8) || hidden_rows < 0)) return COSPEC_ERR_INVALID_ARG;
     const bool do_reduce = phase != kArbitratePhase, do_arbitrate = phase != kReducePhase;
-
-    ReduceArgs ra{};
-    ra.tgt = static_cast<const char *>(c.tgt);
-    ra.drf = static_cast<const char *>(c.drf);
-    ra.ld_bytes = c.ld * eb;
-    ra.V = c.V;
-    ra.n_tgt_rows = static_cast<int32_t>(c.B * c.RT);
-    ra.parent = c.is_tree ? c.parent : nullptr;
-    ra.N = static_cast<int32_t>(c.RT);
-    ra.splits = splits;
-    int64_t vps = (nvec + splits - 1) / splits;
-    if (uniform) vps = (vps + kSegVecs - 1) / kSegVecs * kSegVecs;   // segments never straddle splits
-    ra.vec_per_split = static_cast<int32_t>(vps);
-    ra.partials = partials;
-    ra.seg = uniform ? seg : nullptr;
-    ra.nseg = static_cast<int32_t>(n_segments(c.V, eb));
-
     const Dtype dt = static_cast<Dtype>(c.dt);
-    auto record = [&](hipEvent_t ev, hipStream_t s) { return !ev || hipEventRecord(ev, s) == hipSuccess; };
+    auto record = [&](hipEvent_t ev) { return !ev || hipEventRecord(ev, c.stream) == hipSuccess; };
 
-    // 1. target rows; the draft rows too in the same launch unless the head overlaps
-    //    their reduction on the aux stream (one launch is cheaper than two)
-    const bool split_reduce = aux && head;
-    const int64_t n_drf = static_cast<int64_t>(c.B) * c.RD;
-    const int64_t drf_base = static_cast<int64_t>(ra.n_tgt_rows) * splits;   // first draft partial
-    DraftPlan dp{splits, 0};
-    if (split_reduce) {
-        dp = c.opts->splits ? DraftPlan{splits, kOverlapBlocksPerCU * cu_count()}   // override: as given
-                            : draft_plan(n_drf, nvec, L.partial_slots - drf_base);
-    }
-    // The decision work (sampling, decide, head) runs on the aux stream when given,
-    // overlapping the draft-row reduction; otherwise everything is on `stream`.
-    hipStream_t side = c.stream;
     if (do_reduce) {
-    // the decide step's arguments (its launch follows the reductions)
-    DecideArgs da{};
-    da.tgt = ra.tgt;
-    da.ld_bytes = ra.ld_bytes;
-    da.V = c.V;
-    da.B = c.B;
-    da.RT = static_cast<int32_t>(c.RT);
-    da.D = static_cast<int32_t>(c.D);
-    da.is_tree = c.is_tree;
-    da.parent = c.parent;
-    da.tokens = c.tokens;
-    da.partials = partials;
-    da.splits = splits;
-    da.score_mismatch = phase == kReducePhase ? decisions : head;   // phase 2 may need the list
-    da.sampled = uniform != nullptr;
-    da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
-    da.tgt_cand = F.tgt_candidate;
-    da.logp_tgt = F.logp_tgt; da.delta = F.delta;
-    da.ws_tgt_arg = tgt_arg;
-    da.ws_logp_tgt = ws_logp;
-    da.ws_state = state;
-    da.ws_listpos = listpos;
-    da.ws_list = list;
-    da.ws_count = count;
-    ReduceArgs rt = ra;
-    rt.row_offset = 0;
-    rt.n_rows = split_reduce ? ra.n_tgt_rows : static_cast<int32_t>(c.B * (c.RT + c.RD));
-    rt.reset_counter = count;
-    if (!record(c.opts ? c.opts->reduce_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
-    if (launch_reduce(dt, rt, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
-    if (!record(c.opts ? c.opts->reduce_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
-    if (split_reduce) {
-        if (hipEventRecord(c.opts->aux_ready, c.stream) != hipSuccess ||
-            hipStreamWaitEvent(c.opts->aux_stream, c.opts->aux_ready, 0) != hipSuccess)
-            return COSPEC_ERR_HIP;
-        side = c.opts->aux_stream;
-    }
+        DecideArgs da{};
+        da.tgt = static_cast<const char *>(c.tgt);
+        da.ld_bytes = c.ld * eb;
+        da.V = c.V;
+        da.B = c.B;
+        da.RT = static_cast<int32_t>(c.RT);
+        da.D = static_cast<int32_t>(c.D);
+        da.is_tree = c.is_tree;
+        da.parent = c.parent;
+        da.tokens = c.tokens;
+        da.partials = partials;
+        da.plan = plan;
+        da.score_mismatch = phase == kReducePhase ? decisions : head;   // phase 2 may need the list
+        da.sampled = uniform != nullptr;
+        da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
+        da.tgt_cand = F.tgt_candidate;
+        da.logp_tgt = F.logp_tgt; da.delta = F.delta;
+        da.ws_tgt_arg = tgt_arg;
+        da.ws_logp_tgt = ws_logp;
+        da.ws_state = state;
+        da.ws_listpos = listpos;
+        da.ws_list = list;
+        da.ws_count = count;
 
-    // 1b. temperature-1 candidates
-    if (uniform) {
-        SampleArgs sa{};
-        sa.tgt = ra.tgt;
-        sa.ld_bytes = ra.ld_bytes;
-        sa.V = c.V;
-        sa.n_rows = ra.n_tgt_rows;
-        sa.partials = partials;
-        sa.splits = splits;
-        sa.seg = seg;
-        sa.nseg = ra.nseg;
-        sa.uniform = uniform;
-        sa.cand = tgt_arg;
-        if (launch_sample(dt, sa, side) != hipSuccess) return COSPEC_ERR_HIP;
-    }
+        ReduceArgs ra{};
+        ra.tgt = da.tgt;
+        ra.drf = static_cast<const char *>(c.drf);
+        ra.ld_bytes = da.ld_bytes;
+        ra.V = c.V;
+        ra.n_tgt_rows = static_cast<int32_t>(n_tgt);
+        ra.n_rows = static_cast<int32_t>(rows);
+        ra.parent = c.is_tree ? c.parent : nullptr;
+        ra.N = static_cast<int32_t>(c.RT);
+        ra.plan = plan;
+        int64_t vps = (nvec + plan.splits - 1) / plan.splits;
+        if (uniform) vps = (vps + kSegVecs - 1) / kSegVecs * kSegVecs;   // segments never straddle splits
+        ra.vec_per_split = static_cast<int32_t>(vps);
+        ra.partials = partials;
+        ra.reset_counter = count;
+        ra.seg = uniform ? seg : nullptr;
+        ra.nseg = static_cast<int32_t>(n_segments(c.V, eb));
 
-    // 2. decide
-    if (launch_decide(dt, da, side) != hipSuccess) return COSPEC_ERR_HIP;
+        if (!record(c.opts ? c.opts->reduce_begin : nullptr)) return COSPEC_ERR_HIP;
+        if (launch_reduce(dt, ra, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        if (!record(c.opts ? c.opts->reduce_end : nullptr)) return COSPEC_ERR_HIP;
+        // the second pair brackets nothing: back to back, it measures what an event
+        // interval adds by itself
+        if (!record(c.opts ? c.opts->reduce2_begin : nullptr)) return COSPEC_ERR_HIP;
+        if (!record(c.opts ? c.opts->reduce2_end : nullptr)) return COSPEC_ERR_HIP;
+
+        // temperature-1 candidates
+        if (uniform) {
+            SampleArgs sa{};
+            sa.tgt = ra.tgt;
+            sa.ld_bytes = ra.ld_bytes;
+            sa.V = c.V;
+            sa.n_rows = ra.n_tgt_rows;
+            sa.partials = partials;
+            sa.plan = plan;
+            sa.seg = seg;
+            sa.nseg = ra.nseg;
+            sa.uniform = uniform;
+            sa.cand = tgt_arg;
+            if (launch_sample(dt, sa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        }
+        if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
     }
     if (!do_arbitrate) return COSPEC_OK;
 
-    // 3. head, on the aux stream when given; for chains the finish computes its
-    //    second layer (the logits of each sequence's mismatches) itself
+    // the head; for chains the finish computes its second layer (the logits of each
+    // sequence's mismatches) itself
     const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
     const bool fuse_head = head && !c.is_tree;
     HeadArgs ha{};
@@ -361,30 +336,14 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ha.upart = upart;
         ha.z = zlog;
         const Dtype hdt = static_cast<Dtype>(c.head->dtype);
-        if ((fuse_head ? launch_head_gemm(hdt, ha, side) : launch_head(hdt, ha, side)) != hipSuccess)
+        if ((fuse_head ? launch_head_gemm(hdt, ha, c.stream) : launch_head(hdt, ha, c.stream)) != hipSuccess)
             return COSPEC_ERR_HIP;
     }
-    if (split_reduce && hipEventRecord(c.opts->aux_done, side) != hipSuccess) return COSPEC_ERR_HIP;
 
-    // 4. draft rows (features only), when they were not reduced with the target rows:
-    //    a capped grid, so that the aux stream's kernels find room on every CU
-    ReduceArgs rd = ra;
-    rd.row_offset = ra.n_tgt_rows;
-    rd.n_rows = split_reduce ? static_cast<int32_t>(n_drf) : 0;   // only in a whole step
-    rd.reset_counter = nullptr;
-    rd.splits = dp.splits;
-    rd.vec_per_split = static_cast<int32_t>((nvec + dp.splits - 1) / dp.splits);
-    rd.part_base = drf_base;
-    rd.max_blocks = dp.blocks;
-    if (!record(c.opts ? c.opts->reduce2_begin : nullptr, c.stream)) return COSPEC_ERR_HIP;
-    if (launch_reduce(dt, rd, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
-    if (!record(c.opts ? c.opts->reduce2_end : nullptr, c.stream)) return COSPEC_ERR_HIP;
-    if (split_reduce && hipStreamWaitEvent(c.stream, c.opts->aux_done, 0) != hipSuccess) return COSPEC_ERR_HIP;
-
-    // 5. finish
+    // finish
     FinishArgs fa{};
-    fa.drf = ra.drf;
-    fa.ld_bytes = ra.ld_bytes;
+    fa.drf = static_cast<const char *>(c.drf);
+    fa.ld_bytes = c.ld * eb;
     fa.V = c.V;
     fa.B = c.B;
     fa.RT = static_cast<int32_t>(c.RT);
@@ -393,8 +352,8 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     fa.is_tree = c.is_tree;
     fa.parent = c.parent;
     fa.tokens = c.tokens;
-    fa.drf_partials = partials + drf_base;
-    fa.drf_splits = split_reduce ? dp.splits : splits;
+    fa.partials = partials;
+    fa.plan = plan;
     fa.ws_state = state;
     fa.ws_listpos = listpos;
     fa.z = zlog;
@@ -611,19 +570,21 @@ cospec_status cospec_verify_block_sps(const void *target_logits, const void *dra
     if (!uniforms || !aligned(uniforms, 4) || !accept_len || !aligned(accept_len, 4) || !out_tokens ||
         !aligned(out_tokens, 4) || !feats_aligned(feats))
         return COSPEC_ERR_INVALID_ARG;
-    if (opts && (opts->aux_stream || opts->sample_uniform || opts->policy_uniform || opts->rl || opts->hidden_row0))
+    if (opts && (opts->sample_uniform || opts->policy_uniform || opts->rl || opts->hidden_row0))
         return COSPEC_ERR_INVALID_ARG;                  // only splits and the timing events apply
     if (static_cast<int64_t>(B) * (2 * K + 1) > INT32_MAX / 2) return COSPEC_ERR_UNSUPPORTED;
     const int eb = elem_bytes(logit_dtype);
-    const int64_t rows = static_cast<int64_t>(B) * (2 * K + 1);
+    const int64_t n_tgt = static_cast<int64_t>(B) * (K + 1), n_drf = static_cast<int64_t>(B) * K;
+    const int64_t rows = n_tgt + n_drf;
     const int64_t nvec = static_cast<int64_t>(V) * eb / 16;
-    int32_t splits = auto_splits(rows, nvec);
+    int32_t override_splits = 0;
     if (opts && opts->splits) {
         if (opts->splits < 0 || opts->splits > COSPEC_MAX_SPLITS) return COSPEC_ERR_UNSUPPORTED;
-        splits = opts->splits;
+        override_splits = opts->splits;
     }
     const Layout L = layout(rows, B, K + 1, K, nullptr, V);
-    if (rows * splits > L.partial_slots || rows * splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
+    const PartPlan plan = make_plan(n_tgt, n_drf, nvec, override_splits, static_cast<Dtype>(logit_dtype));
+    if (rows * plan.splits > L.partial_slots || rows * plan.splits > INT32_MAX) return COSPEC_ERR_UNSUPPORTED;
     if (!workspace || !aligned(workspace, kAlign) || workspace_bytes < L.total) return COSPEC_ERR_WORKSPACE;
     char *ws = static_cast<char *>(workspace);
     float4 *partials = reinterpret_cast<float4 *>(ws + L.partials);
@@ -635,24 +596,23 @@ cospec_status cospec_verify_block_sps(const void *target_logits, const void *dra
     ra.drf = static_cast<const char *>(draft_logits);
     ra.ld_bytes = ld * eb;
     ra.V = V;
-    ra.n_tgt_rows = B * (K + 1);
-    ra.row_offset = 0;
+    ra.n_tgt_rows = static_cast<int32_t>(n_tgt);
     ra.n_rows = static_cast<int32_t>(rows);
-    ra.splits = splits;
-    ra.vec_per_split = static_cast<int32_t>((nvec + splits - 1) / splits);
+    ra.plan = plan;
+    ra.vec_per_split = static_cast<int32_t>((nvec + plan.splits - 1) / plan.splits);
     ra.partials = partials;
     ra.reset_counter = reinterpret_cast<int32_t *>(ws + L.count);
     if (opts && opts->reduce_begin && hipEventRecord(opts->reduce_begin, stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (launch_reduce(dt, ra, stream) != hipSuccess) return COSPEC_ERR_HIP;
     if (opts && opts->reduce_end && hipEventRecord(opts->reduce_end, stream) != hipSuccess) return COSPEC_ERR_HIP;
-    // no second reduction launch here: the second pair brackets nothing, as in a whole step
+    // the second pair brackets nothing, as in a whole step
     if (opts && opts->reduce2_begin && hipEventRecord(opts->reduce2_begin, stream) != hipSuccess)
         return COSPEC_ERR_HIP;
     if (opts && opts->reduce2_end && hipEventRecord(opts->reduce2_end, stream) != hipSuccess) return COSPEC_ERR_HIP;
 
     DecideArgs da{};
     da.tgt = ra.tgt; da.ld_bytes = ra.ld_bytes; da.V = V; da.B = B; da.RT = K + 1; da.D = K;
-    da.tokens = draft_tokens; da.partials = partials; da.splits = splits;
+    da.tokens = draft_tokens; da.partials = partials; da.plan = plan;
     da.tgt_argmax = F.tgt_argmax; da.tgt_max = F.tgt_max; da.tgt_lse = F.tgt_lse; da.tgt_ent = F.tgt_entropy;
     da.tgt_cand = F.tgt_candidate; da.logp_tgt = F.logp_tgt; da.delta = F.delta;
     da.ws_tgt_arg = reinterpret_cast<int32_t *>(ws + L.tgt_arg);
@@ -665,8 +625,7 @@ cospec_status cospec_verify_block_sps(const void *target_logits, const void *dra
 
     SpsArgs sa{};
     sa.tgt = ra.tgt; sa.drf = ra.drf; sa.ld_bytes = ra.ld_bytes; sa.V = V; sa.B = B; sa.K = K;
-    sa.tokens = draft_tokens; sa.uniform = uniforms; sa.partials = partials; sa.splits = splits;
-    sa.drf_row0 = static_cast<int64_t>(B) * (K + 1);
+    sa.tokens = draft_tokens; sa.uniform = uniforms; sa.partials = partials; sa.plan = plan;
     sa.ws_state = da.ws_state; sa.ws_logp_tgt = da.ws_logp_tgt;
     sa.seg_mass = reinterpret_cast<float *>(ws + L.seg);
     sa.nseg = static_cast<int32_t>(n_segments(V, eb));

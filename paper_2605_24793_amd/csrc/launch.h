@@ -17,11 +17,35 @@ constexpr int kHeadMaxSplit = 32;
 constexpr int kXcds = 8;             // MI355X: 8 XCDs, each with its own L2
 constexpr int kMaxSeqRows = 256;      // rows per sequence / nodes per tree held in LDS
 constexpr int kSegVecs = 64;          // 16-byte vectors per probability-mass segment (one wave load)
+constexpr int kMaxReduceSlots = 4096; // cap on the resident reduction workgroups the split rule assumes
 
 enum Dtype : int32_t { kF32 = 0, kBF16 = 1 };
 
-// Per-decision state byte written by the decide kernel.
+// Per-decision state byte written by the decide step.
 enum : uint8_t { kStateMismatch = 0, kStateMatch = 1, kStateReject = 2 };
+
+// Where the split partials of the logit rows are.  Rows are numbered target rows
+// first (0 .. n_tgt_rows-1), then draft rows; every row is cut into `splits` pieces of
+// equal length (one workgroup each) and row r's partials are slots r * splits ..
+// r * splits + splits - 1, so a sequence's rows' partials are consecutive slots too.
+struct PartPlan {
+    int32_t splits;
+    int64_t n_tgt_rows;
+};
+
+struct RowParts {
+    int64_t first;
+    int32_t count;
+};
+
+__host__ __device__ inline RowParts row_parts(const PartPlan &p, int64_t r) {
+    return RowParts{r * p.splits, p.splits};
+}
+
+// The partials of rows [r0, r1): consecutive slots.
+__host__ __device__ inline RowParts rows_parts(const PartPlan &p, int64_t r0, int64_t r1) {
+    return RowParts{r0 * p.splits, static_cast<int32_t>((r1 - r0) * p.splits)};
+}
 
 struct DecideArgs {
     const char *tgt;
@@ -34,7 +58,7 @@ struct DecideArgs {
     const int32_t *parent;     // tree only
     const int32_t *tokens;     // chain [B][K], tree [B][N]
     const float4 *partials;
-    int32_t splits;
+    PartPlan plan;
     int32_t score_mismatch;    // compact mismatches for the head
     int32_t sampled;           // ws_tgt_arg already holds the candidates (k_sample)
     int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent; int32_t *tgt_cand;
@@ -53,21 +77,16 @@ struct ReduceArgs {
     int64_t ld_bytes;          // row stride in bytes (multiple of 16)
     int32_t V;
     int32_t n_tgt_rows;        // B * target rows per sequence; rows past it are draft rows
-    int32_t row_offset;        // first row of this launch (target rows, then draft rows)
-    int32_t n_rows;            // rows in this launch
+    int32_t n_rows;            // rows of the launch (target rows, then draft rows)
     const int32_t *parent;     // tree: [B][N]; draft rows of leaves are skipped
     int32_t N;                 // tree nodes per tree
-    int32_t splits;            // units per row of this launch
+    PartPlan plan;
     int32_t vec_per_split;     // 16-byte vectors per split
-    float4 *partials;          // {max, argmax bits, S, T} per unit
-    int64_t part_base;         // slot of the launch's first unit; unit u (split fastest)
-                               // writes partials[part_base + u]
-    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide kernel's counter), or null
+    float4 *partials;          // {max, argmax bits, S, T} per piece
+    int32_t *reset_counter;    // zeroed by workgroup 0 (the decide step's list counter), or null
     float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
                                // target row, or null; needs vec_per_split % kSegVecs == 0
     int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
-    int32_t max_blocks;        // grid cap (0 = one workgroup per unit): each workgroup then
-                               // takes every max_blocks-th unit
 };
 
 // Temperature-1 candidates: one wave per target row inverts its uniform through
@@ -78,7 +97,7 @@ struct SampleArgs {
     int32_t V;
     int32_t n_rows;            // target rows
     const float4 *partials;
-    int32_t splits;
+    PartPlan plan;
     const float2 *seg;
     int32_t nseg;
     const float *uniform;      // [n_rows]
@@ -115,8 +134,8 @@ struct FinishArgs {
     int32_t is_tree;
     const int32_t *parent;     // tree only
     const int32_t *tokens;     // chain [B][K], tree [B][N]
-    const float4 *drf_partials; // partials of the draft rows: draft row j (B * RD of them)
-    int32_t drf_splits;         // owns drf_partials[j * drf_splits, (j + 1) * drf_splits)
+    const float4 *partials;    // split partials; draft row j is row n_tgt_rows + j of the plan
+    PartPlan plan;
     const uint8_t *ws_state;
     const int32_t *ws_listpos;
     const float *z;            // head logits by compacted position
@@ -149,8 +168,7 @@ struct SpsArgs {
     const int32_t *tokens;     // [B][K]
     const float *uniform;      // [B][K+1]: K acceptance tests, then the last token's draw
     const float4 *partials;
-    int32_t splits;
-    int64_t drf_row0;          // partial-row index of draft row 0 (= B * (K+1))
+    PartPlan plan;             // draft row j is row B * (K+1) + j
     const uint8_t *ws_state;   // decide's state (invalid tokens are rejected)
     const float *ws_logp_tgt;
     float *seg_mass;           // [B][nseg] weights of the last token's distribution
@@ -184,6 +202,7 @@ struct ArbFinishArgs {
 };
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
+int32_t reduce_slots(Dtype dt);   // reduction workgroups resident at once on the current device
 hipError_t launch_sample(Dtype dt, const SampleArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);

@@ -10,21 +10,24 @@
 // Milakov & Gimelshein (2018, "Online normalizer calculation for softmax"),
 // extended with the first moment T; the reference is only raised when a chunk
 // max exceeds it by more than 2^32, so the rescale is almost never taken.
-// One launch covers a contiguous range of rows, target rows before draft rows
-// (normally all of them; the draft rows get a launch of their own when the
-// head overlaps them on a second stream).
+// One launch covers every target and draft row, one workgroup per (row, split);
+// tree draft rows of nodes without a child are skipped.
 //
-// k_decide merges the partials of one sequence's target rows in fixed split
-// order, takes the target's verification candidates (the greedy argmax, ties to
-// the lowest index, or the temperature-1 samples of k_sample), sets
-// Delta = 1[draft token == candidate]
-// (Section 3.1), gathers the draft token's target logit for log p_T
-// (Section 3.4), and compacts the mismatch decisions into one list for the
-// head with a wave ballot and a prefix over the workgroup's waves.
+// The decide step (decide_seq) merges the partials of one sequence's target rows
+// in fixed split order, takes the target's verification candidates (the greedy
+// argmax, ties to the lowest index, or the temperature-1 samples of k_sample), sets
+// Delta = 1[draft token == candidate] (Section 3.1), gathers the draft token's target
+// logit for log p_T (Section 3.4), and compacts the mismatch decisions into one
+// list for the head with a wave ballot and a prefix over the workgroup's waves; it
+// runs as k_decide, one workgroup per sequence, after the reduction.  (Run inside the
+// reduction instead, by the workgroup that completes a sequence's target rows, it was
+// measured slower: its memory round trips, queued behind the streaming loads of every
+// other workgroup, took several microseconds each.)
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "launch.h"
@@ -337,31 +340,18 @@ __device__ inline void stream_segmented(const RowReader &rr, int v0, int v1, int
 
 static_assert(kReduceThreads >= kMaxSeqRows, "a tree node's children are found by one thread each");
 
-// One unit of work: split `split` of row `row`, whose partial goes to slot `slot`.
+// Reduces 16-byte vectors [v0, v1) of row `row`, plus the row's elements past its last
+// whole vector when `with_tail`.  Every thread of the workgroup takes part; thread 0
+// returns the piece's partial {max, first index of the max, S, T}.
 template <int DT, bool SEG>
-__device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int split, int64_t slot) {
+__device__ __forceinline__ float4 reduce_piece(const ReduceArgs &a, int row, int v0, int v1, bool with_tail) {
     using E = Elt<DT>;
     constexpr int NV = E::kPerVec;
     const int tid = threadIdx.x;
-
-    const char *rp;
-    if (row < a.n_tgt_rows) {
-        rp = a.tgt + static_cast<int64_t>(row) * a.ld_bytes;
-    } else {
-        const int r = row - a.n_tgt_rows;
-        rp = a.drf + static_cast<int64_t>(r) * a.ld_bytes;
-        if (a.parent) {   // tree: only nodes with a child need their draft row
-            const int b = r / a.N, n = r - b * a.N;
-            const int m = n + 1 + tid;   // every later node: N <= kMaxSeqRows <= kReduceThreads
-            const bool child = m < a.N && a.parent[static_cast<int64_t>(b) * a.N + m] == n;
-            if (!__syncthreads_or(child)) return;
-        }
-    }
-
+    const char *rp = row < a.n_tgt_rows ? a.tgt + static_cast<int64_t>(row) * a.ld_bytes
+                                        : a.drf + static_cast<int64_t>(row - a.n_tgt_rows) * a.ld_bytes;
     const int nvec = static_cast<int>((static_cast<int64_t>(a.V) * E::kBytes) / 16);
     const int tail = a.V - nvec * NV;
-    const int v0 = split * a.vec_per_split;
-    const int v1 = min(v0 + a.vec_per_split, nvec);
     const u32x4 *rv = reinterpret_cast<const u32x4 *>(rp);
 
     Lane st{-INFINITY, -1, -kFarBelow, -INFINITY, 0.f, 0.f};   // the first chunk always rescales
@@ -374,9 +364,9 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
     const bool staged = nsg <= kSegStage;
     if (SEG && seg) stream_segmented<DT>(rr, v0, v1, tid, st, seg, (lds_fw *)s_seg, sbase, staged);
     else stream_plain<DT>(rr, v0, v1, tid, st);
-    // elements past the last whole vector: the last split's first lane (their own
-    // segment, the row's last, when segments are written)
-    if (tail > 0 && split == a.splits - 1 && tid == 0) {
+    // elements past the last whole vector: the first lane of the piece that ends the
+    // row (their own segment, the row's last, when segments are written)
+    if (tail > 0 && with_tail && tid == 0) {
         const int64_t e0 = static_cast<int64_t>(nvec) * NV;
         float cm = -INFINITY;
         for (int k = 0; k < tail; ++k) cm = fmaxf(cm, E::at(rp, e0 + k));
@@ -451,10 +441,11 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
     }
     if (lane == 0) { s_S[wave] = S; s_T[wave] = T; }
     __syncthreads();
+    float4 part = make_float4(0.f, 0.f, 0.f, 0.f);
     if (tid == 0) {
         float SS = s_S[0], TT = s_T[0];
         for (int w = 1; w < kReduceThreads / 64; ++w) { SS += s_S[w]; TT += s_T[w]; }
-        a.partials[slot] = make_float4(M, __int_as_float(s_idx[0]), SS, TT);
+        part = make_float4(M, __int_as_float(s_idx[0]), SS, TT);
     }
     // the staged segment masses, complete since every wave passed the barriers above;
     // nontemporal stores, so that no dirty line waits in L2 for the kernel-end write-back
@@ -465,26 +456,19 @@ __device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int row, int sp
             __builtin_nontemporal_store(s_seg[2 * i], &seg[sbase + i].x);
             __builtin_nontemporal_store(s_seg[2 * i + 1], &seg[sbase + i].y);
         }
+    return part;
 }
 
-// Units are (row, split) pairs of the launch's rows, split fastest.  Normally there is
-// one workgroup per unit; with a capped grid each workgroup takes every gridDim.x-th
-// unit, which bounds how many of its waves share a CU with another stream's kernels.
-template <int DT, bool SEG>
-__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.reset_counter) *a.reset_counter = 0;
-    const int units = a.n_rows * a.splits;
-    for (int u = blockIdx.x; u < units; u += gridDim.x) {
-        const int r = u / a.splits, split = u - r * a.splits;
-        reduce_unit<DT, SEG>(a, a.row_offset + r, split, a.part_base + u);
-        __syncthreads();            // the workgroup's LDS is reused by the next unit
-    }
-}
-
+// One sequence's (or tree's) decision step, by one workgroup of kDecideThreads:
+// merges the partials of its target rows in fixed split order, takes the
+// verification candidates (the greedy argmax, ties to the lowest index, or the
+// temperature-1 samples k_sample left), sets Delta = 1[draft token == candidate]
+// (Section 3.1), gathers the draft token's target logit for log p_T (Section 3.4), and
+// compacts the mismatch decisions into the head's list with a wave ballot and a
+// prefix over the workgroup's waves (one atomic addition per sequence).
 template <int DT>
-__global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
+__device__ __forceinline__ void decide_seq(const DecideArgs &a, int b) {
     using E = Elt<DT>;
-    const int b = blockIdx.x;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     // per row: max and ln S, so that log p(token) = (x - max) - ln S keeps full
@@ -512,18 +496,21 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
             xt = E::at(a.tgt + (static_cast<int64_t>(b) * a.RT + p) * a.ld_bytes, tok);
         }
     }
-    // the sequence's target partials are contiguous: staged in LDS when rows are split
-    const int64_t np = static_cast<int64_t>(a.RT) * a.splits;
-    const float4 *seq_parts = a.partials + static_cast<int64_t>(b) * np;
-    const bool staged = a.splits > 1 && np <= kStageParts;
+    // the sequence's target partials are consecutive slots: staged in LDS when there are
+    // several per row (one memory round trip for all of them)
+    const int64_t r0 = static_cast<int64_t>(b) * a.RT;
+    const RowParts sp = rows_parts(a.plan, r0, r0 + a.RT);
+    const float4 *seq_parts = a.partials + sp.first;
+    const bool staged = sp.count > a.RT && sp.count <= kStageParts;
     if (staged) {
-        stage_partials(seq_parts, np, s_parts, t, kDecideThreads);
+        stage_partials(seq_parts, sp.count, s_parts, t, kDecideThreads);
         __syncthreads();
     }
     for (int j = t; j < a.RT; j += kDecideThreads) {
-        const int64_t r = static_cast<int64_t>(b) * a.RT + j;
-        const RowStat rs = staged ? merge_row_lds(s_parts + j * a.splits, a.splits)
-                                  : merge_row(seq_parts + static_cast<int64_t>(j) * a.splits, a.splits);
+        const int64_t r = r0 + j;
+        const RowParts rp = row_parts(a.plan, r);
+        const int64_t off = rp.first - sp.first;
+        const RowStat rs = staged ? merge_row_lds(s_parts + off, rp.count) : merge_row(seq_parts + off, rp.count);
         // the verification candidate: the argmax, or the temperature-1 sample
         // k_sample left in ws_tgt_arg
         const int cand = a.sampled ? a.ws_tgt_arg[r] : rs.arg;
@@ -573,19 +560,74 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     }
 }
 
+// Units are (row, split) pairs, split fastest, one workgroup each.  Workgroup 0 also
+// zeroes the decide step's list counter.
+template <int DT, bool SEG>
+__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.reset_counter) *a.reset_counter = 0;
+    using E = Elt<DT>;
+    const int splits = a.plan.splits;
+    const int u = blockIdx.x;
+    const int row = u / splits, split = u - row * splits;
+    if (row >= a.n_tgt_rows && a.parent) {   // tree: only nodes with a child need their draft row
+        const int r = row - a.n_tgt_rows;
+        const int b = r / a.N, n = r - b * a.N;
+        const int m = n + 1 + threadIdx.x;   // every later node: N <= kMaxSeqRows <= kReduceThreads
+        const bool child = m < a.N && a.parent[static_cast<int64_t>(b) * a.N + m] == n;
+        if (!__syncthreads_or(child)) return;
+    }
+    const int nvec = static_cast<int>((static_cast<int64_t>(a.V) * E::kBytes) / 16);
+    const int v0 = split * a.vec_per_split;
+    const int v1 = min(v0 + a.vec_per_split, nvec);
+    const float4 part = reduce_piece<DT, SEG>(a, row, v0, v1, split == splits - 1);
+    if (threadIdx.x == 0) a.partials[u] = part;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
+    decide_seq<DT>(a, blockIdx.x);
+}
+
 }  // namespace
 
 template <int DT>
 void launch_reduce_t(const ReduceArgs &a, dim3 grid, hipStream_t s) {
-    const bool seg = a.seg && a.row_offset < a.n_tgt_rows;
-    if (seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true>), grid, dim3(kReduceThreads), 0, s, a);
+    if (a.seg) hipLaunchKernelGGL((k_vocab_reduce<DT, true>), grid, dim3(kReduceThreads), 0, s, a);
     else hipLaunchKernelGGL((k_vocab_reduce<DT, false>), grid, dim3(kReduceThreads), 0, s, a);
 }
 
+// Reduction workgroups resident at once on the current device (greedy variant of the
+// dtype: eight per CU for bf16 on MI355X, 2048 in all); the split rule sizes the grid
+// by it.  Looked up once per device and dtype.
+int32_t reduce_slots(Dtype dt) {
+    constexpr int kMaxDev = 64;
+    static std::mutex mu;
+    static int32_t cache[kMaxDev][2];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) dev = -1;
+    const int di = dt == kBF16 ? 1 : 0;
+    if (dev >= 0) {
+        std::lock_guard<std::mutex> lock(mu);
+        if (cache[dev][di]) return cache[dev][di];
+    }
+    const void *fn = dt == kBF16 ? reinterpret_cast<const void *>(&k_vocab_reduce<kBF16, false>)
+                                 : reinterpret_cast<const void *>(&k_vocab_reduce<kF32, false>);
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kReduceThreads, 0) != hipSuccess || per_cu < 1)
+        per_cu = 8;
+    if (dev < 0 || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 256;
+    const int64_t g = static_cast<int64_t>(per_cu) * cus;
+    const int32_t r = static_cast<int32_t>(g < kMaxReduceSlots ? g : kMaxReduceSlots);
+    if (dev >= 0) {
+        std::lock_guard<std::mutex> lock(mu);
+        cache[dev][di] = r;
+    }
+    return r;
+}
+
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
-    int64_t units = static_cast<int64_t>(a.n_rows) * a.splits;
-    if (a.max_blocks > 0 && units > a.max_blocks) units = a.max_blocks;
-    const dim3 grid(static_cast<unsigned>(units));
+    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(a.n_rows) * a.plan.splits));
     if (grid.x == 0) return hipSuccess;
     if (dt == kBF16) launch_reduce_t<kBF16>(a, grid, s);
     else launch_reduce_t<kF32>(a, grid, s);

@@ -42,7 +42,8 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= a.n_rows) return;                                   // whole wave leaves
-    const RowStat rs = merge_row(a.partials + static_cast<int64_t>(row) * a.splits, a.splits);
+    const RowParts parts = row_parts(a.plan, row);
+    const RowStat rs = merge_row(a.partials + parts.first, parts.count);
     const float R = __fmul_rn(rs.max, kLog2e);
     float u = a.uniform[row];
     u = u >= 0.f ? fminf(u, kBelowOne) : 0.f;                      // NaN and negatives act as 0

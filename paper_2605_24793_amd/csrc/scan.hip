@@ -2,9 +2,8 @@
 // verdicts, the first stop and the emitted tokens.
 //
 // The draft rows are needed only for features (log p_D of the draft token, the
-// draft entropy); the decision itself needs the target rows alone.  So the
-// draft rows are reduced after the decide kernel, while the head may run on a
-// second stream, and merged here.
+// draft entropy); the decision itself needs the target rows alone, so the draft
+// rows' partials are merged here.
 //
 // Chain (Section 3.3, Eq. cospec_length): one wave per sequence, lane i-1 owns
 // decision i and draft row i-1.  A matched decision passes (z_tilde = +inf,
@@ -87,11 +86,14 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, f
     using E = Elt<DT>;
     const int K = a.D;
     const int64_t di = static_cast<int64_t>(b) * K + lane;  // decision lane+1, draft row lane
-    const int64_t np = static_cast<int64_t>(K) * a.drf_splits;
-    const float4 *seq_parts = a.drf_partials + static_cast<int64_t>(b) * np;
-    const bool staged = a.drf_splits > 1 && np <= cap;
+    // the sequence's draft-row partials are consecutive slots
+    const PartPlan &plan = a.plan;
+    const int64_t r0 = plan.n_tgt_rows + static_cast<int64_t>(b) * K;
+    const RowParts sp = K > 0 ? rows_parts(plan, r0, r0 + K) : RowParts{0, 0};
+    const float4 *seq_parts = a.partials + sp.first;
+    const bool staged = sp.count > K && sp.count <= cap;
     if (staged) {                 // one wave writes and then reads: LDS keeps the wave's order
-        stage_partials(seq_parts, np, stage, lane, 64);
+        stage_partials(seq_parts, sp.count, stage, lane, 64);
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
         __builtin_amdgcn_wave_barrier();
     }
@@ -101,8 +103,9 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, f
         const bool valid = c.st != kStateReject;
         c.tok_d = a.tokens[di];
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
-        const RowStat rs = staged ? merge_row_lds(stage + lane * a.drf_splits, a.drf_splits)
-                                  : merge_row(seq_parts + static_cast<int64_t>(lane) * a.drf_splits, a.drf_splits);
+        const RowParts rp = row_parts(plan, r0 + lane);
+        const RowStat rs = staged ? merge_row_lds(stage + (rp.first - sp.first), rp.count)
+                                  : merge_row(a.partials + rp.first, rp.count);
         write_drf(a, di, rs);
         if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
         c.pos = a.ws_listpos[di];
@@ -246,7 +249,10 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
     // draft rows were reduced for nodes with a child only
     if (n < N) {
         RowStat rs{NAN, NAN, NAN, NAN, -1};
-        if (s_child[n]) rs = merge_row(a.drf_partials + (base + n) * a.drf_splits, a.drf_splits);
+        if (s_child[n]) {
+            const RowParts rp = row_parts(a.plan, a.plan.n_tgt_rows + base + n);
+            rs = merge_row(a.partials + rp.first, rp.count);
+        }
         write_drf(a, base + n, rs);
         s_dmax[n] = rs.max;
         s_dlogs[n] = rs.log_s;

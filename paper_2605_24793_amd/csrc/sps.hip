@@ -43,7 +43,8 @@ __global__ __launch_bounds__(256) void k_sps_finish(SpsArgs a) {
     if (lane < K) {
         const uint8_t st = a.ws_state[di];
         const bool valid = st != kStateReject;
-        const RowStat rs = merge_row(a.partials + (a.drf_row0 + di) * a.splits, a.splits);
+        const RowParts rp = row_parts(a.plan, a.plan.n_tgt_rows + di);
+        const RowStat rs = merge_row(a.partials + rp.first, rp.count);
         const float xd = valid ? E::at(a.drf + di * a.ld_bytes, a.tokens[di]) : 0.f;
         const float lpd = valid ? (xd - rs.max) - rs.log_s : NAN;
         const float ratio = valid ? expf(a.ws_logp_tgt[di] - lpd) : 0.f;
@@ -85,8 +86,12 @@ __device__ inline LastRows last_row_ptrs(const SpsArgs &a, int b) {
 __device__ inline void last_row_stats(const SpsArgs &a, int b, LastRows &r) {
     const int s = a.accept_len[b];
     const int64_t trow = static_cast<int64_t>(b) * (a.K + 1) + (s - 1);
-    r.ts = merge_row(a.partials + trow * a.splits, a.splits);
-    if (r.d) r.ds = merge_row(a.partials + (a.drf_row0 + static_cast<int64_t>(b) * a.K + (s - 1)) * a.splits, a.splits);
+    const RowParts tp = row_parts(a.plan, trow);
+    r.ts = merge_row(a.partials + tp.first, tp.count);
+    if (r.d) {
+        const RowParts dp = row_parts(a.plan, a.plan.n_tgt_rows + static_cast<int64_t>(b) * a.K + (s - 1));
+        r.ds = merge_row(a.partials + dp.first, dp.count);
+    }
 }
 
 __device__ inline LastRows last_rows(const SpsArgs &a, int b) {

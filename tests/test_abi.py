@@ -148,13 +148,6 @@ def test_verify_block_split_override_limits():
     assert _block(L, wsb=16, opts=ctypes.byref(binding._Options(splits=64))) == WORKSPACE
 
 
-def test_verify_block_aux_stream_needs_its_events():
-    L = cs.lib()
-    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE))) == INVALID
-    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE, aux_ready=FAKE))) == INVALID
-    assert _block(L, opts=ctypes.byref(binding._Options(aux_stream=FAKE, aux_done=FAKE))) == INVALID
-
-
 def test_verify_block_sample_uniform_alignment():
     L = cs.lib()
     assert _block(L, opts=ctypes.byref(binding._Options(sample_uniform=FAKE + 2))) == INVALID
@@ -185,8 +178,6 @@ def test_split_phase_arguments():
     assert reduce(cand=FAKE + 2) == INVALID
     assert reduce(toks=None) == INVALID
     assert reduce(B=0, cand=None) == OK
-    aux = binding._Options(aux_stream=FAKE, aux_ready=FAKE, aux_done=FAKE)
-    assert reduce(opts=ctypes.byref(aux)) == INVALID          # no second stream in the split form
     # phase 2 checks like cospec_verify_block; a packed hidden map must be 8-byte aligned
     a = L.cospec_verify_block_arbitrate
     args = [FAKE, FAKE, 1, 151936, FAKE, FAKE, ctypes.byref(hd), 0.5, 4, 7, 151936, FAKE, FAKE, None]

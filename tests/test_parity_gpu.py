@@ -49,10 +49,10 @@ def _padded(t, pad):
     return big[:, :, :V]
 
 
-def _gpu_block(wl, lam, splits=0, pad=0, features=True, overlap=False, u=None):
+def _gpu_block(wl, lam, splits=0, pad=0, features=True, u=None):
     out = cs.verify_block(_padded(wl.target, pad), _padded(wl.draft, pad), wl.draft_tokens.to(DEV),
                           wl.hidden.to(DEV), _head_dev(wl.head), lam, features=features,
-                          splits=splits, overlap=overlap,
+                          splits=splits,
                           sample_u=None if u is None else u.to(DEV))
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
@@ -64,10 +64,10 @@ def _ref_block(wl, lam, u=None, cand=None):
                                sample_u=None if u is None else u.double().numpy(), cand_override=cand)
 
 
-def _gpu_tree(tr, lam, splits=0, pad=0, overlap=False, u=None):
+def _gpu_tree(tr, lam, splits=0, pad=0, u=None):
     out = cs.verify_tree(_padded(tr.target, pad), _padded(tr.draft, pad), tr.parent.to(DEV),
                          tr.node_tokens.to(DEV), tr.hidden.to(DEV), _head_dev(tr.head), lam,
-                         splits=splits, overlap=overlap, sample_u=None if u is None else u.to(DEV))
+                         splits=splits, sample_u=None if u is None else u.to(DEV))
     torch.cuda.synchronize()
     return {k: v.cpu() for k, v in out.items()}
 
@@ -126,15 +126,6 @@ def test_config5_full_size():
     stats = parity.check_tree(gpu, oracle_pool.verify_tree(tr, lam))
     _report(f"config 5 (all {tr.B} trees)", stats, gpu)
     _tree_properties(tr, gpu)
-
-
-def test_overlap_stream_matches_oracle_on_the_peaked_batch():
-    """The optional second-stream launch sequence, on the peaked serving batch at one
-    threshold: every sequence against the oracle."""
-    wl = workloads.make_config(3)
-    gpu = _gpu_block(wl, 0.5, overlap=True)
-    stats = parity.check_block(gpu, oracle_pool.verify_block(wl, 0.5))
-    _report("config 3 lambda 0.5, overlap stream", stats, gpu)
 
 
 def _sample(B, n, seed):
@@ -302,37 +293,6 @@ def test_always_accept_on_gpu(lam):
     gpu = _gpu_block(wl, lam, features=False)
     assert (gpu["accept_len"] == wl.K + 1).all()
     assert torch.equal(gpu["tokens"][:, : wl.K], wl.draft_tokens)
-
-
-# Beside the aux stream the draft rows may be reduced in another number of splits,
-# which changes the fp32 summation order of their sums and nothing else.
-_DRAFT_SUMS = ("drf_lse", "drf_entropy", "logp_drf")
-
-
-def _same_up_to_draft_sums(a, b):
-    for k in a:
-        if k in _DRAFT_SUMS:
-            torch.testing.assert_close(a[k], b[k], rtol=1e-5, atol=1e-5, equal_nan=True)
-        else:
-            assert torch.equal(a[k].view(torch.uint8) if a[k].dtype == torch.float32 else a[k],
-                               b[k].view(torch.uint8) if b[k].dtype == torch.float32 else b[k]), k
-
-
-def test_overlap_stream_gives_the_same_results():
-    wl = workloads.make_chain(B=40, K=7, V=30001, d=256, h=128, seed=12, bias=True, noise=1.2)
-    a = _gpu_block(wl, 0.5)
-    b = _gpu_block(wl, 0.5, overlap=True)
-    _same_up_to_draft_sums(a, b)
-    parity.check_block(b, _ref_block(wl, 0.5))
-    # the large chain batch's shape: target rows in one launch, the draft rows in
-    # another beside the head, each compared with the serial step on every sequence
-    big = workloads.make_chain(B=256, K=7, V=151936 // 8, d=512, h=128, seed=14, noise=1.0)
-    _same_up_to_draft_sums(_gpu_block(big, 0.5), _gpu_block(big, 0.5, overlap=True))
-    tr = workloads.make_random_tree(B=6, N=40, V=3001, d=64, h=32, seed=13, bias=True)
-    a = _gpu_tree(tr, 0.5)
-    b = _gpu_tree(tr, 0.5, overlap=True)
-    _same_up_to_draft_sums(a, b)
-    parity.check_tree(b, _ref_tree(tr, 0.5))
 
 
 def _replays_match_eager(p, perturb):
