@@ -8,14 +8,17 @@
 //   1b. k_sample        temperature 1 only: one wave per target row samples the
 //                       candidate by inversion of its uniform (segment masses
 //                       written by step 1, then one segment re-read)
-//   2. k_decide         one workgroup per sequence: target statistics, Delta,
-//                       log p_T, mismatch compaction (device-side count M)
+//   2. k_decide         trees (and the first phase of a split chain step): one
+//                       workgroup per tree: target statistics, Delta, log p_T, mismatch
+//                       compaction (device-side count M)
 //   3. k_head_gemm (+ k_head_epilogue for trees)   MFMA head over the M compacted
 //                       rows (skipped when the threshold decides every mismatch by
-//                       itself and no score is requested)
-//   4. k_chain_finish(_head) / k_tree_finish   draft statistics, log p_D, the head's
-//                       second layer (chains), verdicts (threshold or sampled), first
-//                       stop, emission, and for chains the optional per-round RL
+//                       itself and no score is requested); for chains each workgroup
+//                       derives the mismatch list itself from the partials
+//   4. k_chain_finish(_head) / k_tree_finish   chains: the decision step (target
+//                       statistics, Delta, log p_T); draft statistics, log p_D, the
+//                       head's second layer (chains), verdicts (threshold or sampled),
+//                       first stop, emission, and for chains the optional per-round RL
 //                       statistics
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -74,7 +77,7 @@ inline size_t head_bytes(int64_t m_cap, const cospec_head *hd) {
 
 // Workspace carving shared by the size query and the call.
 struct Layout {
-    size_t partials, seg, tgt_arg, state, listpos, list, count, logp, upart, z, total;
+    size_t partials, seg, tgt_arg, state, listpos, list, count, logp, xtok, upart, z, total;
     int64_t partial_slots;
 };
 
@@ -110,6 +113,7 @@ Layout layout(int64_t rows, int64_t B, int64_t RT, int64_t D, const cospec_head 
     L.list = off;     off += round_up(static_cast<size_t>(B * D) * 4);
     L.count = off;    off += kAlign;
     L.logp = off;     off += round_up(static_cast<size_t>(B * D) * 4);
+    L.xtok = off;     off += round_up(static_cast<size_t>(rows) * 4);
     const int64_t m_cap = B * D;
     L.upart = off;    off += hd ? round_up(static_cast<size_t>(ksplit_for(m_cap, hd)) * static_cast<size_t>(m_cap) *
                                            static_cast<size_t>(hd->h) * 4) : 0;
@@ -231,6 +235,7 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     float *ws_logp = reinterpret_cast<float *>(ws + L.logp);
     float *upart = reinterpret_cast<float *>(ws + L.upart);
     float *zlog = reinterpret_cast<float *>(ws + L.z);
+    float *xtok = reinterpret_cast<float *>(ws + L.xtok);
 
     const cospec_features F = c.feats ? *c.feats : cospec_features{};
     const bool decisions = c.B > 0 && (c.is_tree ? c.D > 1 : c.D > 0);
@@ -238,8 +243,53 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     const bool want_scores = F.z_tilde || F.policy || F.logp_action;
     const bool head = decisions && (!lambda_decides || want_scores || policy_u);
     const bool do_reduce = phase != kArbitratePhase, do_arbitrate = phase != kReducePhase;
+    // chains: the head GEMM's workgroups derive the mismatch list from the partials
+    const bool build_list = !c.is_tree && static_cast<int64_t>(c.B) * c.D <= kBuildListMax;
+    // the candidates are in the workspace when k_sample drew them, and in the second
+    // phase of a split step (the first phase's decision step stored them, argmax or sample)
+    const bool cand_in_ws = uniform != nullptr || phase == kArbitratePhase;
     const Dtype dt = static_cast<Dtype>(c.dt);
     auto record = [&](hipEvent_t ev) { return !ev || hipEventRecord(ev, c.stream) == hipSuccess; };
+
+    // the head; for chains the finish computes its second layer (the logits of each
+    // sequence's mismatches) itself, and the GEMM's workgroups derive the mismatch list
+    // (or read the decide kernel's) and run on the M listed rows only
+    const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
+    const bool fuse_head = head && !c.is_tree;
+    HeadArgs ha{};
+    if (head) {
+        ha.hidden = c.hidden;
+        ha.n_rows = hidden_rows;
+        ha.row0 = hidden_row0;
+        ha.slots = static_cast<int32_t>(c.D);
+        ha.list = list;
+        ha.count_dev = count;
+        ha.count_host = 0;
+        ha.m_cap = m_cap;
+        ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2; ha.b2 = c.head->b2;
+        ha.d = c.head->d; ha.h = c.head->h;
+        ha.ksplit = ksplit_for(m_cap, c.head);
+        // Trees mismatch most of their slots (about 60% on the 64-tree batch: 304
+        // workgroups at 8 k-slices), more than one workgroup per CU: the shallow ring
+        // lets two share a CU and finish in one round (19.9 -> 13.8 us there).
+        ha.two_per_cu = c.is_tree;
+        ha.upart = upart;
+        ha.z = zlog;
+        if (!c.is_tree) {           // chains: persistent GEMM, partials by decision slot
+            const int64_t nt = (ha.h + kHeadTileN - 1) / kHeadTileN;
+            const int64_t items = (m_cap + kHeadTileM - 1) / kHeadTileM * nt * ha.ksplit;
+            const int64_t slots = head_gemm_slots(static_cast<Dtype>(c.head->dtype), build_list);
+            ha.grid = static_cast<int32_t>(items < slots ? items : slots);
+            ha.out_by_slot = 1;
+            ha.build_list = build_list;
+            ha.partials = partials;
+            ha.plan = plan;
+            ha.tokens = c.tokens;
+            ha.cand = cand_in_ws ? tgt_arg : nullptr;
+            ha.K = static_cast<int32_t>(c.D);
+            ha.V = c.V;
+        }
+    }
 
     if (do_reduce) {
         DecideArgs da{};
@@ -283,6 +333,11 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ra.reset_counter = count;
         ra.seg = uniform ? seg : nullptr;
         ra.nseg = static_cast<int32_t>(n_segments(c.V, eb));
+        if (!c.is_tree) {           // the logit at each row's token, for the chain finish
+            ra.chain_tokens = c.tokens;
+            ra.K = static_cast<int32_t>(c.D);
+            ra.xtok = xtok;
+        }
 
         if (!record(c.opts ? c.opts->reduce_begin : nullptr)) return COSPEC_ERR_HIP;
         if (launch_reduce(dt, ra, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
@@ -307,34 +362,17 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
             sa.cand = tgt_arg;
             if (launch_sample(dt, sa, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
         }
-        if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        // the decision step: its own kernel for trees and for the first phase of a split
+        // step (whose outputs, the candidates, the caller needs before phase 2); in a
+        // whole chain step the finish takes it, and the head GEMM derives its list
+        // itself, unless the batch has more decision slots than the GEMM's workgroups
+        // list (then this kernel builds the list the GEMM reads)
+        if (c.is_tree || phase == kReducePhase || (head && !build_list)) {
+            if (launch_decide(dt, da, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        }
     }
     if (!do_arbitrate) return COSPEC_OK;
-
-    // the head; for chains the finish computes its second layer (the logits of each
-    // sequence's mismatches) itself
-    const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
-    const bool fuse_head = head && !c.is_tree;
-    HeadArgs ha{};
     if (head) {
-        ha.hidden = c.hidden;
-        ha.n_rows = hidden_rows;
-        ha.row0 = hidden_row0;
-        ha.slots = static_cast<int32_t>(c.D);
-        ha.list = list;
-        ha.count_dev = count;
-        ha.count_host = 0;
-        ha.m_cap = m_cap;
-        ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2; ha.b2 = c.head->b2;
-        ha.d = c.head->d; ha.h = c.head->h;
-        ha.ksplit = ksplit_for(m_cap, c.head);
-        // Trees mismatch most of their slots (about 60% on the 64-tree batch: 304
-        // workgroups at 8 k-slices), more than one workgroup per CU: the shallow ring
-        // lets two share a CU and finish in one round (19.9 -> 13.8 us there).  The
-        // chain batches measured fill the CUs once, where the deep ring is 0.9 us faster.
-        ha.two_per_cu = c.is_tree;
-        ha.upart = upart;
-        ha.z = zlog;
         const Dtype hdt = static_cast<Dtype>(c.head->dtype);
         if ((fuse_head ? launch_head_gemm(hdt, ha, c.stream) : launch_head(hdt, ha, c.stream)) != hipSuccess)
             return COSPEC_ERR_HIP;
@@ -370,6 +408,12 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     fa.fuse_head = fuse_head;
     fa.head_dt = head ? c.head->dtype : 0;
     fa.hd = ha;
+    fa.hd.list = nullptr;           // the finish reads the GEMM's partials by decision slot
+    fa.ws_xtok = xtok;
+    fa.sampled = cand_in_ws;
+    fa.tgt_argmax = F.tgt_argmax; fa.tgt_max = F.tgt_max; fa.tgt_lse = F.tgt_lse; fa.tgt_ent = F.tgt_entropy;
+    fa.tgt_cand = F.tgt_candidate;
+    fa.delta = F.delta; fa.logp_tgt = F.logp_tgt;
     if (rl) {
         fa.rl_on = 1;
         fa.rl_correct = rl->correct; fa.rl_alpha = rl->alpha; fa.rl_beta = rl->beta;

@@ -87,6 +87,12 @@ struct ReduceArgs {
     float2 *seg;               // [n_tgt_rows][nseg] {mass, reference} of each segment of a
                                // target row, or null; needs vec_per_split % kSegVecs == 0
     int32_t nseg;              // segments per row: ceil(vectors / kSegVecs) + (tail ? 1 : 0)
+    // chains, or null: xtok[row] = the row's logit at its draft token (target row
+    // b*(K+1)+i and draft row b*K+i: token b*K+i; target row b*(K+1)+K: none), stored
+    // by the piece whose range holds it, when the token is in [0, V)
+    const int32_t *chain_tokens;
+    int32_t K;
+    float *xtok;
 };
 
 // Temperature-1 candidates: one wave per target row inverts its uniform through
@@ -112,17 +118,38 @@ struct HeadArgs {
     const int64_t *row0;       // packed hidden states: entry e of the list reads row
                                // row0[e / slots] + e % slots, or null (row e)
     int32_t slots;
-    const int32_t *count_dev;  // M on the device, or null
+    int32_t *count_dev;        // M on the device, or null (the persistent GEMM that builds
+                               // its list stores M there, for the second layer)
     int64_t count_host;        // M when count_dev is null
     int64_t m_cap;             // capacity of the list (rows of upart and z)
     const void *w1; const void *b1; const void *w2;
     float b2;
     int32_t d, h;
-    int32_t ksplit;            // slices of d, one workgroup each (head_ksplit)
+    int32_t ksplit;            // slices of d, one workgroup each (head_ksplit); the
+                               // persistent form may use fewer (headz::live_ksplit)
+    int32_t grid;              // chains: workgroups of the persistent GEMM (at most one per
+                               // resident slot); 0: one workgroup per (tile, k-slice)
     int32_t two_per_cu;        // use the shallow LDS ring: two workgroups fit on a CU
     float *upart;              // [ksplit][m_cap][h] partial pre-activations
     float *z;                  // [m_cap] head logits of the selected rows
+    // chains: upart row of a selected row = its decision slot b*K + i (the list entry),
+    // not its list position, so that the finish finds it without the list
+    int32_t out_by_slot;
+    // chains: the list is derived in every workgroup from the reduction's partials
+    // instead of read: the decision slots b*K + i (i < K, m_cap = B*K of them) whose
+    // valid draft token differs from the candidate of target row b*(K+1) + i, in slot
+    // order, M of them
+    int32_t build_list;
+    const float4 *partials;
+    PartPlan plan;
+    const int32_t *tokens;     // [B][K] draft tokens
+    const int32_t *cand;       // [B][K+1] candidates already taken (temperature-1 samples, or
+                               // a split step's first phase), or null: the argmax
+    int32_t K, V;
 };
+
+// build_list: at most this many decision slots (eight per thread of a GEMM workgroup)
+constexpr int kBuildListMax = 4096;
 
 // Finish: draft-row statistics, log p_D, verdicts, first stop, emission.
 struct FinishArgs {
@@ -151,6 +178,15 @@ struct FinishArgs {
     float *logp_action;
     const int32_t *ws_tgt_arg;
     int32_t *accept_len; int32_t *out_tokens; int32_t *out_path;
+    // chains: the decision step is taken in the finish (lane j merges target row j, the
+    // row that verifies decision j+1); `sampled`: take the candidates from ws_tgt_arg
+    // (temperature-1 samples, or what a split step's first phase stored) instead of the
+    // merged argmax; ws_xtok: the logit at each row's token, which the reduction
+    // stored (ReduceArgs::xtok)
+    const float *ws_xtok;
+    int32_t sampled;
+    int32_t *tgt_argmax; float *tgt_max; float *tgt_lse; float *tgt_ent; int32_t *tgt_cand;
+    uint8_t *delta; float *logp_tgt;
     int32_t *drf_argmax; float *drf_max; float *drf_lse; float *drf_ent; float *logp_drf;
     float *z_tilde; float *policy; uint8_t *accept;
     // chain only: the head's second layer is computed here from its k-slice partials
@@ -207,7 +243,9 @@ hipError_t launch_sample(Dtype dt, const SampleArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
-hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM only
+hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s);
+// Resident workgroups of the persistent head GEMM on the current device (cached).
+int32_t head_gemm_slots(Dtype dt, bool build);   // GEMM only
 hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);
 hipError_t launch_arb_finish(const ArbFinishArgs &a, hipStream_t s);
 hipError_t launch_sps(Dtype dt, const SpsArgs &a, hipStream_t s);   // finish, weights, pick

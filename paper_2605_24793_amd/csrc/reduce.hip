@@ -579,8 +579,33 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
     const int nvec = static_cast<int>((static_cast<int64_t>(a.V) * E::kBytes) / 16);
     const int v0 = split * a.vec_per_split;
     const int v1 = min(v0 + a.vec_per_split, nvec);
+    // chains: the row's logit at its draft token, read by the piece whose range holds
+    // it (the tail past the last whole vector belongs to the last split); the read is
+    // issued before the streaming and kept until its end
+    bool own = false;
+    float xt = 0.f;
+    if (a.xtok && threadIdx.x == 0) {
+        int tok = -1;
+        const char *base;
+        if (row < a.n_tgt_rows) {
+            const int b = row / (a.K + 1), i = row - b * (a.K + 1);
+            if (i < a.K) tok = a.chain_tokens[static_cast<int64_t>(b) * a.K + i];
+            base = a.tgt + static_cast<int64_t>(row) * a.ld_bytes;
+        } else {
+            tok = a.chain_tokens[row - a.n_tgt_rows];
+            base = a.drf + static_cast<int64_t>(row - a.n_tgt_rows) * a.ld_bytes;
+        }
+        if (tok >= 0 && tok < a.V) {
+            const int tv = tok / E::kPerVec;
+            own = tv < nvec ? (tv >= v0 && tv < v1) : split == splits - 1;
+            if (own) xt = E::at(base, tok);
+        }
+    }
     const float4 part = reduce_piece<DT, SEG>(a, row, v0, v1, split == splits - 1);
-    if (threadIdx.x == 0) a.partials[u] = part;
+    if (threadIdx.x == 0) {
+        a.partials[u] = part;
+        if (own) a.xtok[row] = xt;
+    }
 }
 
 template <int DT>

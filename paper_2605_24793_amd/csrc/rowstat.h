@@ -65,7 +65,8 @@ struct RowStat {
 // kernels that inline it (decide, finish, sampling) give bit-identical statistics for
 // the same partials, whether they read them from global memory or LDS.  The
 // partials are read kMergeChunk at a time, every read of a chunk issued before the
-// first is used; the arithmetic runs over s = 0, 1, ... in order.
+// first is used (unconditionally: the index is clamped, the arithmetic skips what is
+// past the end); the arithmetic runs over s = 0, 1, ... in order.
 constexpr int kMergeChunk = 8;
 
 typedef __attribute__((address_space(3))) const float lds_float;
@@ -90,8 +91,7 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
         float4 q[kMergeChunk];
         for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
 #pragma unroll
-            for (int i = 0; i < kMergeChunk; ++i)
-                if (s0 + i < splits) q[i] = ld(s0 + i);
+            for (int i = 0; i < kMergeChunk; ++i) q[i] = ld(min(s0 + i, splits - 1));   // unconditional
 #pragma unroll
             for (int i = 0; i < kMergeChunk; ++i)   // earlier split wins ties
                 if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
@@ -100,8 +100,7 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
         for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
             if (splits > kMergeChunk) {              // else the chunk is still in registers
 #pragma unroll
-                for (int i = 0; i < kMergeChunk; ++i)
-                    if (s0 + i < splits) q[i] = ld(s0 + i);
+                for (int i = 0; i < kMergeChunk; ++i) q[i] = ld(min(s0 + i, splits - 1));
             }
 #pragma unroll
             for (int i = 0; i < kMergeChunk; ++i) {
@@ -128,6 +127,30 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
     return r;
 }
 
+// The candidate merge_row takes (its .arg) from the partials' maxima alone: the first
+// split, in split order, with S > 0 and the strictly largest maximum (a single split:
+// S > 0 alone, as in merge_row); INT_MAX when none is taken.  One loop, every load
+// unconditional (the index clamped) and no branch on the split count, so a caller that
+// needs only the argmax issues these loads together with its others.
+__device__ inline int merge_arg(const float4 *p, int splits) {
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+    float M = -INFINITY;
+    int arg = INT_MAX;
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+        u32x4 c[kMergeChunk];
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i) c[i] = q[min(s0 + i, splits - 1)];
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i) {
+            const float x = __uint_as_float(c[i].x);
+            const bool take = (s0 + i < splits) & (__uint_as_float(c[i].z) > 0.f) & ((x > M) | (splits == 1));
+            M = take ? x : M;
+            arg = take ? static_cast<int>(c[i].y) : arg;
+        }
+    }
+    return arg;
+}
+
 // A row's partials in global memory.
 __device__ inline RowStat merge_row(const float4 *p, int splits) {
     return merge_row_t([p](int s) { return p[s]; }, splits);
@@ -147,9 +170,23 @@ __device__ inline RowStat merge_row_lds(const float4 *p, int splits) {
 constexpr int kStageParts = 1024;
 
 // Copies n partials from p into stage with the threads [first, first + count) of the
-// caller (each copies every count-th); the caller synchronises before reading them.
+// caller (each copies every count-th, eight loads issued before the first write); the
+// caller synchronises before reading them.
 __device__ inline void stage_partials(const float4 *p, int64_t n, float4 *stage, int idx, int count) {
-    for (int64_t i = idx; i < n; i += count) stage[i] = p[i];
+    constexpr int kBatch = 8;
+    for (int64_t i0 = idx; i0 < n; i0 += kBatch * static_cast<int64_t>(count)) {
+        float4 v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * static_cast<int64_t>(count);
+            v[j] = p[i < n ? i : n - 1];                // unconditional: clamped
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * static_cast<int64_t>(count);
+            if (i < n) stage[i] = v[j];
+        }
+    }
 }
 
 }  // namespace cospec

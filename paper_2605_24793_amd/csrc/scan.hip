@@ -6,7 +6,8 @@
 // rows' partials are merged here.
 //
 // Chain (Section 3.3, Eq. cospec_length): one wave per sequence, lane i-1 owns
-// decision i and draft row i-1.  A matched decision passes (z_tilde = +inf,
+// decision i, target row i-1 and draft row i-1; it takes the decision step itself
+// (the candidate of target row i-1, Delta, log-probabilities).  A matched decision passes (z_tilde = +inf,
 // Eq. policy-prob); a mismatch passes when sigma(z) > lambda (Eq. infer_thre),
 // or, with sampled arbitration, when its uniform is below sigma(z).
 // The first failing decision is the lowest set bit of a wave ballot, s = its
@@ -40,17 +41,16 @@ struct Verdict {
 // log sigma(x) without overflow for either sign of x.
 __device__ inline float log_sigmoid(float x) { return fminf(x, 0.f) - log1pf(expf(-fabsf(x))); }
 
-// Verdict of one decision slot from its decide state and its head logit z (read
-// only when the head ran and the slot is in its list, pos >= 0): the threshold
-// (Eq. infer_thre), or with uniforms a sampled action (u < pi).
-__device__ inline Verdict verdict(uint8_t state, int pos, float z, int head_ran, float lambda,
-                                  const float *pu, int64_t di) {
+// Verdict of one decision slot from its state and its head logit z (read only when
+// the head scored the slot): the threshold (Eq. infer_thre), or with uniforms a
+// sampled action (u < pi).
+__device__ inline Verdict verdict(uint8_t state, bool scored, float z, float lambda, const float *pu, int64_t di) {
     Verdict v;
     if (state == kStateMatch) {
         v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f; v.logp_action = 0.0f;
     } else if (state != kStateMismatch) {          // invalid token or parent: always rejected
         v.pass = false; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
-    } else if (!head_ran || pos < 0) {
+    } else if (!scored) {
         // head skipped: lambda >= 1 or lambda < 0 decides every mismatch by itself
         v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
     } else {
@@ -70,52 +70,103 @@ __device__ inline void write_drf(const FinishArgs &a, int64_t r, const RowStat &
 }
 
 // The chain finish of sequence b by one wave, lane i-1 owning decision i, in two
-// parts: what needs no head logit (the loads, the draft-row statistics), then the
-// verdicts, the stop, the emission and the RL statistics.
+// parts: the decision step and what needs no head logit (the loads, the target- and
+// draft-row statistics, Delta, log-probabilities), then the verdicts, the stop, the
+// emission and the RL statistics.
 struct ChainLane {
     uint8_t st;
-    int pos;          // list position of the decision, -1 if not in the head's list
+    bool scored;      // a mismatch the head scored
     float lpt;        // log p_T of the draft token
     int tok_d, tok_t; // draft token of slot `lane`, target candidate of row `lane`
+    int tok_k;        // K = 64 only, in lane 0: the candidate of target row K (no lane of its own)
 };
 
-// stage: LDS room for `cap` partials of this wave, into which the sequence's draft-row
-// partials are copied first when the rows are split (and they fit).
+// Merged statistics of target row tr: its candidate (the argmax, or the candidate
+// already taken when `sampled`) and the optional per-row features.
+__device__ inline int tgt_row(const FinishArgs &a, int64_t tr, const RowStat &ts) {
+    const int cand = a.sampled ? a.ws_tgt_arg[tr] : ts.arg;
+    if (a.tgt_cand) a.tgt_cand[tr] = cand;
+    if (a.tgt_argmax) a.tgt_argmax[tr] = ts.arg;
+    if (a.tgt_max) a.tgt_max[tr] = ts.max;
+    if (a.tgt_lse) a.tgt_lse[tr] = ts.lse;
+    if (a.tgt_ent) a.tgt_ent[tr] = ts.ent;
+    return cand;
+}
+
+// The decision step of one chain by one wave (Section 3.1): lane j merges target row
+// j in fixed split order (its argmax, ties to the lowest index, is the verification
+// candidate of decision j+1, or of the bonus token for j = K; at temperature 1 the
+// sample k_sample left, in a split step's second phase the first phase's choice) and
+// draft row j; decision j+1 is a match when its draft token
+// equals that candidate; log p_T and log p_D of the draft token come from the same
+// rows (Section 3.4).  stage: LDS room for `cap` partials of this wave, into which the
+// sequence's partials are copied first when the rows are split (and they fit).
 template <int DT>
 __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, float4 *stage, int cap) {
-    using E = Elt<DT>;
     const int K = a.D;
-    const int64_t di = static_cast<int64_t>(b) * K + lane;  // decision lane+1, draft row lane
-    // the sequence's draft-row partials are consecutive slots
+    const int64_t di = static_cast<int64_t>(b) * K + lane;       // decision lane+1, draft row lane
+    const int64_t t0 = static_cast<int64_t>(b) * (K + 1);        // the sequence's first target row
+    const int64_t tr = t0 + lane;                                 // target row `lane`
     const PartPlan &plan = a.plan;
-    const int64_t r0 = plan.n_tgt_rows + static_cast<int64_t>(b) * K;
-    const RowParts sp = K > 0 ? rows_parts(plan, r0, r0 + K) : RowParts{0, 0};
-    const float4 *seq_parts = a.partials + sp.first;
-    const bool staged = sp.count > K && sp.count <= cap;
+    const int64_t d0 = plan.n_tgt_rows + static_cast<int64_t>(b) * K;
+    // the target rows' partials, then the draft rows' (consecutive slots each)
+    const RowParts tp = rows_parts(plan, t0, t0 + K + 1);
+    const RowParts dp = K > 0 ? rows_parts(plan, d0, d0 + K) : RowParts{0, 0};
+    const bool staged = plan.splits > 1 && tp.count + dp.count <= cap;
+    int tok = -1;
+    if (lane < K) tok = a.tokens[di];
     if (staged) {                 // one wave writes and then reads: LDS keeps the wave's order
-        stage_partials(seq_parts, sp.count, stage, lane, 64);
+        stage_partials(a.partials + tp.first, tp.count, stage, lane, 64);
+        stage_partials(a.partials + dp.first, dp.count, stage + tp.count, lane, 64);
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
         __builtin_amdgcn_wave_barrier();
     }
-    ChainLane c{kStateMatch, -1, NAN, -1, -1};
-    if (lane < K) {
-        c.st = a.ws_state[di];
-        const bool valid = c.st != kStateReject;
-        c.tok_d = a.tokens[di];
-        const float xd = valid ? E::at(a.drf + di * a.ld_bytes, c.tok_d) : 0.f;
-        const RowParts rp = row_parts(plan, r0 + lane);
-        const RowStat rs = staged ? merge_row_lds(stage + (rp.first - sp.first), rp.count)
-                                  : merge_row(a.partials + rp.first, rp.count);
-        write_drf(a, di, rs);
-        if (a.logp_drf) a.logp_drf[di] = valid ? (xd - rs.max) - rs.log_s : NAN;
-        c.pos = a.ws_listpos[di];
-        c.lpt = a.ws_logp_tgt[di];
+    // one split per row: each row's only partial is read together with the token and
+    // the logits at it, then the merges, which wait for nothing
+    const bool one = plan.splits == 1;
+    float4 qt{}, qd{}, qk{};
+    if (one) {
+        if (lane <= K) qt = a.partials[tr];
+        if (lane < K) qd = a.partials[d0 + lane];
+        if (K >= 64 && lane == 0) qk = a.partials[t0 + K];
     }
-    if (lane <= K) c.tok_t = a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + lane];
+    // the logits at the draft token, which the reduction stored (read whatever the
+    // token; used only when it is valid)
+    const bool valid = tok >= 0 && tok < a.V;
+    float xt = 0.f, xd = 0.f;
+    if (lane < K) {
+        xt = a.ws_xtok[tr];
+        xd = a.ws_xtok[d0 + lane];
+    }
+    // merged statistics of row r (target rows first in the stage, then draft rows)
+    auto merged = [&](int64_t r, const float4 &q, const RowParts &seq, int64_t stage_off) -> RowStat {
+        if (one) return merge_row_t([q](int) { return q; }, 1);
+        const RowParts rp = row_parts(plan, r);
+        return staged ? merge_row_lds(stage + stage_off + (rp.first - seq.first), rp.count)
+                      : merge_row(a.partials + rp.first, rp.count);
+    };
+    ChainLane c{kStateMatch, false, NAN, -1, -1, -1};
+    if (K >= 64 && lane == 0) c.tok_k = tgt_row(a, t0 + K, merged(t0 + K, qk, tp, 0));
+    if (lane <= K) {
+        const RowStat ts = merged(tr, qt, tp, 0);
+        const int cand = tgt_row(a, tr, ts);
+        c.tok_t = cand;
+        if (lane < K) {
+            const RowStat ds = merged(d0 + lane, qd, dp, tp.count);
+            write_drf(a, di, ds);
+            c.tok_d = tok;
+            c.st = !valid ? kStateReject : tok == cand ? kStateMatch : kStateMismatch;
+            c.lpt = valid ? (xt - ts.max) - ts.log_s : NAN;
+            c.scored = a.head_ran && c.st == kStateMismatch;
+            if (a.delta) a.delta[di] = c.st == kStateMatch;
+            if (a.logp_tgt) a.logp_tgt[di] = c.lpt;
+            if (a.logp_drf) a.logp_drf[di] = valid ? (xd - ds.max) - ds.log_s : NAN;
+        }
+    }
     return c;
 }
 
-// z: the head logit of the lane's decision (read only when it is in the list).
+// z: the head logit of the lane's decision (read only when the head scored it).
 __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const ChainLane &c, float z) {
     const int K = a.D;
     const int64_t di = static_cast<int64_t>(b) * K + lane;
@@ -123,7 +174,7 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
     const bool mism = lane < K && c.st != kStateMatch;
     const float lpt = c.lpt;
     if (lane < K) {
-        const Verdict v = verdict(c.st, c.pos, z, a.head_ran, a.lambda, a.policy_u, di);
+        const Verdict v = verdict(c.st, c.scored, z, a.lambda, a.policy_u, di);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
         if (a.policy) a.policy[di] = v.policy;
@@ -133,10 +184,11 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
     const uint64_t rej = __ballot(fail);
     const int s = rej ? __builtin_ctzll(rej) + 1 : K + 1;
     if (lane == 0) a.accept_len[b] = s;
-    // slot j emits draft token j+1 before the stop, the target's token at it
+    // slot j emits draft token j+1 before the stop, the target's token at it (j = K
+    // = 64 is lane 0's second slot: no draft token, the bonus row's candidate)
     for (int j = lane; j <= K; j += 64) {
-        const int td = j == lane ? c.tok_d : (j < K ? a.tokens[static_cast<int64_t>(b) * K + j] : -1);
-        const int tt = j == lane ? c.tok_t : a.ws_tgt_arg[static_cast<int64_t>(b) * (K + 1) + j];
+        const int td = j == lane ? c.tok_d : -1;
+        const int tt = j == lane ? c.tok_t : c.tok_k;
         a.out_tokens[static_cast<int64_t>(b) * (K + 1) + j] = j < s - 1 ? td : j == s - 1 ? tt : -1;
     }
     if (!a.rl_on) return;
@@ -166,28 +218,23 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
     }
 }
 
-// zd: the sequence's head logits by decision slot (computed by the calling kernel),
-// or null to read them from a.z by list position.
-template <int DT>
-__device__ inline void chain_finish_wave(const FinishArgs &a, int b, int lane, const float *zd, float4 *stage,
-                                         int cap) {
-    const ChainLane c = chain_prefix<DT>(a, b, lane, stage, cap);
-    const float z = lane >= a.D || !a.head_ran || c.pos < 0 ? NAN : zd ? zd[lane] : a.z[c.pos];
-    chain_suffix(a, b, lane, c, z);
-}
-
 template <int DT>
 __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
     constexpr int kCap = kStageParts / 4;
     __shared__ float4 s_parts[4][kCap];
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= a.B) return;                                  // whole wave leaves together
-    chain_finish_wave<DT>(a, b, threadIdx.x & 63, nullptr, s_parts[threadIdx.x >> 6], kCap);
+    const int lane = threadIdx.x & 63;
+    const ChainLane c = chain_prefix<DT>(a, b, lane, s_parts[threadIdx.x >> 6], kCap);
+    chain_suffix(a, b, lane, c, NAN);                      // the head did not run
 }
 
-// One workgroup per sequence: wave 0 issues the finish's loads while waves
-// 1, 2, ... compute the head logits of the decision slots in the head's list (slot
-// t by wave 1 + t mod (waves - 1)); then wave 0 finishes the sequence.
+// One workgroup per sequence: wave 0 takes the decision step while waves 1, 2, ...
+// compute the head logits of the slots the head scored (slot t by wave
+// 1 + t mod (waves - 1)) from the GEMM's k-slice partials, stored by decision slot;
+// then wave 0 finishes the sequence.  A head wave finds out by itself whether its slot
+// was scored (its token against the candidate of its target row, merged as wave 0
+// merges it), so that its loads wait for no other wave.
 constexpr int kFinishWaves = 8;
 template <int DT>
 __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishArgs a) {
@@ -195,21 +242,32 @@ __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishA
     __shared__ float4 s_parts[kStageParts];
     const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int waves = blockDim.x >> 6;                     // >= 2
+    const int K = a.D;
     ChainLane c{};
     if (wave == 0) {
         c = chain_prefix<DT>(a, b, lane, s_parts, kStageParts);
     } else {
-        for (int t = wave - 1; t < a.D; t += waves - 1) {
-            const int pos = a.ws_listpos[static_cast<int64_t>(b) * a.D + t];   // wave-uniform
-            if (pos >= 0) {
-                const float z = a.head_dt == kBF16 ? headz::head_z<kBF16>(a.hd, pos, lane)
-                                                   : headz::head_z<kF32>(a.hd, pos, lane);
+        const int64_t M = *a.hd.count_dev;                 // rows the GEMM ran on
+        for (int t = wave - 1; t < K; t += waves - 1) {    // wave-uniform
+            const int64_t di = static_cast<int64_t>(b) * K + t;
+            const int64_t tr = static_cast<int64_t>(b) * (K + 1) + t;
+            // both candidate sources are read (the workspace always holds ws_tgt_arg) and
+            // one is chosen: no branch for the loads to wait at
+            const int tok = a.tokens[di];
+            const int taken = a.ws_tgt_arg[tr];
+            const RowParts rp = row_parts(a.plan, tr);
+            const int am = merge_arg(a.partials + rp.first, rp.count);
+            const int cand = a.sampled ? taken : am;
+            if (a.head_ran && tok >= 0 && tok < a.V && tok != cand) {
+                const int ksl = headz::live_ksplit(a.hd, M);
+                const float z = a.head_dt == kBF16 ? headz::head_z<kBF16>(a.hd, di, lane, ksl)
+                                                   : headz::head_z<kF32>(a.hd, di, lane, ksl);
                 if (lane == 0) s_z[t] = z;
             }
         }
     }
     __syncthreads();
-    if (wave == 0) chain_suffix(a, b, lane, c, lane < a.D && c.pos >= 0 ? s_z[lane] : NAN);
+    if (wave == 0) chain_suffix(a, b, lane, c, lane < K && c.scored ? s_z[lane] : NAN);
 }
 
 template <int DT>
@@ -262,8 +320,8 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
     int anc = -1, dep = 0, ok = 1;
     if (n < N) {
         const int pos = a.ws_listpos[base + n];
-        const float z = !a.head_ran || pos < 0 ? NAN : a.z[pos];
-        const Verdict v = verdict(st, pos, z, a.head_ran, a.lambda, a.policy_u, base + n);
+        const bool scored = a.head_ran && pos >= 0;
+        const Verdict v = verdict(st, scored, scored ? a.z[pos] : NAN, a.lambda, a.policy_u, base + n);
         if (n > 0) {
             anc = par;
             dep = 1;

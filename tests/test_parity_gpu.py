@@ -186,6 +186,9 @@ FUZZ = [
     # vocabularies far past the workloads' (2 MiB and 4 MiB rows, ragged tails)
     (2, 3, 1048583, "bf16", 0, 0, 0.5, 4.0, 1.0),
     (1, 2, 1048577, "f32", 3, 0, 0.5, 4.0, 1.0),
+    # more decision slots (600 x 8) than the head GEMM's workgroups list themselves:
+    # the decide kernel builds the list
+    (600, 8, 257, "bf16", 0, 0, 0.5, 4.0, 1.0),
 ]
 
 
@@ -481,6 +484,9 @@ T1_FUZZ = [
     (2, 3, 1, "bf16", 0, 0), (3, 2, 7, "f32", 4, 0), (2, 4, 9, "bf16", 0, 3),
     (4, 5, 4095, "bf16", 8, 3), (5, 6, 4097, "f32", 0, 7), (3, 7, 32001, "bf16", 24, 0),
     (2, 9, 50001, "f32", 0, 64), (40, 3, 513, "bf16", 0, 0), (2, 3, 151936, "bf16", 0, 13),
+    # one split per row over 2 MiB and 4 MiB rows: the segment masses are written
+    # without staging
+    (2, 3, 1048583, "bf16", 0, 1), (1, 2, 1048577, "f32", 3, 1),
 ]
 
 
