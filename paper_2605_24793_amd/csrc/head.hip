@@ -38,6 +38,30 @@
 namespace cospec {
 namespace {
 
+typedef __attribute__((address_space(3))) char lds_char;
+
+// Sixteen zero bytes in device memory: the operand loads past the end of d read them.
+__device__ __attribute__((aligned(16))) const uint32_t kZeroVec[4] = {0, 0, 0, 0};
+
+// Loads 16 bytes per lane from global memory straight into LDS, lane l's at byte
+// lds + 16*l (lds is the wave's base, the same in every lane).  Written as assembly:
+// the compiler cannot tell the ring slots apart, and for its own form of this load it
+// makes every later LDS read wait until the load has landed, which would stall each
+// stage for a full memory round trip.  The GEMM's own vmcnt waits order these loads.
+// M0 is declared clobbered; the compiler reserves it and nothing else in this file's
+// kernels uses it (their assembly sets M0 only here), so no value of its is lost.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ inline void load_lds16(const void *g, const char *lds) {
+    const uint32_t base =
+        __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_char *)lds)));
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(base), "v"(g)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float floatx4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -65,7 +89,6 @@ template <> __device__ inline floatx4 mma<kF32>(u32x4 a, u32x4 b, floatx4 c) {
     return c;
 }
 
-typedef __attribute__((address_space(3))) char lds_char;
 
 // Waits until at most N vector-memory operations of this wave are outstanding.
 template <int N> __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
@@ -95,125 +118,91 @@ constexpr int kGemmThreads = 64 * kGemmWaves;
 constexpr int kBuildPer = kBuildListMax / kGemmThreads;   // slots per thread in the scan
 static_assert(kBuildPer == 8 && kBuildPer * kGemmThreads == kBuildListMax, "build_list: 8 slots per thread");
 
-// Lane exchanges of build_list's combine, all in the VALU: DPP inside rows of 16 lanes,
-// the gfx950 permlane swaps across rows.  The combine (larger maximum, then the earlier
-// split) is commutative and associative, so pairing lanes by mirrors instead of xor
-// masks reduces every group of G = 2, 4, ..., 64 lanes all the same.
-constexpr int kDppXor1 = 0xB1;     // quad_perm [1,0,3,2]
-constexpr int kDppXor2 = 0x4E;     // quad_perm [2,3,0,1]
-constexpr int kDppMirror8 = 0x141; // row_half_mirror: lane i <-> 7 - i within 8
-constexpr int kDppMirror16 = 0x140;// row_mirror:      lane i <-> 15 - i within 16
-
-struct ArgPick {
-    float x;    // the largest maximum so far (-inf: none)
-    int s;      // its split (INT_MAX: none)
-    int c;      // its argmax
-};
-
-__device__ inline ArgPick better(const ArgPick &p, const ArgPick &q) {
-    const bool t = (q.x > p.x) | ((q.x == p.x) & (q.s < p.s));
-    return ArgPick{t ? q.x : p.x, t ? q.s : p.s, t ? q.c : p.c};
-}
-
-template <int CTRL>
-__device__ inline int dpp_int(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
-}
-
-template <int CTRL>
-__device__ inline ArgPick combine_dpp(const ArgPick &p) {
-    const ArgPick q{__int_as_float(dpp_int<CTRL>(__float_as_int(p.x))), dpp_int<CTRL>(p.s), dpp_int<CTRL>(p.c)};
-    return better(p, q);
-}
-
-// Lane l combined with lane l ^ 16 (ROW32 false) or l ^ 32 (true): each swap returns
-// the pair (own, partner) in some order, and the combine is symmetric in it.
-template <bool ROW32>
-__device__ inline ArgPick combine_swap(const ArgPick &p) {
-    auto sw = [](int v) {
-        const auto r = ROW32 ? __builtin_amdgcn_permlane32_swap(v, v, false, false)
-                             : __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return r;
-    };
-    const auto x = sw(__float_as_int(p.x)), s = sw(p.s), c = sw(p.c);
-    return better(ArgPick{__int_as_float(static_cast<int>(x[0])), static_cast<int>(s[0]), static_cast<int>(c[0])},
-                  ArgPick{__int_as_float(static_cast<int>(x[1])), static_cast<int>(s[1]), static_cast<int>(c[1])});
-}
-
-// Part 1 of build_list for one batch of NB (slot, split) items per thread: item
-// i = base + j * kGemmThreads + tid is split (i mod G) of slot i / G.
+// Part 1 of build_list, rows of one split (or candidates already taken): NB slots per
+// thread, slot base + j * kGemmThreads + tid, every load issued before the first use,
+// unconditionally (slots past the end read slot 0 and are dropped).
 template <bool CAND, int NB>
-__device__ inline void mark_batch(const HeadArgs &a, int base, int n, int lg, int splits, uint64_t kmag,
-                                  uint8_t *s_need) {
+__device__ inline void mark_single(const HeadArgs &a, int base, int n, uint64_t kmag, uint8_t *s_need) {
     const int tid = threadIdx.x;
-    const int G = 1 << lg;
-    int tok[NB], r[NB];
-    ArgPick p[NB];
+    int tok[NB], r[NB], cand[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         const int i = base + j * kGemmThreads + tid;
-        const int di = (i >> lg) < n ? (i >> lg) : 0;      // past the end: slot 0, dropped
+        const int di = i < n ? i : 0;
         r[j] = di + static_cast<int>((static_cast<uint64_t>(di) * kmag) >> 32);   // b*(K+1) + i
     }
-    // every load of the batch first, unconditionally, so that none waits for another
     if constexpr (CAND) {
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int i = base + j * kGemmThreads + tid;
-            tok[j] = a.tokens[(i >> lg) < n ? (i >> lg) : 0];
-            p[j] = ArgPick{-INFINITY, INT_MAX, a.cand[r[j]]};
+            tok[j] = a.tokens[i < n ? i : 0];
+            cand[j] = a.cand[r[j]];
         }
     } else {
         u32x4 q[NB];
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int i = base + j * kGemmThreads + tid;
-            q[j] = *reinterpret_cast<const u32x4 *>(a.partials + (r[j] * splits + min(i & (G - 1), splits - 1)));
-            tok[j] = a.tokens[(i >> lg) < n ? (i >> lg) : 0];
+            q[j] = *reinterpret_cast<const u32x4 *>(a.partials + r[j]);
+            tok[j] = a.tokens[i < n ? i : 0];
         }
+        // the single partial's argmax when S > 0, as merge_row takes it
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            // the split's maximum when it holds one (S > 0) and the lane has a split;
-            // a single split is taken on S > 0 alone, as merge_row takes it
-            const int sub = (base + j * kGemmThreads + tid) & (G - 1);
-            const float qx = __uint_as_float(q[j].x), qs = __uint_as_float(q[j].z);
-            const bool take = (sub < splits) & (qs > 0.f) & ((qx > -INFINITY) | (splits == 1));
-            p[j] = take ? ArgPick{qx, sub, static_cast<int>(q[j].y)} : ArgPick{-INFINITY, INT_MAX, INT_MAX};
-        }
-        // the loads' unused fourth words stay live until here, so their registers are
-        // not reused (which would make the first load wait before the others)
+        for (int j = 0; j < NB; ++j) cand[j] = __uint_as_float(q[j].z) > 0.f ? static_cast<int>(q[j].y) : INT_MAX;
+        // the loads' unused words stay live until here, so their registers are not
+        // reused (which would make the first load wait before the others)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) asm volatile("" ::"v"(q[j].w));
-        if (lg >= 1) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_dpp<kDppXor1>(p[j]);
-        }
-        if (lg >= 2) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_dpp<kDppXor2>(p[j]);
-        }
-        if (lg >= 3) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_dpp<kDppMirror8>(p[j]);
-        }
-        if (lg >= 4) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_dpp<kDppMirror16>(p[j]);
-        }
-        if (lg >= 5) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_swap<false>(p[j]);
-        }
-        if (lg >= 6) {
-#pragma unroll
-            for (int j = 0; j < NB; ++j) p[j] = combine_swap<true>(p[j]);
-        }
+        for (int j = 0; j < NB; ++j) asm volatile("" ::"v"(q[j].x), "v"(q[j].w));
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         const int i = base + j * kGemmThreads + tid;
-        const int di = i >> lg;
-        if (di < n && (i & (G - 1)) == 0) s_need[di] = tok[j] >= 0 && tok[j] < a.V && tok[j] != p[j].c;
+        if (i < n) s_need[i] = tok[j] >= 0 && tok[j] < a.V && tok[j] != cand[j];
+    }
+}
+
+// Part 1 of build_list, split rows: NS slots per thread, each merged by its thread in
+// split order, kMergeChunk partials of every slot loaded at once; the argmax is the one
+// merge_row takes (the first split with S > 0 and the strictly largest maximum).
+template <int NS>
+__device__ inline void mark_split(const HeadArgs &a, int base, int n, int splits, uint64_t kmag, uint8_t *s_need) {
+    const int tid = threadIdx.x;
+    int tok[NS], r[NS], arg[NS];
+    float M[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const int i = base + j * kGemmThreads + tid;
+        const int di = i < n ? i : 0;
+        r[j] = di + static_cast<int>((static_cast<uint64_t>(di) * kmag) >> 32);
+        tok[j] = a.tokens[di];
+        M[j] = -INFINITY;
+        arg[j] = INT_MAX;
+    }
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {       // uniform trip count
+        u32x4 q[NS][kMergeChunk];
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+#pragma unroll
+            for (int k = 0; k < kMergeChunk; ++k)
+                q[j][k] = *reinterpret_cast<const u32x4 *>(a.partials + (r[j] * splits + min(s0 + k, splits - 1)));
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+#pragma unroll
+            for (int k = 0; k < kMergeChunk; ++k) {
+                const float x = __uint_as_float(q[j][k].x);
+                const bool take = (s0 + k < splits) & (__uint_as_float(q[j][k].z) > 0.f) & (x > M[j]);
+                M[j] = take ? x : M[j];
+                arg[j] = take ? static_cast<int>(q[j][k].y) : arg[j];
+            }
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+#pragma unroll
+            for (int k = 0; k < kMergeChunk; ++k) asm volatile("" ::"v"(q[j][k].w));
+    }
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const int i = base + j * kGemmThreads + tid;
+        if (i < n) s_need[i] = tok[j] >= 0 && tok[j] < a.V && tok[j] != arg[j];
     }
 }
 
@@ -224,14 +213,11 @@ __device__ inline void mark_batch(const HeadArgs &a, int base, int n, int lg, in
 // the candidate already taken (a.cand).  Writes the list (kBuildListMax entries of
 // LDS) and returns M, the number of mismatches.
 //
-// Part 1 marks the mismatches in LDS.  The argmax is the one merge_row takes (the
-// first split, in split order, whose maximum is strictly the largest): G lanes
-// (G = splits rounded up to a power of two) take one split each and combine their
-// (max, split) pairs, larger maximum first and the earlier split on ties.  The
-// (slot, split) items are dealt in batches of 4, 8 or 16 per thread (the fewest that
-// cover them), every load of a batch issued before the first is used.  Part 2 numbers
-// the mismatches in slot order: thread t owns slots [kBuildPer*t, kBuildPer*(t+1)), a
-// workgroup-wide exclusive scan gives their positions.
+// Part 1 marks the mismatches in LDS, one thread per slot (several slots per thread
+// when there are more than threads), every load of a batch issued before the first
+// is used.  Part 2 numbers the mismatches in slot order: thread t owns slots
+// [kBuildPer*t, kBuildPer*(t+1)), a workgroup-wide exclusive scan gives their
+// positions.
 template <bool CAND>
 __device__ inline int64_t build_list(const HeadArgs &a, int32_t *list) {
     __shared__ int s_wave[kGemmWaves];
@@ -239,20 +225,17 @@ __device__ inline int64_t build_list(const HeadArgs &a, int32_t *list) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = static_cast<int>(a.m_cap);
     const int splits = CAND ? 1 : a.plan.splits;
-    int lg = 0;
-    while ((1 << lg) < splits) ++lg;                  // G = 2^lg <= 64 lanes per slot
-    const int items = n << lg;
     // floor(di / K) = (di * kmag) >> 32 with kmag = ceil(2^32 / K), exact for every
     // di < 2^16 and K <= 64 (here di < kBuildListMax)
     const uint64_t kmag = ((uint64_t{1} << 32) + static_cast<uint64_t>(a.K) - 1) / static_cast<uint64_t>(a.K);
-    const int per = (items + kGemmThreads - 1) / kGemmThreads;
-    if (per <= 4) {
-        mark_batch<CAND, 4>(a, 0, n, lg, splits, kmag, s_need);
-    } else if (per <= 8) {
-        mark_batch<CAND, 8>(a, 0, n, lg, splits, kmag, s_need);
+    if (splits == 1) {
+        if (n <= 4 * kGemmThreads) mark_single<CAND, 4>(a, 0, n, kmag, s_need);
+        else mark_single<CAND, 8>(a, 0, n, kmag, s_need);          // n <= kBuildListMax
+    } else if (n <= kGemmThreads) {
+        mark_split<1>(a, 0, n, splits, kmag, s_need);
     } else {
-        for (int base = 0; base < items; base += 16 * kGemmThreads)      // uniform trip count
-            mark_batch<CAND, 16>(a, base, n, lg, splits, kmag, s_need);
+        for (int base = 0; base < n; base += 2 * kGemmThreads)      // uniform trip count
+            mark_split<2>(a, base, n, splits, kmag, s_need);
     }
     __syncthreads();
     // part 2: exclusive scan of the per-thread counts, within the wave, then over the waves
@@ -337,6 +320,8 @@ __device__ inline void gemm_tile(const HeadArgs &a, int64_t M, int64_t m_base, i
         if (n >= a.h) n = a.h - 1;
         gb[i] = static_cast<const char *>(a.w1) + static_cast<int64_t>(n) * a.d * EB;
     }
+    // Branch-free: a lane past the ragged end of d (d is a multiple of VE) loads the zero
+    // vector instead, so a stage's loads are one straight run of instructions.
     auto issue = [&](int st) {
         char *slot = ring[st % kRing];
 #pragma unroll
@@ -344,13 +329,11 @@ __device__ inline void gemm_tile(const HeadArgs &a, int64_t M, int64_t m_base, i
             const int e = k0 + st * BK + lvec[i] * VE;          // first element of the vector
             char *la = slot + (wave * 2 + i) * 1024;
             char *lb = slot + kHeadTileM * kStageBytes + (wave * 2 + i) * 1024;
-            if (e < k1) {                                       // d is a multiple of VE
-                __builtin_amdgcn_global_load_lds(ga[i] + static_cast<int64_t>(e) * EB, (lds_char *)la, 16, 0, 0);
-                __builtin_amdgcn_global_load_lds(gb[i] + static_cast<int64_t>(e) * EB, (lds_char *)lb, 16, 0, 0);
-            } else {                                            // ragged end of d: zeros
-                *reinterpret_cast<u32x4 *>(la + lane * 16) = u32x4{0, 0, 0, 0};
-                *reinterpret_cast<u32x4 *>(lb + lane * 16) = u32x4{0, 0, 0, 0};
-            }
+            const bool in = e < k1;
+            const char *pa = in ? ga[i] + static_cast<int64_t>(e) * EB : reinterpret_cast<const char *>(kZeroVec);
+            const char *pb = in ? gb[i] + static_cast<int64_t>(e) * EB : reinterpret_cast<const char *>(kZeroVec);
+            load_lds16(pa, la);
+            load_lds16(pb, lb);
         }
     };
 
@@ -360,41 +343,89 @@ __device__ inline void gemm_tile(const HeadArgs &a, int64_t M, int64_t m_base, i
 #pragma unroll
         for (int c = 0; c < 2; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll
-    for (int st = 0; st < kRing - 1; ++st)
-        if (st < nst) issue(st);
-    for (int st = 0; st < nst; ++st) {
-        // this wave's loads of stage st are done once at most the later stages' remain
-        wait_later<4, kRing - 2>(min(kRing - 2, nst - 1 - st));   // 4 loads per wave and stage
-        lds_barrier();                            // every wave's part of stage st has landed
-        if (st + kRing - 1 < nst) issue(st + kRing - 1);   // refills the slot of stage st-1
+    // Fragments of one 64-byte k-step q of stage st: this wave's 4 row tiles of A and 2
+    // column tiles of B.
+    auto read_frags = [&](int st, int q, u32x4 (&av)[4], u32x4 (&bv)[2]) {
         const char *sa = ring[st % kRing];
         const char *sb = sa + kHeadTileM * kStageBytes;
-        // every fragment of the stage is read before the first product, so the LDS
-        // latency is paid once per stage rather than once per k-step
-        constexpr int KS = kStageBytes / 64;                // 64-byte k-steps per stage
-        u32x4 av[KS][4], bv[KS][2];
+        const int kk = 4 * q;
 #pragma unroll
-        for (int q = 0; q < KS; ++q) {
-            const int kk = 4 * q;
+        for (int r = 0; r < 4; ++r) {
+            const int row = wr * kWaveTile + r * 16 + l16;
+            av[r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+        }
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = wr * kWaveTile + r * 16 + l16;
-                av[q][r] = *reinterpret_cast<const u32x4 *>(sa + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
-            }
+        for (int c = 0; c < 2; ++c) {
+            const int row = wc * kWaveCols + c * 16 + l16;
+            bv[c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
+        }
+    };
+    auto products = [&](const u32x4 (&av)[4], const u32x4 (&bv)[2]) {
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                const int row = wc * kWaveCols + c * 16 + l16;
-                bv[q][c] = *reinterpret_cast<const u32x4 *>(sb + row * kStageBytes + (((kk + g) ^ (row & 7)) * 16));
-            }
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
+    };
+    static_assert(kStageBytes == 128, "two 64-byte k-steps per stage");
+
+    // Software pipeline: the fragments of the next k-step are read from LDS while the
+    // products of the current one run (the second k-step of a stage during the first's
+    // products, the first of the next stage during the second's).  A slot is refilled
+    // as soon as every wave has read the stage in it, so all kRing slots are in flight.
+    u32x4 a0[4], b0[2], a1[4], b1[2];
+#pragma unroll
+    for (int st = 0; st < kRing; ++st)
+        if (st < nst) issue(st);
+    if (nst > 0) {
+        wait_later<4, kRing - 1>(min(kRing - 1, nst - 1));     // 4 loads per wave and stage
+        lds_barrier();                                          // stage 0 has landed
+        read_frags(0, 0, a0, b0);
+    }
+    int st = 0;
+    // steady state, one basic block: every stage after the next is in flight and the
+    // refill always happens; the loads, LDS reads and products are interleaved so that
+    // a wave's products run while its loads wait to be accepted
+    for (; st + kRing < nst; ++st) {
+        read_frags(st, 1, a1, b1);
+        products(a0, b0);
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one product
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        wait_vm<4 * (kRing - 2)>();                             // stage st+1 landed here
+        lds_barrier();                                          // ... and everywhere
+        issue(st + kRing);
+        read_frags(st + 1, 0, a0, b0);
+        products(a1, b1);
+        // per load: one or two LDS reads, two products
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    for (; st < nst; ++st) {                                    // the last kRing stages
+        read_frags(st, 1, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        products(a0, b0);
+        if (st + 1 < nst) {
+            // this wave's loads of stage st+1 are done once at most the later stages'
+            // remain; the barrier's LDS wait also completes this wave's reads of stage st
+            wait_later<4, kRing - 2>(min(kRing - 2, nst - 2 - st));
+            lds_barrier();                        // stage st+1 landed, stage st read by all
+            read_frags(st + 1, 0, a0, b0);
         }
         __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int q = 0; q < KS; ++q)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-                for (int c = 0; c < 2; ++c) acc[r][c] = mma<DT>(av[q][r], bv[q][c], acc[r][c]);
+        products(a1, b1);
     }
 
     // partial U of this k-slice: upart[ks][row][n], row the list position m, or with

@@ -503,7 +503,7 @@ __device__ __forceinline__ void decide_seq(const DecideArgs &a, int b) {
     const float4 *seq_parts = a.partials + sp.first;
     const bool staged = sp.count > a.RT && sp.count <= kStageParts;
     if (staged) {
-        stage_partials(seq_parts, sp.count, s_parts, t, kDecideThreads);
+        stage_partials(seq_parts, sp.count, seq_parts, 0, s_parts, t, kDecideThreads);
         __syncthreads();
     }
     for (int j = t; j < a.RT; j += kDecideThreads) {

@@ -74,6 +74,45 @@ typedef __attribute__((address_space(3))) const float lds_float;
 // ld(s) returns partial s, read from global memory or from LDS through a pointer of
 // that address space: a global and an LDS pointer are never merged into one, so
 // every access is a global or an LDS instruction, never a flat one.
+// The steps of the merge, shared by every form of it so that all of them round alike:
+// the maximum and its argmax over one chunk of partials (s0 .. s0 + kMergeChunk - 1,
+// those past `splits` skipped; the earlier split wins ties), the sums over one chunk
+// against the reference R, and the statistics from the totals.
+__device__ inline void merge_max_chunk(const float4 (&q)[kMergeChunk], int s0, int splits, float &M, int &arg) {
+#pragma unroll
+    for (int i = 0; i < kMergeChunk; ++i)
+        if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
+}
+
+__device__ inline void merge_sum_chunk(const float4 (&q)[kMergeChunk], int s0, int splits, float R, float &S, float &T) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int i = 0; i < kMergeChunk; ++i) {
+        if (s0 + i < splits && q[i].z > 0.f) {
+            const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
+                                                              // k_vocab_reduce rounded it
+            const float f = __builtin_amdgcn_exp2f(dr);
+            S = fmaf(f, q[i].z, S);
+            T = fmaf(f, fmaf(dr, q[i].z, q[i].w), T);
+        }
+    }
+}
+
+__device__ inline RowStat merge_final(float M, int arg, float R, float S, float T) {
+#pragma clang fp contract(off)
+    // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
+    // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
+    const float delta = fmaf(M, kLog2e, -R);
+    const float l2s = __log2f(S);
+    RowStat r;
+    r.max = M;
+    r.arg = arg;
+    r.log_s = (l2s - delta) * kLn2;
+    r.lse = M + r.log_s;
+    r.ent = (l2s - T / S) * kLn2;
+    return r;
+}
+
 template <typename Ld>
 __device__ inline RowStat merge_row_t(Ld ld, int splits) {
 #pragma clang fp contract(off)
@@ -92,9 +131,7 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
         for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
 #pragma unroll
             for (int i = 0; i < kMergeChunk; ++i) q[i] = ld(min(s0 + i, splits - 1));   // unconditional
-#pragma unroll
-            for (int i = 0; i < kMergeChunk; ++i)   // earlier split wins ties
-                if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
+            merge_max_chunk(q, s0, splits, M, arg);
         }
         R = __fmul_rn(M, kLog2e);
         for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
@@ -102,29 +139,47 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
 #pragma unroll
                 for (int i = 0; i < kMergeChunk; ++i) q[i] = ld(min(s0 + i, splits - 1));
             }
-#pragma unroll
-            for (int i = 0; i < kMergeChunk; ++i) {
-                if (s0 + i < splits && q[i].z > 0.f) {
-                    const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
-                                                                      // k_vocab_reduce rounded it
-                    const float f = __builtin_amdgcn_exp2f(dr);
-                    S = fmaf(f, q[i].z, S);
-                    T = fmaf(f, fmaf(dr, q[i].z, q[i].w), T);
-                }
-            }
+            merge_sum_chunk(q, s0, splits, R, S, T);
         }
     }
-    // S = sum 2^(x*log2e - R) = 2^delta * sum e^(x - M) with delta = M*log2e - R the
-    // rounding residual of R (exact by one fma); it matters once |M| is in the thousands
-    const float delta = fmaf(M, kLog2e, -R);
-    const float l2s = __log2f(S);
-    RowStat r;
-    r.max = M;
-    r.arg = arg;
-    r.log_s = (l2s - delta) * kLn2;
-    r.lse = M + r.log_s;
-    r.ent = (l2s - T / S) * kLn2;
-    return r;
+    return merge_final(M, arg, R, S, T);
+}
+
+// Two rows of `splits` > 1 partials each, at pa and pb in global memory, merged as
+// merge_row merges them, the loads of both rows' chunk issued together (one memory
+// round trip when splits <= kMergeChunk, else two per chunk).
+__device__ inline void merge_rows2(const float4 *pa, const float4 *pb, int splits, RowStat &ra, RowStat &rb) {
+#pragma clang fp contract(off)
+    float Ma = -INFINITY, Mb = -INFINITY, Sa = 0.f, Ta = 0.f, Sb = 0.f, Tb = 0.f;
+    int aa = INT_MAX, ab = INT_MAX;
+    float4 qa[kMergeChunk], qb[kMergeChunk];
+    auto load = [&](int s0) {
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i) {
+            const int s = min(s0 + i, splits - 1);   // unconditional
+            qa[i] = pa[s];
+            qb[i] = pb[s];
+        }
+        // every word stays live until here, so no load register is reused while the
+        // later loads are in flight
+#pragma unroll
+        for (int i = 0; i < kMergeChunk; ++i)
+            asm volatile("" ::"v"(qa[i].x), "v"(qa[i].y), "v"(qa[i].z), "v"(qa[i].w), "v"(qb[i].x), "v"(qb[i].y),
+                         "v"(qb[i].z), "v"(qb[i].w));
+    };
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+        load(s0);
+        merge_max_chunk(qa, s0, splits, Ma, aa);
+        merge_max_chunk(qb, s0, splits, Mb, ab);
+    }
+    const float Ra = __fmul_rn(Ma, kLog2e), Rb = __fmul_rn(Mb, kLog2e);
+    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+        if (splits > kMergeChunk) load(s0);        // else the chunk is still in registers
+        merge_sum_chunk(qa, s0, splits, Ra, Sa, Ta);
+        merge_sum_chunk(qb, s0, splits, Rb, Sb, Tb);
+    }
+    ra = merge_final(Ma, aa, Ra, Sa, Ta);
+    rb = merge_final(Mb, ab, Rb, Sb, Tb);
 }
 
 // The candidate merge_row takes (its .arg) from the partials' maxima alone: the first
@@ -169,22 +224,27 @@ __device__ inline RowStat merge_row_lds(const float4 *p, int splits) {
 // memory directly.
 constexpr int kStageParts = 1024;
 
-// Copies n partials from p into stage with the threads [first, first + count) of the
-// caller (each copies every count-th, eight loads issued before the first write); the
-// caller synchronises before reading them.
-__device__ inline void stage_partials(const float4 *p, int64_t n, float4 *stage, int idx, int count) {
+// Copies the n1 partials at p1, then the n2 at p2, into stage[0, n1 + n2) with the
+// threads [idx, idx + count) of the caller (each copies every count-th, eight loads
+// issued before the first write); the caller synchronises before reading them.
+__device__ inline void stage_partials(const float4 *p1, int64_t n1, const float4 *p2, int64_t n2, float4 *stage,
+                                      int idx, int count) {
     constexpr int kBatch = 8;
+    const int64_t n = n1 + n2;
     for (int64_t i0 = idx; i0 < n; i0 += kBatch * static_cast<int64_t>(count)) {
         float4 v[kBatch];
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
-            const int64_t i = i0 + j * static_cast<int64_t>(count);
-            v[j] = p[i < n ? i : n - 1];                // unconditional: clamped
+            int64_t i = i0 + j * static_cast<int64_t>(count);
+            i = i < n ? i : n - 1;                       // unconditional: clamped
+            v[j] = *(i < n1 ? p1 + i : p2 + (i - n1));
         }
+        // unconditional too: an index past the end writes partial n-1's own value to
+        // its slot again (a store under a branch would pull its load in after it)
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             const int64_t i = i0 + j * static_cast<int64_t>(count);
-            if (i < n) stage[i] = v[j];
+            stage[i < n ? i : n - 1] = v[j];
         }
     }
 }

@@ -99,37 +99,22 @@ __device__ inline int tgt_row(const FinishArgs &a, int64_t tr, const RowStat &ts
 // sample k_sample left, in a split step's second phase the first phase's choice) and
 // draft row j; decision j+1 is a match when its draft token
 // equals that candidate; log p_T and log p_D of the draft token come from the same
-// rows (Section 3.4).  stage: LDS room for `cap` partials of this wave, into which the
-// sequence's partials are copied first when the rows are split (and they fit).
-template <int DT>
-__device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, float4 *stage, int cap) {
+// rows (Section 3.4).  PM, how the partials are read (a template parameter, so that
+// each kernel holds one way and no memory wait is placed for another): kPartOne, one
+// split per row, each row's partial read with the token; kPartSplit, split rows, the
+// lane's target and draft rows merged from registers, their partials loaded together.
+enum { kPartOne, kPartSplit };
+
+template <int PM>
+__device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
     const int K = a.D;
     const int64_t di = static_cast<int64_t>(b) * K + lane;       // decision lane+1, draft row lane
     const int64_t t0 = static_cast<int64_t>(b) * (K + 1);        // the sequence's first target row
     const int64_t tr = t0 + lane;                                 // target row `lane`
     const PartPlan &plan = a.plan;
     const int64_t d0 = plan.n_tgt_rows + static_cast<int64_t>(b) * K;
-    // the target rows' partials, then the draft rows' (consecutive slots each)
-    const RowParts tp = rows_parts(plan, t0, t0 + K + 1);
-    const RowParts dp = K > 0 ? rows_parts(plan, d0, d0 + K) : RowParts{0, 0};
-    const bool staged = plan.splits > 1 && tp.count + dp.count <= cap;
     int tok = -1;
     if (lane < K) tok = a.tokens[di];
-    if (staged) {                 // one wave writes and then reads: LDS keeps the wave's order
-        stage_partials(a.partials + tp.first, tp.count, stage, lane, 64);
-        stage_partials(a.partials + dp.first, dp.count, stage + tp.count, lane, 64);
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
-        __builtin_amdgcn_wave_barrier();
-    }
-    // one split per row: each row's only partial is read together with the token and
-    // the logits at it, then the merges, which wait for nothing
-    const bool one = plan.splits == 1;
-    float4 qt{}, qd{}, qk{};
-    if (one) {
-        if (lane <= K) qt = a.partials[tr];
-        if (lane < K) qd = a.partials[d0 + lane];
-        if (K >= 64 && lane == 0) qk = a.partials[t0 + K];
-    }
     // the logits at the draft token, which the reduction stored (read whatever the
     // token; used only when it is valid)
     const bool valid = tok >= 0 && tok < a.V;
@@ -138,21 +123,31 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane, f
         xt = a.ws_xtok[tr];
         xd = a.ws_xtok[d0 + lane];
     }
-    // merged statistics of row r (target rows first in the stage, then draft rows)
-    auto merged = [&](int64_t r, const float4 &q, const RowParts &seq, int64_t stage_off) -> RowStat {
-        if (one) return merge_row_t([q](int) { return q; }, 1);
-        const RowParts rp = row_parts(plan, r);
-        return staged ? merge_row_lds(stage + stage_off + (rp.first - seq.first), rp.count)
-                      : merge_row(a.partials + rp.first, rp.count);
-    };
+    // the merged statistics of target row `lane` (lanes <= K) and draft row `lane`
+    // (lanes < K; the others merge a row they drop)
+    RowStat ts{}, ds{}, ks{};
+    const int64_t trc = lane <= K ? tr : t0, drc = lane < K ? d0 + lane : t0;
+    if constexpr (PM == kPartOne) {
+        const float4 qt = a.partials[trc], qd = a.partials[drc];
+        float4 qk{};
+        if (K >= 64 && lane == 0) qk = a.partials[t0 + K];
+        ts = merge_row_t([qt](int) { return qt; }, 1);
+        ds = merge_row_t([qd](int) { return qd; }, 1);
+        if (K >= 64 && lane == 0) ks = merge_row_t([qk](int) { return qk; }, 1);
+    } else {
+        merge_rows2(a.partials + row_parts(plan, trc).first, a.partials + row_parts(plan, drc).first, plan.splits,
+                    ts, ds);
+        if (K >= 64 && lane == 0) {
+            const RowParts rk = row_parts(plan, t0 + K);
+            ks = merge_row(a.partials + rk.first, rk.count);
+        }
+    }
     ChainLane c{kStateMatch, false, NAN, -1, -1, -1};
-    if (K >= 64 && lane == 0) c.tok_k = tgt_row(a, t0 + K, merged(t0 + K, qk, tp, 0));
+    if (K >= 64 && lane == 0) c.tok_k = tgt_row(a, t0 + K, ks);
     if (lane <= K) {
-        const RowStat ts = merged(tr, qt, tp, 0);
         const int cand = tgt_row(a, tr, ts);
         c.tok_t = cand;
         if (lane < K) {
-            const RowStat ds = merged(d0 + lane, qd, dp, tp.count);
             write_drf(a, di, ds);
             c.tok_d = tok;
             c.st = !valid ? kStateReject : tok == cand ? kStateMatch : kStateMismatch;
@@ -218,14 +213,12 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
     }
 }
 
-template <int DT>
+template <int PM>
 __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
-    constexpr int kCap = kStageParts / 4;
-    __shared__ float4 s_parts[4][kCap];
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= a.B) return;                                  // whole wave leaves together
     const int lane = threadIdx.x & 63;
-    const ChainLane c = chain_prefix<DT>(a, b, lane, s_parts[threadIdx.x >> 6], kCap);
+    const ChainLane c = chain_prefix<PM>(a, b, lane);
     chain_suffix(a, b, lane, c, NAN);                      // the head did not run
 }
 
@@ -236,16 +229,15 @@ __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
 // was scored (its token against the candidate of its target row, merged as wave 0
 // merges it), so that its loads wait for no other wave.
 constexpr int kFinishWaves = 8;
-template <int DT>
+template <int HD, int PM>
 __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishArgs a) {
     __shared__ float s_z[64];                              // K <= 64
-    __shared__ float4 s_parts[kStageParts];
     const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int waves = blockDim.x >> 6;                     // >= 2
     const int K = a.D;
     ChainLane c{};
     if (wave == 0) {
-        c = chain_prefix<DT>(a, b, lane, s_parts, kStageParts);
+        c = chain_prefix<PM>(a, b, lane);
     } else {
         const int64_t M = *a.hd.count_dev;                 // rows the GEMM ran on
         for (int t = wave - 1; t < K; t += waves - 1) {    // wave-uniform
@@ -260,8 +252,7 @@ __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishA
             const int cand = a.sampled ? taken : am;
             if (a.head_ran && tok >= 0 && tok < a.V && tok != cand) {
                 const int ksl = headz::live_ksplit(a.hd, M);
-                const float z = a.head_dt == kBF16 ? headz::head_z<kBF16>(a.hd, di, lane, ksl)
-                                                   : headz::head_z<kF32>(a.hd, di, lane, ksl);
+                const float z = headz::head_z<HD>(a.hd, di, lane, ksl);
                 if (lane == 0) s_z[t] = z;
             }
         }
@@ -394,14 +385,21 @@ hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s) {
         if (dt == kBF16) hipLaunchKernelGGL(k_tree_finish<kBF16>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
         else hipLaunchKernelGGL(k_tree_finish<kF32>, dim3(a.B), dim3(kMaxSeqRows), 0, s, a);
     } else {
+        const bool one = a.plan.splits == 1;
         if (a.fuse_head) {
             const dim3 block(64 * std::min(a.D + 1, kFinishWaves));   // D >= 1 when the head ran
-            if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish_head<kBF16>, dim3(a.B), block, 0, s, a);
-            else hipLaunchKernelGGL(k_chain_finish_head<kF32>, dim3(a.B), block, 0, s, a);
+            const bool bf = a.head_dt == kBF16;
+            if (one) {
+                if (bf) hipLaunchKernelGGL((k_chain_finish_head<kBF16, kPartOne>), dim3(a.B), block, 0, s, a);
+                else hipLaunchKernelGGL((k_chain_finish_head<kF32, kPartOne>), dim3(a.B), block, 0, s, a);
+            } else {
+                if (bf) hipLaunchKernelGGL((k_chain_finish_head<kBF16, kPartSplit>), dim3(a.B), block, 0, s, a);
+                else hipLaunchKernelGGL((k_chain_finish_head<kF32, kPartSplit>), dim3(a.B), block, 0, s, a);
+            }
         } else {
             const unsigned blocks = static_cast<unsigned>((a.B + 3) / 4);
-            if (dt == kBF16) hipLaunchKernelGGL(k_chain_finish<kBF16>, dim3(blocks), dim3(256), 0, s, a);
-            else hipLaunchKernelGGL(k_chain_finish<kF32>, dim3(blocks), dim3(256), 0, s, a);
+            if (one) hipLaunchKernelGGL(k_chain_finish<kPartOne>, dim3(blocks), dim3(256), 0, s, a);
+            else hipLaunchKernelGGL(k_chain_finish<kPartSplit>, dim3(blocks), dim3(256), 0, s, a);
         }
     }
     return hipGetLastError();
