@@ -157,7 +157,8 @@ typedef struct {
  * Optional hooks; a NULL options pointer, or zero/NULL members, mean defaults.
  *
  * Order of work inside a verify call: (1) reduce the logit rows, (2) decide
- * (verification tokens, Delta, mismatch list), (3) the head on the mismatch
+ * (verification tokens, Delta, mismatch list; for chains taken inside the head
+ * GEMM, which derives its list, and the finish), (3) the head on the mismatch
  * rows, (4) finish (draft statistics, log p_D, verdicts, first stop, emission).
  */
 typedef struct {
