@@ -191,16 +191,18 @@ class Prepared:
         self.uniform = uniform
         self.policy_u = policy_u
         self.rl = rl                    # (struct, output tensors, correct tensor) or None
+        self.hidden_row0 = None         # packed hidden rows: int64 [B] device tensor, and
+        self.hidden_rows = 0            # the rows of the packed array
         self._keep = []
 
     def _options(self, timing):
         if (timing is None and not self.splits and self.uniform is None
-                and self.policy_u is None and self.rl is None):
+                and self.policy_u is None and self.rl is None and self.hidden_row0 is None):
             return None
         ev = [None] * 4 if timing is None else [None if e is None else _event_handle(e) for e in timing]
         rl = None if self.rl is None else ctypes.pointer(self.rl[0])
         return _Options(ev[0], ev[1], ev[2], ev[3], self.splits, _ptr(self.uniform),
-                        _ptr(self.policy_u), rl)
+                        _ptr(self.policy_u), rl, _ptr(self.hidden_row0), int(self.hidden_rows))
 
     def launch(self, timing=None):
         """Enqueue the step on torch's current stream.  `timing` = four torch events
@@ -273,20 +275,29 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
                   sample_u: Optional[torch.Tensor] = None,
                   policy_u: Optional[torch.Tensor] = None,
                   correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
-                  beta: float = 0.25) -> Prepared:
+                  beta: float = 0.25, hidden_row0: Optional[torch.Tensor] = None) -> Prepared:
     """sample_u: one uniform per target row [B, K+1] for temperature-1 candidates
     (cospec_options.sample_uniform); None for the greedy argmax.  policy_u: one
     uniform per decision [B, K] for sampled arbitration.  correct: uint8 [B]
     rollout correctness; turns on the per-round RL statistics (returned with an
-    "rl_" prefix) with failure-reward weights alpha and beta."""
+    "rl_" prefix) with failure-reward weights alpha and beta.  hidden_row0: int64 [B]
+    device tensor; hidden is then a packed [rows, d] array and decision i of sequence
+    b reads row hidden_row0[b] + i - 1 (cospec_options.hidden_row0)."""
     B, R, V = target.shape
     K = R - 1
     ld = _row_stride(target)
     if K > 0 and _row_stride(draft) != ld:
         raise ValueError("target and draft rows must share one stride")
+    if hidden_row0 is not None:
+        if tuple(hidden_row0.shape) != (B,) or hidden_row0.dtype != torch.int64 or not hidden_row0.is_cuda:
+            raise ValueError("hidden_row0 must be an int64 device tensor [B]")
+        if hidden.dim() != 2 or not hidden.is_contiguous():
+            raise ValueError("with hidden_row0, hidden must be a contiguous [rows, d] array")
+        hidden_row0 = hidden_row0.contiguous()
+    packed_ok = hidden_row0 is not None or (hidden.shape[:2] == (B, K) and hidden.is_contiguous())
     if K > 0 and (tuple(draft.shape) != (B, K, V) or tuple(draft_tokens.shape) != (B, K)
                   or draft_tokens.dtype != torch.int32 or not draft_tokens.is_contiguous()
-                  or hidden.shape[:2] != (B, K) or not hidden.is_contiguous()):
+                  or not packed_ok):
         raise ValueError("shape/dtype mismatch between target, draft, draft_tokens and hidden")
     dev = target.device
     hs = _head_struct(head)
@@ -305,6 +316,8 @@ def prepare_block(target, draft, draft_tokens, hidden, head, lam: float, feature
     p = Prepared(L.cospec_verify_block, args, outputs, feats, fst, workspace, splits,
                  _uniforms(sample_u, B, K + 1), _policy_uniforms(policy_u, B, K),
                  _rl(correct, alpha, beta, B, K, dev))
+    if hidden_row0 is not None:
+        p.hidden_row0, p.hidden_rows = hidden_row0, hidden.shape[0]
     p._keep = [hs, target, draft, draft_tokens, hidden, head]
     return p
 
@@ -349,11 +362,11 @@ def verify_block(target, draft, draft_tokens, hidden, head, lam: float, features
                  sample_u: Optional[torch.Tensor] = None,
                  policy_u: Optional[torch.Tensor] = None,
                  correct: Optional[torch.Tensor] = None, alpha: float = 1.0,
-                 beta: float = 0.25) -> dict:
+                 beta: float = 0.25, hidden_row0: Optional[torch.Tensor] = None) -> dict:
     """cospec_verify_block on device tensors; returns accept_len, tokens (+ features,
     + rl_* statistics when `correct` is given)."""
     p = prepare_block(target, draft, draft_tokens, hidden, head, lam, features, splits,
-                      sample_u, policy_u, correct, alpha, beta)
+                      sample_u, policy_u, correct, alpha, beta, hidden_row0)
     p.launch()
     return p.result()
 

@@ -45,6 +45,9 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
 constexpr int64_t kMaxRowBytes = INT32_MAX;    // V * element bytes of one logit row
+// Chain batches with at most this many decision slots run the head's first layer on
+// every slot (slot_gemm.h) rather than on the mismatch rows after the reduction.
+constexpr int64_t kEverySlotMax = 512;
 
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -256,9 +259,16 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     // (or read the decide kernel's) and run on the M listed rows only
     const int64_t m_cap = static_cast<int64_t>(c.B) * c.D;
     const bool fuse_head = head && !c.is_tree;
+    // small chain batches: the first layer runs on every decision slot (slot_gemm.h), in
+    // the reduction's launch for a whole step and on its own in the second phase of a
+    // split one, instead of on the mismatch rows after the reduction (both forms of the
+    // step then compute z alike)
+    const bool every_slot = fuse_head && phase != kReducePhase && m_cap <= kEverySlotMax;
     HeadArgs ha{};
     if (head) {
-        ha.hidden = c.hidden;
+        // no hidden rows at all (a packed array of none): every z is NaN, and the GEMMs'
+        // clamped operand loads read W1's first row (valid memory of d elements) instead
+        ha.hidden = hidden_rows > 0 ? c.hidden : c.head->w1;
         ha.n_rows = hidden_rows;
         ha.row0 = hidden_row0;
         ha.slots = static_cast<int32_t>(c.D);
@@ -340,7 +350,9 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         }
 
         if (!record(c.opts ? c.opts->reduce_begin : nullptr)) return COSPEC_ERR_HIP;
-        if (launch_reduce(dt, ra, c.stream) != hipSuccess) return COSPEC_ERR_HIP;
+        const hipError_t re = every_slot ? launch_reduce_head(dt, static_cast<Dtype>(c.head->dtype), ra, ha, c.stream)
+                                         : launch_reduce(dt, ra, c.stream);
+        if (re != hipSuccess) return COSPEC_ERR_HIP;
         if (!record(c.opts ? c.opts->reduce_end : nullptr)) return COSPEC_ERR_HIP;
         // the second pair brackets nothing: back to back, it measures what an event
         // interval adds by itself
@@ -372,10 +384,12 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         }
     }
     if (!do_arbitrate) return COSPEC_OK;
-    if (head) {
+    if (head && !(every_slot && do_reduce)) {
         const Dtype hdt = static_cast<Dtype>(c.head->dtype);
-        if ((fuse_head ? launch_head_gemm(hdt, ha, c.stream) : launch_head(hdt, ha, c.stream)) != hipSuccess)
-            return COSPEC_ERR_HIP;
+        const hipError_t he = every_slot ? launch_slot_gemm(hdt, ha, c.stream)
+                              : fuse_head ? launch_head_gemm(hdt, ha, c.stream)
+                                          : launch_head(hdt, ha, c.stream);
+        if (he != hipSuccess) return COSPEC_ERR_HIP;
     }
 
     // finish
@@ -406,6 +420,7 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
     fa.policy_u = policy_u;
     fa.ws_logp_tgt = ws_logp;
     fa.fuse_head = fuse_head;
+    fa.head_every_slot = every_slot;
     fa.head_dt = head ? c.head->dtype : 0;
     fa.hd = ha;
     fa.hd.list = nullptr;           // the finish reads the GEMM's partials by decision slot

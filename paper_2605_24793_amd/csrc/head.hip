@@ -21,10 +21,7 @@
 // k_head_epilogue: one wave per row adds the k-slices in a fixed order, then
 // b1, the ReLU, w2 and b2, so z is bit-identical run to run.
 //
-// MFMA operand layout used: for the 16x16 shapes, lane l supplies row (l % 16)
-// of A and column (l % 16) of B for the k-slice owned by lane group l / 16, and
-// receives D[4*(l/16) + j][l % 16] in accumulator element j.  A and B take the
-// same k-slice per lane, so the order of k inside an instruction is immaterial.
+// The MFMA step and its operand layout are in mfma.h.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -33,7 +30,9 @@
 
 #include "head_z.h"
 #include "launch.h"
+#include "mfma.h"
 #include "rowstat.h"
+#include "slot_gemm.h"
 
 namespace cospec {
 namespace {
@@ -62,10 +61,6 @@ __device__ inline void load_lds16(const void *g, const char *lds) {
 }
 #pragma clang diagnostic pop
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float floatx4;
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 constexpr int kStageBytes = 128;                  // bytes of k per row per stage
 // LDS ring depth: four stages (three in flight while one is used, 128 KiB: one
 // workgroup per CU), or two (64 KiB: two workgroups per CU) when the grid has more
@@ -75,20 +70,6 @@ constexpr int kRingShallow = 2;
 constexpr int kWaveTile = 64;                    // rows of a wave's sub-tile
 constexpr int kWaveCols = 32;                    // columns of a wave's sub-tile
 constexpr int kGemmWaves = 8;                    // 2 x 4 waves per workgroup: two per SIMD
-
-// One 64-byte k-step of a 16x16 tile: one 16-byte operand vector per lane.
-template <int DT> __device__ inline floatx4 mma(u32x4 a, u32x4 b, floatx4 c);
-template <> __device__ inline floatx4 mma<kBF16>(u32x4 a, u32x4 b, floatx4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-template <> __device__ inline floatx4 mma<kF32>(u32x4 a, u32x4 b, floatx4 c) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[j]), __uint_as_float(b[j]), c, 0, 0, 0);
-    return c;
-}
-
 
 // Waits until at most N vector-memory operations of this wave are outstanding.
 template <int N> __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
@@ -162,9 +143,9 @@ __device__ inline void mark_single(const HeadArgs &a, int base, int n, uint64_t 
 }
 
 // Part 1 of build_list, split rows: NS slots per thread, each merged by its thread in
-// split order, kMergeChunk partials of every slot loaded at once; the argmax is the one
+// split order, CH partials of every slot loaded at once; the argmax is the one
 // merge_row takes (the first split with S > 0 and the strictly largest maximum).
-template <int NS>
+template <int NS, int CH>
 __device__ inline void mark_split(const HeadArgs &a, int base, int n, int splits, uint64_t kmag, uint8_t *s_need) {
     const int tid = threadIdx.x;
     int tok[NS], r[NS], arg[NS];
@@ -178,17 +159,17 @@ __device__ inline void mark_split(const HeadArgs &a, int base, int n, int splits
         M[j] = -INFINITY;
         arg[j] = INT_MAX;
     }
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {       // uniform trip count
-        u32x4 q[NS][kMergeChunk];
+    for (int s0 = 0; s0 < splits; s0 += CH) {       // uniform trip count
+        u32x4 q[NS][CH];
 #pragma unroll
         for (int j = 0; j < NS; ++j)
 #pragma unroll
-            for (int k = 0; k < kMergeChunk; ++k)
+            for (int k = 0; k < CH; ++k)
                 q[j][k] = *reinterpret_cast<const u32x4 *>(a.partials + (r[j] * splits + min(s0 + k, splits - 1)));
 #pragma unroll
         for (int j = 0; j < NS; ++j)
 #pragma unroll
-            for (int k = 0; k < kMergeChunk; ++k) {
+            for (int k = 0; k < CH; ++k) {
                 const float x = __uint_as_float(q[j][k].x);
                 const bool take = (s0 + k < splits) & (__uint_as_float(q[j][k].z) > 0.f) & (x > M[j]);
                 M[j] = take ? x : M[j];
@@ -197,7 +178,7 @@ __device__ inline void mark_split(const HeadArgs &a, int base, int n, int splits
 #pragma unroll
         for (int j = 0; j < NS; ++j)
 #pragma unroll
-            for (int k = 0; k < kMergeChunk; ++k) asm volatile("" ::"v"(q[j][k].w));
+            for (int k = 0; k < CH; ++k) asm volatile("" ::"v"(q[j][k].w));
     }
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
@@ -232,10 +213,10 @@ __device__ inline int64_t build_list(const HeadArgs &a, int32_t *list) {
         if (n <= 4 * kGemmThreads) mark_single<CAND, 4>(a, 0, n, kmag, s_need);
         else mark_single<CAND, 8>(a, 0, n, kmag, s_need);          // n <= kBuildListMax
     } else if (n <= kGemmThreads) {
-        mark_split<1>(a, 0, n, splits, kmag, s_need);
+        mark_split<1, 16>(a, 0, n, splits, kmag, s_need);          // one round trip to 16 splits
     } else {
         for (int base = 0; base < n; base += 2 * kGemmThreads)      // uniform trip count
-            mark_split<2>(a, base, n, splits, kmag, s_need);
+            mark_split<2, 8>(a, base, n, splits, kmag, s_need);
     }
     __syncthreads();
     // part 2: exclusive scan of the per-thread counts, within the wave, then over the waves
@@ -526,6 +507,14 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_head_gemm_loop(HeadArgs a) 
     }
 }
 
+// The slot GEMM (slot_gemm.h) on its own, for the second phase of a split chain step
+// (whose hidden states arrive after the reduction): the same work and the same
+// partials as in the whole step's reduction launch, so both give the same z.
+template <int DT>
+__global__ __launch_bounds__(kReduceThreads) void k_slot_gemm(HeadArgs a) {
+    slotgemm::run<DT>(a, blockIdx.x, reinterpret_cast<const u32x4 *>(kZeroVec));
+}
+
 // z[m] = w2 . relu(sum_ks upart[ks][m] + b1) + b2, one wave per row, fixed order.
 template <int DT>
 __global__ __launch_bounds__(256) void k_head_epilogue(HeadArgs a) {
@@ -595,6 +584,15 @@ int32_t head_gemm_slots(Dtype dt, bool build) {
         cache[dev][di][bi] = r;
     }
     return r;
+}
+
+hipError_t launch_slot_gemm(Dtype dt, const HeadArgs &a, hipStream_t s) {
+    const int64_t blocks = slotgemm::blocks(a);
+    if (blocks <= 0 || blocks > INT32_MAX) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(blocks));
+    if (dt == kBF16) hipLaunchKernelGGL(k_slot_gemm<kBF16>, grid, dim3(kReduceThreads), 0, s, a);
+    else hipLaunchKernelGGL(k_slot_gemm<kF32>, grid, dim3(kReduceThreads), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s) {

@@ -194,6 +194,9 @@ struct FinishArgs {
     int32_t fuse_head;
     int32_t head_dt;
     HeadArgs hd;
+    // chain only: the first layer ran over every decision slot (hd.ksplit slices, in the
+    // reduction's launch), not over the mismatch list of the persistent GEMM
+    int32_t head_every_slot;
 };
 
 // Speculative sampling baseline (k_sps_finish, k_sps_mass, k_sps_pick).
@@ -238,12 +241,17 @@ struct ArbFinishArgs {
 };
 
 hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s);
+// The reduction with the head's first layer over all h.m_cap decision slots in the same
+// launch (chains; h.upart by slot, h.ksplit slices; logit dtype dt, head dtype hdt).
+hipError_t launch_reduce_head(Dtype dt, Dtype hdt, const ReduceArgs &a, const HeadArgs &h, hipStream_t s);
 int32_t reduce_slots(Dtype dt);   // reduction workgroups resident at once on the current device
 hipError_t launch_sample(Dtype dt, const SampleArgs &a, hipStream_t s);
 hipError_t launch_decide(Dtype dt, const DecideArgs &a, hipStream_t s);
 int32_t head_ksplit(int64_t m_cap, int32_t d, int32_t h, int32_t elem_bytes);
 hipError_t launch_head(Dtype dt, const HeadArgs &a, hipStream_t s);   // GEMM + epilogue
 hipError_t launch_head_gemm(Dtype dt, const HeadArgs &a, hipStream_t s);
+// The first layer over all a.m_cap decision slots on its own (slot_gemm.h).
+hipError_t launch_slot_gemm(Dtype dt, const HeadArgs &a, hipStream_t s);
 // Resident workgroups of the persistent head GEMM on the current device (cached).
 int32_t head_gemm_slots(Dtype dt, bool build);   // GEMM only
 hipError_t launch_finish(Dtype dt, const FinishArgs &a, hipStream_t s);

@@ -32,6 +32,7 @@
 
 #include "launch.h"
 #include "rowstat.h"
+#include "slot_gemm.h"
 
 // Products and sums are rounded as written in this file: the references (x * log2e
 // rounded) must be the same numbers in every kernel that forms them, so no
@@ -560,14 +561,13 @@ __device__ __forceinline__ void decide_seq(const DecideArgs &a, int b) {
     }
 }
 
-// Units are (row, split) pairs, split fastest, one workgroup each.  Workgroup 0 also
+// Units are (row, split) pairs, split fastest, one workgroup each.  Unit 0 also
 // zeroes the decide step's list counter.
 template <int DT, bool SEG>
-__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.reset_counter) *a.reset_counter = 0;
+__device__ __forceinline__ void reduce_unit(const ReduceArgs &a, int u) {
+    if (u == 0 && threadIdx.x == 0 && a.reset_counter) *a.reset_counter = 0;
     using E = Elt<DT>;
     const int splits = a.plan.splits;
-    const int u = blockIdx.x;
     const int row = u / splits, split = u - row * splits;
     if (row >= a.n_tgt_rows && a.parent) {   // tree: only nodes with a child need their draft row
         const int r = row - a.n_tgt_rows;
@@ -606,6 +606,30 @@ __global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
         a.partials[u] = part;
         if (own) a.xtok[row] = xt;
     }
+}
+
+template <int DT, bool SEG>
+__global__ __launch_bounds__(kReduceThreads) void k_vocab_reduce(ReduceArgs a) {
+    reduce_unit<DT, SEG>(a, blockIdx.x);
+}
+
+// Sixteen zero bytes in device memory, loaded by the slot GEMM's lanes past the end of d.
+__device__ __attribute__((aligned(16))) const u32x4 kZero16 = {0u, 0u, 0u, 0u};
+
+// A small chain step's reduction launch with the head's first layer over every decision
+// slot beside it (slot_gemm.h): the first `head_blocks` workgroups are the slot GEMM's,
+// dispatched first so that they start at once; the rest are the reduction's units.
+// The occupancy bound is k_vocab_reduce's own (eight waves per SIMD for bf16 rows
+// without segments, six otherwise): left free, the compiler gives the reduction's code
+// more registers here, and the launch fewer resident units.
+template <int DT, bool SEG, int HD>
+__global__ __launch_bounds__(kReduceThreads) __attribute__((amdgpu_waves_per_eu(DT == kBF16 && !SEG ? 8 : 6)))
+void k_vocab_reduce_head(ReduceArgs a, HeadArgs h, int head_blocks) {
+    if (static_cast<int>(blockIdx.x) < head_blocks) {
+        slotgemm::run<HD>(h, blockIdx.x, &kZero16);
+        return;
+    }
+    reduce_unit<DT, SEG>(a, blockIdx.x - head_blocks);
 }
 
 template <int DT>
@@ -656,6 +680,31 @@ hipError_t launch_reduce(Dtype dt, const ReduceArgs &a, hipStream_t s) {
     if (grid.x == 0) return hipSuccess;
     if (dt == kBF16) launch_reduce_t<kBF16>(a, grid, s);
     else launch_reduce_t<kF32>(a, grid, s);
+    return hipGetLastError();
+}
+
+template <int DT, bool SEG>
+void launch_reduce_head_t(Dtype hdt, const ReduceArgs &a, const HeadArgs &h, int head_blocks, dim3 grid,
+                          hipStream_t s) {
+    if (hdt == kBF16)
+        hipLaunchKernelGGL((k_vocab_reduce_head<DT, SEG, kBF16>), grid, dim3(kReduceThreads), 0, s, a, h, head_blocks);
+    else
+        hipLaunchKernelGGL((k_vocab_reduce_head<DT, SEG, kF32>), grid, dim3(kReduceThreads), 0, s, a, h, head_blocks);
+}
+
+hipError_t launch_reduce_head(Dtype dt, Dtype hdt, const ReduceArgs &a, const HeadArgs &h, hipStream_t s) {
+    const int64_t hb = slotgemm::blocks(h);
+    const int64_t units = static_cast<int64_t>(a.n_rows) * a.plan.splits;
+    if (hb <= 0 || hb + units > INT32_MAX) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(hb + units));
+    const int hbi = static_cast<int>(hb);
+    if (dt == kBF16) {
+        if (a.seg) launch_reduce_head_t<kBF16, true>(hdt, a, h, hbi, grid, s);
+        else launch_reduce_head_t<kBF16, false>(hdt, a, h, hbi, grid, s);
+    } else {
+        if (a.seg) launch_reduce_head_t<kF32, true>(hdt, a, h, hbi, grid, s);
+        else launch_reduce_head_t<kF32, false>(hdt, a, h, hbi, grid, s);
+    }
     return hipGetLastError();
 }
 

@@ -78,16 +78,18 @@ typedef __attribute__((address_space(3))) const float lds_float;
 // the maximum and its argmax over one chunk of partials (s0 .. s0 + kMergeChunk - 1,
 // those past `splits` skipped; the earlier split wins ties), the sums over one chunk
 // against the reference R, and the statistics from the totals.
-__device__ inline void merge_max_chunk(const float4 (&q)[kMergeChunk], int s0, int splits, float &M, int &arg) {
+template <int N>
+__device__ inline void merge_max_chunk(const float4 (&q)[N], int s0, int splits, float &M, int &arg) {
 #pragma unroll
-    for (int i = 0; i < kMergeChunk; ++i)
+    for (int i = 0; i < N; ++i)
         if (s0 + i < splits && q[i].z > 0.f && q[i].x > M) { M = q[i].x; arg = __float_as_int(q[i].y); }
 }
 
-__device__ inline void merge_sum_chunk(const float4 (&q)[kMergeChunk], int s0, int splits, float R, float &S, float &T) {
+template <int N>
+__device__ inline void merge_sum_chunk(const float4 (&q)[N], int s0, int splits, float R, float &S, float &T) {
 #pragma clang fp contract(off)
 #pragma unroll
-    for (int i = 0; i < kMergeChunk; ++i) {
+    for (int i = 0; i < N; ++i) {
         if (s0 + i < splits && q[i].z > 0.f) {
             const float dr = __fmul_rn(q[i].x, kLog2e) - R;   // the split's reference, as
                                                               // k_vocab_reduce rounded it
@@ -146,16 +148,19 @@ __device__ inline RowStat merge_row_t(Ld ld, int splits) {
 }
 
 // Two rows of `splits` > 1 partials each, at pa and pb in global memory, merged as
-// merge_row merges them, the loads of both rows' chunk issued together (one memory
-// round trip when splits <= kMergeChunk, else two per chunk).
+// merge_row merges them (the same steps in split order, so the same bits), the loads
+// of both rows' chunk of kWideChunk issued together: one memory round trip when
+// splits <= kWideChunk, else two per chunk.
+constexpr int kWideChunk = 16;
 __device__ inline void merge_rows2(const float4 *pa, const float4 *pb, int splits, RowStat &ra, RowStat &rb) {
 #pragma clang fp contract(off)
+    constexpr int N = kWideChunk;
     float Ma = -INFINITY, Mb = -INFINITY, Sa = 0.f, Ta = 0.f, Sb = 0.f, Tb = 0.f;
     int aa = INT_MAX, ab = INT_MAX;
-    float4 qa[kMergeChunk], qb[kMergeChunk];
+    float4 qa[N], qb[N];
     auto load = [&](int s0) {
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) {
+        for (int i = 0; i < N; ++i) {
             const int s = min(s0 + i, splits - 1);   // unconditional
             qa[i] = pa[s];
             qb[i] = pb[s];
@@ -163,18 +168,18 @@ __device__ inline void merge_rows2(const float4 *pa, const float4 *pb, int split
         // every word stays live until here, so no load register is reused while the
         // later loads are in flight
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i)
+        for (int i = 0; i < N; ++i)
             asm volatile("" ::"v"(qa[i].x), "v"(qa[i].y), "v"(qa[i].z), "v"(qa[i].w), "v"(qb[i].x), "v"(qb[i].y),
                          "v"(qb[i].z), "v"(qb[i].w));
     };
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
+    for (int s0 = 0; s0 < splits; s0 += N) {
         load(s0);
         merge_max_chunk(qa, s0, splits, Ma, aa);
         merge_max_chunk(qb, s0, splits, Mb, ab);
     }
     const float Ra = __fmul_rn(Ma, kLog2e), Rb = __fmul_rn(Mb, kLog2e);
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-        if (splits > kMergeChunk) load(s0);        // else the chunk is still in registers
+    for (int s0 = 0; s0 < splits; s0 += N) {
+        if (splits > N) load(s0);                  // else the chunk is still in registers
         merge_sum_chunk(qa, s0, splits, Ra, Sa, Ta);
         merge_sum_chunk(qb, s0, splits, Rb, Sb, Tb);
     }
@@ -188,15 +193,16 @@ __device__ inline void merge_rows2(const float4 *pa, const float4 *pb, int split
 // unconditional (the index clamped) and no branch on the split count, so a caller that
 // needs only the argmax issues these loads together with its others.
 __device__ inline int merge_arg(const float4 *p, int splits) {
+    constexpr int N = 16;                        // one round trip up to 16 splits
     const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
     float M = -INFINITY;
     int arg = INT_MAX;
-    for (int s0 = 0; s0 < splits; s0 += kMergeChunk) {
-        u32x4 c[kMergeChunk];
+    for (int s0 = 0; s0 < splits; s0 += N) {
+        u32x4 c[N];
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) c[i] = q[min(s0 + i, splits - 1)];
+        for (int i = 0; i < N; ++i) c[i] = q[min(s0 + i, splits - 1)];
 #pragma unroll
-        for (int i = 0; i < kMergeChunk; ++i) {
+        for (int i = 0; i < N; ++i) {
             const float x = __uint_as_float(c[i].x);
             const bool take = (s0 + i < splits) & (__uint_as_float(c[i].z) > 0.f) & ((x > M) | (splits == 1));
             M = take ? x : M;

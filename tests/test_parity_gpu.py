@@ -656,9 +656,11 @@ def _same(a, b, keys):
             assert torch.equal(x, y), k
 
 
-@pytest.mark.parametrize("t1", [False, True])
-def test_split_phases_equal_the_whole_step(t1):
-    wl = workloads.make_config(3, B=24)
+# 24 x 7 decision slots: the head's first layer runs on every slot (beside the
+# reduction, and on its own in phase 2); 80 x 7 = 560: on the mismatch rows only
+@pytest.mark.parametrize("t1,B", [(False, 24), (True, 24), (False, 80)])
+def test_split_phases_equal_the_whole_step(t1, B):
+    wl = workloads.make_config(3, B=B)
     u = _uniforms((wl.B, wl.K + 1), 61) if t1 else None
     pu = _uniforms((wl.B, wl.K), 62)
     corr = (torch.arange(wl.B) % 2).to(torch.uint8)
@@ -702,6 +704,38 @@ def test_packed_hidden_rows():
     for i in range(2, K):
         if not delta[i]:
             assert torch.isnan(zt[i]) and acc[i] == 0
+
+
+@pytest.mark.parametrize("B", [16, 90])
+def test_packed_hidden_rows_whole_step(B):
+    # the whole step with packed hidden states (16 x 7 slots: first layer on every slot;
+    # 90 x 7 = 630: on the mismatch rows) equals the step on [B, K, d] bit for bit
+    wl = workloads.make_config(3, B=B)
+    K, d = wl.K, wl.head.d
+    g = torch.Generator().manual_seed(5)
+    gap = torch.randint(0, 9, (B,), generator=g)
+    start = torch.cumsum(gap + K, 0) - K
+    packed = torch.randn(int(start[-1]) + K + 3, d, generator=g).to(wl.hidden.dtype)
+    for b in range(B):
+        packed[start[b]:start[b] + K] = wl.hidden[b]
+    ref = _gpu_block(wl, 0.5)
+    tgt, drf, tok = wl.target.to(DEV), wl.draft.to(DEV), wl.draft_tokens.to(DEV)
+    out = cs.verify_block(tgt, drf, tok, packed.to(DEV), _head_dev(wl.head), 0.5, hidden_row0=start.to(DEV))
+    torch.cuda.synchronize()
+    _same(ref, out, ["accept_len", "tokens", "z_tilde", "accept", "policy", "delta"])
+    # rows past the packed array's end: their mismatches get z = NaN and are rejected
+    bad = start.clone()
+    bad[B // 2] = packed.shape[0] - 2
+    out = cs.verify_block(tgt, drf, tok, packed.to(DEV), _head_dev(wl.head), 0.5, hidden_row0=bad.to(DEV))
+    torch.cuda.synchronize()
+    zt, acc, delta = out["z_tilde"].cpu(), out["accept"].cpu(), out["delta"].cpu()
+    for i in range(2, K):
+        if not delta[B // 2, i]:
+            assert torch.isnan(zt[B // 2, i]) and acc[B // 2, i] == 0
+    others = torch.arange(B) != B // 2
+    for k in ("z_tilde", "accept"):
+        x, y = ref[k].cpu()[others], out[k].cpu()[others]
+        assert torch.equal(torch.nan_to_num(x, nan=-7.0), torch.nan_to_num(y, nan=-7.0)), k
 
 
 # ------------------------------------------------------------------ speculative sampling baseline
