@@ -23,6 +23,9 @@ import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
+# Chain batches of at most this many decision slots run the head's first layer in the
+# reduction's launch (kEverySlotMax in paper_2605_24793_amd/csrc/cospec_api.hip).
+EVERY_SLOT_MAX = 256
 sys.path.insert(0, ROOT)
 
 METRIC = "verified rows/sec (B×(k+1)) and achieved HBM GB/s vs peak, V=151936 bf16"
@@ -252,6 +255,10 @@ class Step:
             self.reduced_rows = wl.B * (2 * wl.K + 1)
         self.elem = tgt.element_size()
         self.kernel = "k_vocab_reduce"
+        if not self.tree and sps_u is None and 0 < wl.B * wl.K <= EVERY_SLOT_MAX:
+            # the library runs the head's first layer over every decision slot in the
+            # reduction's launch: the timed launch holds both
+            self.kernel = "k_vocab_reduce_head (reduction + the head's first layer on every slot)"
         self.logit_bytes = self.reduced_rows * wl.V * self.elem   # algorithmic bytes of the reductions
         self.step = self.p.launch
 

@@ -46,8 +46,14 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kMinPartialSlots = 16384;   // room for a split override on small batches
 constexpr int64_t kMaxRowBytes = INT32_MAX;    // V * element bytes of one logit row
 // Chain batches with at most this many decision slots run the head's first layer on
-// every slot (slot_gemm.h) rather than on the mismatch rows after the reduction.
-constexpr int64_t kEverySlotMax = 512;
+// every slot (slot_gemm.h) rather than on the mismatch rows after the reduction, in at
+// most kEverySlotSplits k-slices (fewer partials for the finish to add; the slot GEMM's
+// extra k-steps hide behind the reduction).  Measured on MI355X, step times: B=8 K=5
+// (40 slots, d=4096, h=256) 24.5 us on the mismatch rows, 16.6 us on every slot with 32
+// slices, 14.1 with 16, 14.4 with 8; B=1 K=4 (fp32 head, d=512) 19.0 -> 10.5 us; B=64
+// K=7 (448 slots) 65.6 us on the mismatch rows, 66.8 on every slot.
+constexpr int64_t kEverySlotMax = 256;
+constexpr int32_t kEverySlotSplits = 16;
 
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -279,6 +285,7 @@ cospec_status run(const Common &c, Phase phase, int32_t *accept_len, int32_t *ou
         ha.w1 = c.head->w1; ha.b1 = c.head->b1; ha.w2 = c.head->w2; ha.b2 = c.head->b2;
         ha.d = c.head->d; ha.h = c.head->h;
         ha.ksplit = ksplit_for(m_cap, c.head);
+        if (every_slot && ha.ksplit > kEverySlotSplits) ha.ksplit = kEverySlotSplits;
         // Trees mismatch most of their slots (about 60% on the 64-tree batch: 304
         // workgroups at 8 k-slices), more than one workgroup per CU: the shallow ring
         // lets two share a CU and finish in one round (19.9 -> 13.8 us there).

@@ -228,7 +228,7 @@ __global__ __launch_bounds__(256) void k_chain_finish(FinishArgs a) {
 // then wave 0 finishes the sequence.  A head wave finds out by itself whether its slot
 // was scored (its token against the candidate of its target row, merged as wave 0
 // merges it), so that its loads wait for no other wave; when the first layer ran on
-// every slot, it scores each slot with a valid token.
+// every slot, it scores every slot.
 constexpr int kFinishWaves = 8;
 template <int HD, int PM>
 __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishArgs a) {
@@ -240,15 +240,11 @@ __global__ __launch_bounds__(64 * kFinishWaves) void k_chain_finish_head(FinishA
     if (wave == 0) {
         c = chain_prefix<PM>(a, b, lane);
     } else if (a.head_every_slot) {
-        // the first layer ran on every slot: z of each slot with a valid token, without
-        // waiting for its candidate (wave 0 uses the mismatches' only)
+        // the first layer ran on every slot: z of every slot, waiting for nothing (wave 0
+        // uses the mismatches' only)
         for (int t = wave - 1; t < K; t += waves - 1) {    // wave-uniform
-            const int64_t di = static_cast<int64_t>(b) * K + t;
-            const int tok = a.tokens[di];
-            if (tok >= 0 && tok < a.V) {
-                const float z = headz::head_z<HD>(a.hd, di, lane, a.hd.ksplit);
-                if (lane == 0) s_z[t] = z;
-            }
+            const float z = headz::head_z<HD>(a.hd, static_cast<int64_t>(b) * K + t, lane, a.hd.ksplit);
+            if (lane == 0) s_z[t] = z;
         }
     } else {
         const int64_t M = *a.hd.count_dev;                 // rows the GEMM ran on
