@@ -736,6 +736,17 @@ def test_packed_hidden_rows_whole_step(B):
     for k in ("z_tilde", "accept"):
         x, y = ref[k].cpu()[others], out[k].cpu()[others]
         assert torch.equal(torch.nan_to_num(x, nan=-7.0), torch.nan_to_num(y, nan=-7.0)), k
+    # a packed array of no rows (hidden_rows = 0 with a valid pointer): every mismatch has
+    # z = NaN and is rejected, so each round stops at its first mismatch
+    p = cs.prepare_block(tgt, drf, tok, packed.to(DEV), _head_dev(wl.head), 0.5, hidden_row0=start.to(DEV))
+    p.hidden_rows = 0
+    p.launch()
+    torch.cuda.synchronize()
+    out = p.result()
+    delta, zt, acc = out["delta"].cpu().bool(), out["z_tilde"].cpu(), out["accept"].cpu().bool()
+    assert torch.equal(acc, delta) and torch.isnan(zt[~delta]).all() and torch.isinf(zt[delta]).all()
+    first = torch.where((~delta).any(1), (~delta).int().argmax(1) + 1, torch.full((B,), K + 1))
+    assert torch.equal(out["accept_len"].cpu(), first.int())
 
 
 # ------------------------------------------------------------------ speculative sampling baseline
