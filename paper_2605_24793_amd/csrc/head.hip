@@ -587,8 +587,9 @@ int32_t head_gemm_slots(Dtype dt, bool build) {
 }
 
 hipError_t launch_slot_gemm(Dtype dt, const HeadArgs &a, hipStream_t s) {
+    if (a.m_cap <= 0 || a.m_cap > slotgemm::kMaxSlots || a.ksplit < 1) return hipErrorInvalidValue;
     const int64_t blocks = slotgemm::blocks(a);
-    if (blocks <= 0 || blocks > INT32_MAX) return hipErrorInvalidValue;
+    if (blocks > INT32_MAX) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(blocks));
     if (dt == kBF16) hipLaunchKernelGGL(k_slot_gemm<kBF16>, grid, dim3(kReduceThreads), 0, s, a);
     else hipLaunchKernelGGL(k_slot_gemm<kF32>, grid, dim3(kReduceThreads), 0, s, a);

@@ -693,9 +693,10 @@ void launch_reduce_head_t(Dtype hdt, const ReduceArgs &a, const HeadArgs &h, int
 }
 
 hipError_t launch_reduce_head(Dtype dt, Dtype hdt, const ReduceArgs &a, const HeadArgs &h, hipStream_t s) {
+    if (h.m_cap <= 0 || h.m_cap > slotgemm::kMaxSlots || h.ksplit < 1) return hipErrorInvalidValue;
     const int64_t hb = slotgemm::blocks(h);
     const int64_t units = static_cast<int64_t>(a.n_rows) * a.plan.splits;
-    if (hb <= 0 || hb + units > INT32_MAX) return hipErrorInvalidValue;
+    if (hb + units > INT32_MAX) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(hb + units));
     const int hbi = static_cast<int>(hb);
     if (dt == kBF16) {

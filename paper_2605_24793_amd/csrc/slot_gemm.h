@@ -35,6 +35,9 @@ namespace slotgemm {
 
 constexpr int kWaves = kReduceThreads / 64;   // waves per workgroup (the reduction's)
 
+// Decision slots this form takes at most (its index arithmetic is 32-bit).
+constexpr int64_t kMaxSlots = 1 << 20;
+
 // Workgroups for the a.m_cap decision slots of a.
 __host__ __device__ inline int64_t blocks(const HeadArgs &a) {
     const int64_t row_tiles = (a.m_cap + 15) / 16;
@@ -49,9 +52,8 @@ __device__ inline void run(const HeadArgs &a, int64_t w, const u32x4 *zero) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
     constexpr int KE = 64 / EB;                  // elements of a 64-byte k-step
     constexpr int VE = 16 / EB;                  // elements of a lane's 16-byte piece
-    // 32-bit index arithmetic: blocks(a) and m_cap stay far below 2^31 (the caller
-    // takes this form for small batches only), and 64-bit divisions cost registers
-    // that the reduction units of the launch would lose
+    // 32-bit index arithmetic (the launchers refuse more than kMaxSlots slots): 64-bit
+    // divisions cost registers that the reduction units of the launch would lose
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int l16 = lane & 15, g = lane >> 4;
     const int wi = static_cast<int>(w);
