@@ -45,8 +45,8 @@ __host__ __device__ inline int64_t blocks(const HeadArgs &a) {
     return row_tiles * col_groups * a.ksplit;
 }
 
-// Workgroup w of blocks(a).  zero: sixteen zero bytes in device memory, which the
-// lanes past the end of d load instead of the operands (branch-free loads).
+// Workgroup w of blocks(a).  zero: sixteen zero bytes in device memory, which a lane
+// loads instead of an operand piece past the end of its k-slice (branch-free loads).
 template <int DT>
 __device__ inline void run(const HeadArgs &a, int64_t w, const u32x4 *zero) {
     constexpr int EB = DT == kBF16 ? 2 : 4;
