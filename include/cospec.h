@@ -160,6 +160,9 @@ typedef struct {
  * (verification tokens, Delta, mismatch list; for chains taken inside the head
  * GEMM, which derives its list, and the finish), (3) the head on the mismatch
  * rows, (4) finish (draft statistics, log p_D, verdicts, first stop, emission).
+ * Chain batches of at most 256 decision slots run the head's first layer on
+ * every slot inside the reduction's launch instead, and the finish keeps the
+ * mismatches' logits (the reduce events then bracket that launch).
  */
 typedef struct {
     hipEvent_t reduce_begin;  /* if non-NULL, recorded on `stream` just before ...        */
