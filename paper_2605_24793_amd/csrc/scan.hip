@@ -42,9 +42,10 @@ struct Verdict {
 __device__ inline float log_sigmoid(float x) { return fminf(x, 0.f) - log1pf(expf(-fabsf(x))); }
 
 // Verdict of one decision slot from its state and its head logit z (read only when
-// the head scored the slot): the threshold (Eq. infer_thre), or with uniforms a
-// sampled action (u < pi).
-__device__ inline Verdict verdict(uint8_t state, bool scored, float z, float lambda, const float *pu, int64_t di) {
+// the head scored the slot): the threshold (Eq. infer_thre), or with sampled
+// arbitration (`sampled`) the action u < pi for the slot's uniform u, which the caller
+// loaded with its other inputs.
+__device__ inline Verdict verdict(uint8_t state, bool scored, float z, float lambda, bool sampled, float u) {
     Verdict v;
     if (state == kStateMatch) {
         v.pass = true; v.z_tilde = INFINITY; v.policy = 1.0f; v.logp_action = 0.0f;
@@ -55,7 +56,7 @@ __device__ inline Verdict verdict(uint8_t state, bool scored, float z, float lam
         v.pass = lambda < 0.0f; v.z_tilde = NAN; v.policy = NAN; v.logp_action = NAN;
     } else {
         const float pi = 1.0f / (1.0f + expf(-z));
-        v.pass = pu ? pu[di] < pi : pi > lambda;
+        v.pass = sampled ? u < pi : pi > lambda;
         v.z_tilde = z; v.policy = pi;
         v.logp_action = log_sigmoid(v.pass ? z : -z);
     }
@@ -79,6 +80,7 @@ struct ChainLane {
     float lpt;        // log p_T of the draft token
     int tok_d, tok_t; // draft token of slot `lane`, target candidate of row `lane`
     int tok_k;        // K = 64 only, in lane 0: the candidate of target row K (no lane of its own)
+    float u;          // sampled arbitration: the decision's uniform
 };
 
 // Merged statistics of target row tr: its candidate (the argmax, or the candidate
@@ -114,7 +116,11 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
     const PartPlan &plan = a.plan;
     const int64_t d0 = plan.n_tgt_rows + static_cast<int64_t>(b) * K;
     int tok = -1;
-    if (lane < K) tok = a.tokens[di];
+    float u = 0.f;
+    if (lane < K) {
+        tok = a.tokens[di];
+        if (a.policy_u) u = a.policy_u[di];
+    }
     // the logits at the draft token, which the reduction stored (read whatever the
     // token; used only when it is valid)
     const bool valid = tok >= 0 && tok < a.V;
@@ -142,7 +148,7 @@ __device__ inline ChainLane chain_prefix(const FinishArgs &a, int b, int lane) {
             ks = merge_row(a.partials + rk.first, rk.count);
         }
     }
-    ChainLane c{kStateMatch, false, NAN, -1, -1, -1};
+    ChainLane c{kStateMatch, false, NAN, -1, -1, -1, u};
     if (K >= 64 && lane == 0) c.tok_k = tgt_row(a, t0 + K, ks);
     if (lane <= K) {
         const int cand = tgt_row(a, tr, ts);
@@ -169,7 +175,7 @@ __device__ inline void chain_suffix(const FinishArgs &a, int b, int lane, const 
     const bool mism = lane < K && c.st != kStateMatch;
     const float lpt = c.lpt;
     if (lane < K) {
-        const Verdict v = verdict(c.st, c.scored, z, a.lambda, a.policy_u, di);
+        const Verdict v = verdict(c.st, c.scored, z, a.lambda, a.policy_u != nullptr, c.u);
         fail = !v.pass;
         if (a.z_tilde) a.z_tilde[di] = v.z_tilde;
         if (a.policy) a.policy[di] = v.policy;
@@ -284,32 +290,45 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
     __shared__ int s_child[kMaxSeqRows];
     __shared__ float s_dmax[kMaxSeqRows], s_dlogs[kMaxSeqRows];
     __shared__ int s_key[kMaxSeqRows / 64];
+    __shared__ int s_tok[kMaxSeqRows], s_cand[kMaxSeqRows];
 
-    // node n's parent, state and the draft logit of its token in the parent's row
-    int par = -1;
+    // Two memory round trips: first every input that depends on the node alone (its
+    // state, parent, token, list position, target candidate and uniform), then what
+    // those locate (the draft logit of its token in the parent's row, its head logit)
+    // together with the partials of its own draft row, merged for every node (leaves'
+    // draft rows were not reduced: their stale partials are dropped below).  Later
+    // steps read all of it from LDS.
+    int par = -1, tok = -1, pos = -1;
     uint8_t st = kStateMatch;
-    float xd = 0.f;
+    float u = 0.f;
     if (n < N) {
-        s_child[n] = 0;
         st = a.ws_state[base + n];
+        tok = a.tokens[base + n];
+        if (a.head_ran) pos = a.ws_listpos[base + n];
+        if (a.policy_u) u = a.policy_u[base + n];
+        s_cand[n] = a.ws_tgt_arg[base + n];
         if (n > 0) {
             par = a.parent[base + n];
             if (!(par >= 0 && par < n)) par = -1;
-            if (st != kStateReject && par >= 0)
-                xd = E::at(a.drf + (base + par) * a.ld_bytes, a.tokens[base + n]);
         }
         s_par[n] = par;
+        s_tok[n] = tok;
+        s_child[n] = 0;
+    }
+    float xd = 0.f, z = NAN;
+    RowStat rs{NAN, NAN, NAN, NAN, -1};
+    if (n < N) {
+        if (n > 0 && st != kStateReject && par >= 0) xd = E::at(a.drf + (base + par) * a.ld_bytes, tok);
+        if (pos >= 0) z = a.z[pos];
+        const RowParts rp = row_parts(a.plan, a.plan.n_tgt_rows + base + n);
+        rs = merge_row(a.partials + rp.first, rp.count);
     }
     __syncthreads();
     if (n < N && par >= 0) s_child[par] = 1;
     __syncthreads();
     // draft rows were reduced for nodes with a child only
     if (n < N) {
-        RowStat rs{NAN, NAN, NAN, NAN, -1};
-        if (s_child[n]) {
-            const RowParts rp = row_parts(a.plan, a.plan.n_tgt_rows + base + n);
-            rs = merge_row(a.partials + rp.first, rp.count);
-        }
+        if (!s_child[n]) rs = RowStat{NAN, NAN, NAN, NAN, -1};
         write_drf(a, base + n, rs);
         s_dmax[n] = rs.max;
         s_dlogs[n] = rs.log_s;
@@ -318,9 +337,8 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
 
     int anc = -1, dep = 0, ok = 1;
     if (n < N) {
-        const int pos = a.ws_listpos[base + n];
-        const bool scored = a.head_ran && pos >= 0;
-        const Verdict v = verdict(st, scored, scored ? a.z[pos] : NAN, a.lambda, a.policy_u, base + n);
+        const bool scored = pos >= 0;
+        const Verdict v = verdict(st, scored, z, a.lambda, a.policy_u != nullptr, u);
         if (n > 0) {
             anc = par;
             dep = 1;
@@ -377,10 +395,10 @@ __global__ __launch_bounds__(kMaxSeqRows) void k_tree_finish(FinishArgs a) {
     __syncthreads();
     const int best = s_key[0], depth = s_key[1];
     if (n < N) {
-        int tok = -1;
-        if (n < depth) tok = a.tokens[base + s_path[n + 1]];
-        else if (n == depth) tok = a.ws_tgt_arg[base + best];
-        a.out_tokens[base + n] = tok;
+        int t = -1;
+        if (n < depth) t = s_tok[s_path[n + 1]];
+        else if (n == depth) t = s_cand[best];
+        a.out_tokens[base + n] = t;
         if (a.out_path) a.out_path[base + n] = n <= depth ? s_path[n] : -1;
     }
 }
