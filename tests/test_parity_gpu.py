@@ -189,6 +189,9 @@ FUZZ = [
     # more decision slots (600 x 8) than the head GEMM's workgroups list themselves:
     # the decide kernel builds the list
     (600, 8, 257, "bf16", 0, 0, 0.5, 4.0, 1.0),
+    # either side of the 256-slot limit of the head's first layer on every slot
+    (32, 8, 4099, "bf16", 0, 0, 0.5, 4.0, 1.0),
+    (37, 7, 4099, "f32", 0, 0, 0.5, 4.0, 1.0),
 ]
 
 
