@@ -269,3 +269,14 @@ def test_static_scratch_entry_point_rejects_before_any_launch():
     assert call(-1, 7, 151936) == INVALID
     assert call(0, 7, 151936) == OK                       # empty batch: nothing to do
     assert "static buffer" in binding.status_string(-5)
+
+
+def test_bench_names_the_launch_the_library_takes():
+    # bench.py labels the timed launch of chain batches of at most EVERY_SLOT_MAX decision
+    # slots as the reduction with the head's first layer; the library's limit must agree
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = open(os.path.join(root, "paper_2605_24793_amd", "csrc", "cospec_api.hip")).read()
+    lib_max = int(re.search(r"constexpr int64_t kEverySlotMax = (\d+);", src).group(1))
+    bench_src = open(os.path.join(root, "bench.py")).read()
+    bench_max = int(re.search(r"^EVERY_SLOT_MAX = (\d+)$", bench_src, flags=re.M).group(1))
+    assert lib_max == bench_max
