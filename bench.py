@@ -149,8 +149,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline sample (0 disables it)")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the records of the peaked serving chain and the tree batch that the "
-                         "default run appends")
+                    help="skip the records of the peaked serving chain, the tree batch and the small "
+                         "and tiny chains that the default run appends")
     return ap.parse_args()
 
 
@@ -476,7 +476,7 @@ def main():
     default_mode = (args.config == 4 and not (args.sample or args.sps or args.graph or args.splits)
                     and not args.no_extras)
     if default_mode:
-        for key, cfg in (("peaked_chain", 3), ("tree", 5)):
+        for key, cfg in (("peaked_chain", 3), ("tree", 5), ("small_chain", 2), ("tiny_chain", 1)):
             print(f"[bench] workload {cfg}: timing, flushed reduction events, parity of every sequence",
                   file=sys.stderr, flush=True)
             extras[key] = extra_workload(cs, workloads, torch, np, bf16_bits, cfg, dev, args, nth)
